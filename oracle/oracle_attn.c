@@ -1,0 +1,375 @@
+/*
+ * oracle_attn.c -- plain fp64 CPU oracle for causal grouped-query
+ * scaled-dot-product attention (forward) and its split-KV decode form.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the checker the GPU path is
+ * measured against; it is loaded by the test suite, by the smoke check and
+ * by the benchmark's CPU-baseline leg, and by nothing else.  It shares no
+ * code, header, table or helper with the HIP library.
+ *
+ * What it computes.  The paper names the operation only as workloads (the
+ * "Flash Attention" and "GQA Attention" rows of Table 2, tolerances in
+ * Table 4 of Appendix A) and states the correctness criterion as agreement
+ * with an unoptimised reference (Section 3.1).  Flash/online-softmax
+ * tiling and split-KV with a log-sum-exp merge are exact rewrites of the
+ * plain definition in real arithmetic, so the oracle is the plain
+ * definition, evaluated in double precision on the exact bf16 inputs:
+ *
+ *   G   = Hq / Hkv,  g = hq / G                       (grouped heads)
+ *   L_b = clamp(kv_seqlens ? kv_seqlens[b] : Skv, 0, Skv)
+ *   off = L_b - Sq                                    (bottom-right causal)
+ *   J_i = { j : 0 <= j < L_b and (!causal or j <= i + off) }
+ *   s_j = scale * sum_d q[b,hq,i,d] * k[b,g,j,d]
+ *   m   = max_j s_j ;  w_j = exp(s_j - m) ;  l = sum_j w_j
+ *   O[b,hq,i,d] = sum_j (w_j / l) * v[b,g,j,d]
+ *   LSE[b,hq,i] = m + log(l)                          (natural log)
+ *   J_i empty  =>  O = 0, LSE = -inf
+ *
+ * The clamp of L_b follows the robustness fix described in Section 3.4
+ * (clamped lengths so that no slice size can go negative).
+ *
+ * Layouts (all contiguous, last dimension fastest):
+ *   q [B,Hq,Sq,D], k/v [B,Hkv,Skv,D] as raw bf16 bit patterns (uint16),
+ *   o [B,Hq,R,D] double, lse [B,Hq,R] double, where R = Sq or the number
+ *   of sampled rows.
+ *
+ * Pins: every function here is checked by the CPU test tier against brute
+ * force on tiny inputs, closed forms (scale 0, one key, equal V rows,
+ * causal row 0), invariants (rows of P sum to 1, GQA equals MHA with
+ * repeated K/V heads, decode equals the last prefill row, split-combine
+ * equals unsplit) and hand-derived values stored under tests/golden/.
+ *
+ * Build: plain C11, no -ffast-math, libm only (gcc -O2 -shared -fPIC).
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* bf16 is the top half of an IEEE binary32; widening is exact. */
+static double bf16_bits_to_double(uint16_t bits)
+{
+    uint32_t u = ((uint32_t)bits) << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+static int clamp_len(int len, int hi)
+{
+    if (len < 0) return 0;
+    if (len > hi) return hi;
+    return len;
+}
+
+/* ------------------------------------------------------------------ */
+/* One query row of the plain definition.                              */
+/* ------------------------------------------------------------------ */
+
+/*
+ * q_row: D bf16 values; k_head, v_head: Skv x D bf16 values of the key /
+ * value head the query head maps to.  Keys j in [0, n_valid) are the
+ * valid set J (a prefix of the key axis in every case this oracle
+ * handles: causal masking and length masking both cut a prefix).
+ * s_buf: scratch of at least n_valid doubles.
+ * Writes D outputs to o_row and the natural-log LSE to *lse_out.
+ */
+static void attend_row(const uint16_t *q_row, const uint16_t *k_head,
+                       const uint16_t *v_head, int D, int n_valid,
+                       double scale, double *s_buf, double *o_row,
+                       double *lse_out)
+{
+    if (n_valid <= 0) {
+        for (int d = 0; d < D; ++d) o_row[d] = 0.0;
+        *lse_out = -INFINITY;
+        return;
+    }
+    /* scores */
+    for (int j = 0; j < n_valid; ++j) {
+        double dot = 0.0;
+        for (int d = 0; d < D; ++d)
+            dot += bf16_bits_to_double(q_row[d]) *
+                   bf16_bits_to_double(k_head[(size_t)j * D + d]);
+        s_buf[j] = scale * dot;
+    }
+    /* max, then weights and their sum (two-pass softmax) */
+    double m = s_buf[0];
+    for (int j = 1; j < n_valid; ++j)
+        if (s_buf[j] > m) m = s_buf[j];
+    double l = 0.0;
+    for (int j = 0; j < n_valid; ++j) {
+        s_buf[j] = exp(s_buf[j] - m);
+        l += s_buf[j];
+    }
+    /* weighted sum of value rows */
+    for (int d = 0; d < D; ++d) o_row[d] = 0.0;
+    for (int j = 0; j < n_valid; ++j) {
+        double p = s_buf[j] / l;
+        for (int d = 0; d < D; ++d)
+            o_row[d] += p * bf16_bits_to_double(v_head[(size_t)j * D + d]);
+    }
+    *lse_out = m + log(l);
+}
+
+/* ------------------------------------------------------------------ */
+/* Prefill / general forward                                           */
+/* ------------------------------------------------------------------ */
+
+typedef struct {
+    const uint16_t *q, *k, *v;
+    int B, Hq, Hkv, Sq, Skv, D, causal;
+    double scale;
+    const int32_t *kv_seqlens; /* host array [B] or NULL */
+    const int32_t *rows;       /* host array [B*Hq*nrows] or NULL */
+    int nrows;                 /* rows per (b, hq) */
+    double *o, *lse;
+    /* work split */
+    long long n_items;
+    int n_threads;
+    int tid;
+} fwd_job;
+
+static void *fwd_worker(void *arg)
+{
+    fwd_job *job = (fwd_job *)arg;
+    double *s_buf = (double *)malloc(sizeof(double) * (size_t)(job->Skv > 0 ? job->Skv : 1));
+    if (!s_buf) return (void *)1;
+    const int G = job->Hq / job->Hkv;
+    const int D = job->D;
+    for (long long it = job->tid; it < job->n_items; it += job->n_threads) {
+        /* item = ((b * Hq) + hq) * nrows + r */
+        long long r = it % job->nrows;
+        long long bh = it / job->nrows;
+        int hq = (int)(bh % job->Hq);
+        int b = (int)(bh / job->Hq);
+        int g = hq / G;
+        int i = job->rows ? job->rows[it] : (int)r;
+        int L = clamp_len(job->kv_seqlens ? job->kv_seqlens[b] : job->Skv, job->Skv);
+        int n_valid = L;
+        if (job->causal) {
+            int off = L - job->Sq;
+            int last = i + off; /* largest admissible key index */
+            if (last + 1 < n_valid) n_valid = last + 1;
+            if (n_valid < 0) n_valid = 0;
+        }
+        const uint16_t *q_row = job->q + (((size_t)b * job->Hq + hq) * job->Sq + i) * D;
+        const uint16_t *k_head = job->k + ((size_t)b * job->Hkv + g) * (size_t)job->Skv * D;
+        const uint16_t *v_head = job->v + ((size_t)b * job->Hkv + g) * (size_t)job->Skv * D;
+        attend_row(q_row, k_head, v_head, D, n_valid, job->scale, s_buf,
+                   job->o + (size_t)it * D, job->lse + it);
+    }
+    free(s_buf);
+    return NULL;
+}
+
+static int run_jobs(fwd_job *proto, int n_threads)
+{
+    if (n_threads < 1) n_threads = 1;
+    if (n_threads > 256) n_threads = 256;
+    pthread_t th[256];
+    fwd_job jobs[256];
+    int started = 0, rc = 0;
+    for (int t = 0; t < n_threads; ++t) {
+        jobs[t] = *proto;
+        jobs[t].n_threads = n_threads;
+        jobs[t].tid = t;
+    }
+    if (n_threads == 1) return fwd_worker(&jobs[0]) ? -5 : 0;
+    for (int t = 0; t < n_threads; ++t) {
+        if (pthread_create(&th[t], NULL, fwd_worker, &jobs[t]) != 0) { rc = -6; break; }
+        ++started;
+    }
+    for (int t = 0; t < started; ++t) {
+        void *ret = NULL;
+        pthread_join(th[t], &ret);
+        if (ret) rc = -5;
+    }
+    return rc;
+}
+
+/*
+ * Attention forward by the plain definition above.
+ * rows == NULL: every query row, nrows must equal Sq, outputs [B,Hq,Sq,(D)].
+ * rows != NULL: rows[(b*Hq + hq)*nrows + r] is the r-th query row computed
+ *               for head (b, hq); outputs [B,Hq,nrows,(D)].
+ * Returns 0 on success, a negative code on bad arguments.
+ */
+int oracle_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                    int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                    int causal, double scale, const int32_t *kv_seqlens,
+                    const int32_t *rows, int nrows, double *o, double *lse,
+                    int n_threads)
+{
+    if (!q || !k || !v || !o || !lse) return -1;
+    if (B < 1 || Hq < 1 || Hkv < 1 || Sq < 1 || Skv < 1 || D < 1) return -2;
+    if (Hq % Hkv != 0) return -3;
+    if (!rows) nrows = Sq;
+    if (nrows < 1) return -4;
+    if (rows) {
+        for (long long t = 0; t < (long long)B * Hq * nrows; ++t)
+            if (rows[t] < 0 || rows[t] >= Sq) return -4;
+    }
+    fwd_job job;
+    memset(&job, 0, sizeof job);
+    job.q = q; job.k = k; job.v = v;
+    job.B = B; job.Hq = Hq; job.Hkv = Hkv; job.Sq = Sq; job.Skv = Skv; job.D = D;
+    job.causal = causal ? 1 : 0;
+    job.scale = scale;
+    job.kv_seqlens = kv_seqlens;
+    job.rows = rows;
+    job.nrows = nrows;
+    job.o = o; job.lse = lse;
+    job.n_items = (long long)B * Hq * nrows;
+    return run_jobs(&job, n_threads);
+}
+
+/*
+ * The normalised attention weights P[b,hq,i,j] = w_j / l (0 outside J_i),
+ * for the rows-sum-to-one pin.  p: [B,Hq,Sq,Skv] doubles.  Single thread;
+ * meant for small shapes.
+ */
+int oracle_attn_probs(const uint16_t *q, const uint16_t *k, int B, int Hq,
+                      int Hkv, int Sq, int Skv, int D, int causal,
+                      double scale, const int32_t *kv_seqlens, double *p)
+{
+    if (!q || !k || !p) return -1;
+    if (B < 1 || Hq < 1 || Hkv < 1 || Sq < 1 || Skv < 1 || D < 1) return -2;
+    if (Hq % Hkv != 0) return -3;
+    const int G = Hq / Hkv;
+    double *s = (double *)malloc(sizeof(double) * (size_t)Skv);
+    if (!s) return -5;
+    for (int b = 0; b < B; ++b)
+        for (int hq = 0; hq < Hq; ++hq)
+            for (int i = 0; i < Sq; ++i) {
+                int g = hq / G;
+                int L = clamp_len(kv_seqlens ? kv_seqlens[b] : Skv, Skv);
+                int n_valid = L;
+                if (causal) {
+                    int last = i + (L - Sq);
+                    if (last + 1 < n_valid) n_valid = last + 1;
+                    if (n_valid < 0) n_valid = 0;
+                }
+                double *prow = p + (((size_t)b * Hq + hq) * Sq + i) * (size_t)Skv;
+                for (int j = 0; j < Skv; ++j) prow[j] = 0.0;
+                if (n_valid == 0) continue;
+                const uint16_t *q_row = q + (((size_t)b * Hq + hq) * Sq + i) * D;
+                const uint16_t *k_head = k + ((size_t)b * Hkv + g) * (size_t)Skv * D;
+                for (int j = 0; j < n_valid; ++j) {
+                    double dot = 0.0;
+                    for (int d = 0; d < D; ++d)
+                        dot += bf16_bits_to_double(q_row[d]) *
+                               bf16_bits_to_double(k_head[(size_t)j * D + d]);
+                    s[j] = scale * dot;
+                }
+                double m = s[0];
+                for (int j = 1; j < n_valid; ++j) if (s[j] > m) m = s[j];
+                double l = 0.0;
+                for (int j = 0; j < n_valid; ++j) l += exp(s[j] - m);
+                for (int j = 0; j < n_valid; ++j) prow[j] = exp(s[j] - m) / l;
+            }
+    free(s);
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Decode: one query token per sequence over a length-masked cache     */
+/* ------------------------------------------------------------------ */
+
+/*
+ * q [B,Hq,D], k_cache/v_cache [B,Hkv,Smax,D], kv_seqlens [B] (required).
+ * Query (b, hq) attends to every key j < clamp(kv_seqlens[b], 0, Smax).
+ * o [B,Hq,D], lse [B,Hq].
+ */
+int oracle_decode(const uint16_t *q, const uint16_t *k_cache,
+                  const uint16_t *v_cache, int B, int Hq, int Hkv, int Smax,
+                  int D, double scale, const int32_t *kv_seqlens, double *o,
+                  double *lse, int n_threads)
+{
+    if (!kv_seqlens) return -1;
+    /* A decode step is the forward with one query row per sequence whose
+       admissible keys are the whole valid prefix: run it non-causally
+       under the length mask. */
+    return oracle_attn_fwd(q, k_cache, v_cache, B, Hq, Hkv, 1, Smax, D, 0,
+                           scale, kv_seqlens, NULL, 1, o, lse, n_threads);
+}
+
+/*
+ * Merge per-split partial results by their log-sum-exp (the split-KV
+ * decode's final step).  o_part [R,nsplit,D] holds each split's own
+ * normalised output, lse_part [R,nsplit] its natural-log LSE (-inf for an
+ * empty split).  For each r:
+ *   M = max_s lse_s ;  LSE = M + log(sum_s exp(lse_s - M))
+ *   O = sum_s exp(lse_s - LSE) * O_s
+ * and O = 0, LSE = -inf when every split is empty.
+ */
+int oracle_lse_combine(const double *o_part, const double *lse_part, int R,
+                       int nsplit, int D, double *o, double *lse)
+{
+    if (!o_part || !lse_part || !o || !lse) return -1;
+    if (R < 1 || nsplit < 1 || D < 1) return -2;
+    for (int r = 0; r < R; ++r) {
+        const double *ls = lse_part + (size_t)r * nsplit;
+        double M = -INFINITY;
+        for (int s = 0; s < nsplit; ++s) if (ls[s] > M) M = ls[s];
+        double *orow = o + (size_t)r * D;
+        for (int d = 0; d < D; ++d) orow[d] = 0.0;
+        if (M == -INFINITY) { lse[r] = -INFINITY; continue; }
+        double sum = 0.0;
+        for (int s = 0; s < nsplit; ++s) sum += exp(ls[s] - M);
+        double L = M + log(sum);
+        lse[r] = L;
+        for (int s = 0; s < nsplit; ++s) {
+            if (ls[s] == -INFINITY) continue;
+            double w = exp(ls[s] - L);
+            const double *op = o_part + ((size_t)r * nsplit + s) * D;
+            for (int d = 0; d < D; ++d) orow[d] += w * op[d];
+        }
+    }
+    return 0;
+}
+
+/*
+ * Split-KV decode carried out step by step: keys of sequence b are cut
+ * into consecutive splits of `split` keys, each split is attended on its
+ * own (plain definition restricted to the split), and the partials are
+ * merged with oracle_lse_combine.  nsplit = ceil(Smax / split).
+ * o_part [B,Hq,nsplit,D] and lse_part [B,Hq,nsplit] receive the partials.
+ */
+int oracle_decode_split(const uint16_t *q, const uint16_t *k_cache,
+                        const uint16_t *v_cache, int B, int Hq, int Hkv,
+                        int Smax, int D, double scale,
+                        const int32_t *kv_seqlens, int split, double *o_part,
+                        double *lse_part, double *o, double *lse)
+{
+    if (!q || !k_cache || !v_cache || !kv_seqlens || !o_part || !lse_part || !o || !lse)
+        return -1;
+    if (B < 1 || Hq < 1 || Hkv < 1 || Smax < 1 || D < 1 || split < 1) return -2;
+    if (Hq % Hkv != 0) return -3;
+    const int G = Hq / Hkv;
+    const int nsplit = (Smax + split - 1) / split;
+    double *s_buf = (double *)malloc(sizeof(double) * (size_t)split);
+    if (!s_buf) return -5;
+    for (int b = 0; b < B; ++b) {
+        int L = clamp_len(kv_seqlens[b], Smax);
+        for (int hq = 0; hq < Hq; ++hq) {
+            int g = hq / G;
+            const uint16_t *q_row = q + ((size_t)b * Hq + hq) * D;
+            for (int sp = 0; sp < nsplit; ++sp) {
+                int j0 = sp * split;
+                int n = L - j0;
+                if (n > split) n = split;
+                if (n < 0) n = 0;
+                const uint16_t *k_head = k_cache + (((size_t)b * Hkv + g) * Smax + j0) * D;
+                const uint16_t *v_head = v_cache + (((size_t)b * Hkv + g) * Smax + j0) * D;
+                size_t pr = ((size_t)b * Hq + hq) * nsplit + sp;
+                attend_row(q_row, k_head, v_head, D, n, scale, s_buf,
+                           o_part + pr * D, lse_part + pr);
+            }
+        }
+    }
+    free(s_buf);
+    return oracle_lse_combine(o_part, lse_part, B * Hq, nsplit, D, o, lse);
+}
+
+int oracle_version(void) { return 1; }

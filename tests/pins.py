@@ -1,0 +1,283 @@
+"""Pins for the CPU oracle: checks against facts fixed by the mathematics.
+
+Each ``pin_*`` function takes an oracle ctypes handle and raises
+``AssertionError`` when the oracle disagrees with the fact it checks.  The
+test suite runs them against the real oracle (they must pass) and against
+deliberately broken copies of the oracle built on the CPU (at least one
+must fail for every planted mistake).
+
+The facts, none of which re-types the oracle's own formula:
+  * brute force: a pure-Python evaluation that materialises the masked
+    score matrix and exponentiates without max-subtraction (tiny inputs);
+  * hand-derived closed forms stored under tests/golden/;
+  * rows of the attention weights sum to 1, and vanish where masked;
+  * all value rows equal to r  =>  every output row equals r;
+  * causal query 0 returns v_0 with LSE = scale * q_0 . k_0;
+  * a single key returns v_0 for every query;
+  * scale 0 turns softmax into a prefix mean with LSE = log(count);
+  * grouped heads equal plain multi-head attention on K/V heads repeated
+    G times in order (the contiguous grouping);
+  * a decode step equals the last row of the causal prefill over the same
+    keys;
+  * the split-KV form with its log-sum-exp merge equals the unsplit result
+    for any split length.
+"""
+from __future__ import annotations
+
+import json
+import math
+import os
+
+import numpy as np
+import torch
+
+import workloads
+from oracle import brute
+from oracle import oracle as orc
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "hand_cases.json")
+
+
+def _bits_of_floats(x) -> np.ndarray:
+    t = torch.tensor(x, dtype=torch.float32).to(torch.bfloat16)
+    # values in the golden file are exact in bf16
+    assert torch.equal(t.float(), torch.tensor(x, dtype=torch.float32)), "inexact bf16 value"
+    return workloads.bits(t)
+
+
+def _f(bits: np.ndarray) -> np.ndarray:
+    """uint16 bf16 bits -> float64, via torch (independent of the oracle)."""
+    t = torch.from_numpy(bits.astype(np.int16)).view(torch.bfloat16)
+    return t.double().numpy()
+
+
+def _rand(shape, seed, lo=-2.0, hi=2.0):
+    g = torch.Generator().manual_seed(seed)
+    x = torch.rand(shape, generator=g) * (hi - lo) + lo
+    return workloads.bits(x.to(torch.bfloat16))
+
+
+def _close(a, b, tol, what):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    both_inf = np.isinf(a) & np.isinf(b) & (np.sign(a) == np.sign(b))
+    with np.errstate(invalid="ignore"):
+        err = np.where(both_inf, 0.0, np.abs(a - b))
+    scale = np.maximum(1.0, np.where(both_inf, 1.0, np.abs(b)))
+    bad = ~(err <= tol * scale)
+    assert not bad.any(), f"{what}: max err {np.nanmax(np.where(bad, err, 0))} (tol {tol})"
+
+
+# --------------------------------------------------------------------------
+def pin_golden(lib):
+    with open(GOLDEN) as fh:
+        cases = json.load(fh)["cases"]
+    env = {"e": math.e, "exp": math.exp, "log": math.log, "sqrt": math.sqrt,
+           "inf": math.inf, "__builtins__": {}}
+    for c in cases:
+        q = _bits_of_floats(c["q"])
+        k = _bits_of_floats(c["k"])
+        v = _bits_of_floats(c["v"])
+        o, lse = orc.attn_fwd(q, k, v, causal=c["causal"], scale=c["scale"],
+                              kv_seqlens=c["kv_seqlens"], lib=lib, threads=1)
+        o_exp = np.vectorize(lambda s: float(eval(s, env)))(np.array(c["o"], dtype=object))
+        lse_exp = np.vectorize(lambda s: float(eval(s, env)))(np.array(c["lse"], dtype=object))
+        _close(o, o_exp.astype(np.float64), 1e-14, c["name"] + " O")
+        _close(lse, lse_exp.astype(np.float64), 1e-14, c["name"] + " LSE")
+
+
+BRUTE_CASES = [
+    # B, Hq, Hkv, Sq, Skv, D, causal, seqlens
+    (1, 1, 1, 5, 5, 4, True, None),
+    (1, 2, 2, 7, 7, 1, False, None),
+    (2, 4, 2, 6, 6, 4, True, None),
+    (1, 4, 1, 3, 9, 8, True, None),          # Sq < Skv, bottom-right
+    (2, 2, 1, 4, 8, 4, True, [5, 8]),        # ragged lengths
+    (2, 2, 2, 8, 8, 4, False, [3, 0]),       # an empty sequence
+    (3, 2, 1, 4, 6, 2, True, [9, -3, 2]),    # out-of-range lengths clamp
+    (1, 2, 1, 16, 16, 64, True, None),
+]
+
+
+def pin_brute_force(lib):
+    for n, (B, Hq, Hkv, Sq, Skv, D, causal, sl) in enumerate(BRUTE_CASES):
+        q = _rand((B, Hq, Sq, D), 10 + n)
+        k = _rand((B, Hkv, Skv, D), 20 + n)
+        v = _rand((B, Hkv, Skv, D), 30 + n)
+        scale = 0.7 / math.sqrt(D)
+        o, lse = orc.attn_fwd(q, k, v, causal=causal, scale=scale, kv_seqlens=sl, lib=lib,
+                              threads=2)
+        ob, lb = brute.attention(q.tolist(), k.tolist(), v.tolist(), causal=causal,
+                                 scale=scale, kv_seqlens=sl)
+        _close(o, np.array(ob), 1e-12, f"brute case {n} O")
+        _close(lse, np.array(lb), 1e-12, f"brute case {n} LSE")
+
+
+def pin_rows_sum_to_one(lib):
+    B, Hq, Hkv, Sq, Skv, D = 2, 4, 2, 9, 13, 8
+    q = _rand((B, Hq, Sq, D), 41, -3, 3)
+    k = _rand((B, Hkv, Skv, D), 42, -3, 3)
+    for causal in (True, False):
+        for sl in (None, [13, 6]):
+            p = orc.attn_probs(q, k, causal=causal, scale=0.9, kv_seqlens=sl, lib=lib)
+            for b in range(B):
+                L = Skv if sl is None else sl[b]
+                for i in range(Sq):
+                    last = i + (L - Sq) if causal else L - 1
+                    lim = max(0, min(L, last + 1))  # admissible keys are [0, lim)
+                    row = p[b, :, i]
+                    if lim == 0:
+                        assert np.all(row == 0.0), "weights on an empty row"
+                        continue
+                    s = row.sum(axis=-1)
+                    assert np.all(np.abs(s - 1.0) <= 1e-13), f"rows sum {s.min()}..{s.max()}"
+                    # weights vanish exactly outside the admissible set
+                    assert np.all(row[:, lim:] == 0.0), "weight on a masked key"
+                    assert np.all(row[:, :lim] > 0.0), "zero weight on an admissible key"
+
+
+def pin_equal_value_rows(lib):
+    B, Hq, Hkv, S, D = 1, 4, 2, 33, 16
+    q = _rand((B, Hq, S, D), 51, -4, 4)
+    k = _rand((B, Hkv, S, D), 52, -4, 4)
+    r = _rand((1, 1, 1, D), 53)
+    v = np.broadcast_to(r, (B, Hkv, S, D)).copy()
+    for causal in (True, False):
+        o, _ = orc.attn_fwd(q, k, v, causal=causal, scale=0.5, lib=lib)
+        _close(o, np.broadcast_to(_f(r), o.shape), 1e-13, "equal V rows")
+
+
+def pin_causal_row0(lib):
+    B, Hq, Hkv, S, D = 2, 4, 1, 11, 32
+    q = _rand((B, Hq, S, D), 61)
+    k = _rand((B, Hkv, S, D), 62)
+    v = _rand((B, Hkv, S, D), 63)
+    scale = 0.125
+    o, lse = orc.attn_fwd(q, k, v, causal=True, scale=scale, lib=lib)
+    qf, kf, vf = _f(q), _f(k), _f(v)
+    for b in range(B):
+        for h in range(Hq):
+            assert np.array_equal(o[b, h, 0], vf[b, 0, 0]), "causal row 0 is not v_0"
+            dot = math.fsum(qf[b, h, 0, d] * kf[b, 0, 0, d] for d in range(D))
+            _close(lse[b, h, 0], scale * dot, 1e-15, "causal row 0 LSE")
+
+
+def pin_single_key(lib):
+    B, Hq, Hkv, Sq, D = 1, 2, 2, 6, 8
+    q = _rand((B, Hq, Sq, D), 71)
+    k = _rand((B, Hkv, 1, D), 72)
+    v = _rand((B, Hkv, 1, D), 73)
+    o, lse = orc.attn_fwd(q, k, v, causal=False, scale=0.3, lib=lib)
+    qf, kf, vf = _f(q), _f(k), _f(v)
+    for h in range(Hq):
+        for i in range(Sq):
+            assert np.array_equal(o[0, h, i], vf[0, h, 0]), "single key output is not v_0"
+            dot = math.fsum(qf[0, h, i, d] * kf[0, h, 0, d] for d in range(D))
+            _close(lse[0, h, i], 0.3 * dot, 1e-15, "single key LSE")
+
+
+def pin_scale_zero(lib):
+    B, Hq, Hkv, S, D = 2, 2, 1, 19, 8
+    q = _rand((B, Hq, S, D), 81)
+    k = _rand((B, Hkv, S, D), 82)
+    v = _rand((B, Hkv, S, D), 83)
+    vf = _f(v)
+    sl = [19, 7]
+    o, lse = orc.attn_fwd(q, k, v, causal=True, scale=0.0, kv_seqlens=sl, lib=lib)
+    for b in range(B):
+        L = sl[b]
+        for i in range(S):
+            n = max(0, min(L, i + (L - S) + 1))
+            if n == 0:
+                assert np.all(o[b, :, i] == 0) and np.all(np.isneginf(lse[b, :, i]))
+                continue
+            mean = vf[b, 0, :n].mean(axis=0)
+            _close(o[b, :, i], np.broadcast_to(mean, (Hq, D)), 1e-14, "scale 0 prefix mean")
+            _close(lse[b, :, i], math.log(n), 1e-15, "scale 0 LSE")
+    o, lse = orc.attn_fwd(q, k, v, causal=False, scale=0.0, kv_seqlens=sl, lib=lib)
+    for b in range(B):
+        _close(o[b], np.broadcast_to(vf[b, 0, :sl[b]].mean(axis=0), o[b].shape), 1e-14,
+               "scale 0 non-causal mean")
+        _close(lse[b], math.log(sl[b]), 1e-15, "scale 0 non-causal LSE")
+
+
+def pin_gqa_equals_repeated_mha(lib):
+    B, Hq, Hkv, S, D = 2, 8, 2, 12, 16
+    q = _rand((B, Hq, S, D), 91)
+    k = _rand((B, Hkv, S, D), 92)
+    v = _rand((B, Hkv, S, D), 93)
+    G = Hq // Hkv
+    k_rep = np.repeat(k, G, axis=1)  # head h of the repeat is KV head h // G
+    v_rep = np.repeat(v, G, axis=1)
+    for causal in (True, False):
+        o1, l1 = orc.attn_fwd(q, k, v, causal=causal, scale=0.25, lib=lib)
+        o2, l2 = orc.attn_fwd(q, k_rep, v_rep, causal=causal, scale=0.25, lib=lib)
+        _close(o1, o2, 1e-15, "GQA vs repeated MHA O")
+        _close(l1, l2, 1e-15, "GQA vs repeated MHA LSE")
+    # and the grouping really is contiguous: perturbing KV head 1 moves query
+    # heads G..2G-1 and no other
+    k2 = k.copy()
+    k2[:, 1] = _rand((B, 1, S, D), 94)[:, 0]
+    o3, _ = orc.attn_fwd(q, k2, v, causal=True, scale=0.25, lib=lib)
+    o1, _ = orc.attn_fwd(q, k, v, causal=True, scale=0.25, lib=lib)
+    same = np.all(o1 == o3, axis=(0, 2, 3))
+    assert list(same) == [True] * G + [False] * G, f"head grouping {same}"
+
+
+def pin_decode_equals_last_prefill_row(lib):
+    B, Hq, Hkv, Smax, D = 3, 4, 2, 20, 16
+    q_all = _rand((B, Hq, Smax, D), 101)
+    kc = _rand((B, Hkv, Smax, D), 102)
+    vc = _rand((B, Hkv, Smax, D), 103)
+    lens = [20, 1, 13]
+    q_dec = np.stack([q_all[b, :, lens[b] - 1] for b in range(B)])
+    od, ld = orc.decode(q_dec, kc, vc, lens, scale=0.2, lib=lib)
+    for b in range(B):
+        L = lens[b]
+        o, lse = orc.attn_fwd(q_all[b:b + 1, :, :L], kc[b:b + 1, :, :L], vc[b:b + 1, :, :L],
+                              causal=True, scale=0.2, lib=lib)
+        _close(od[b], o[0, :, L - 1], 1e-15, "decode vs prefill row O")
+        _close(ld[b], lse[0, :, L - 1], 1e-15, "decode vs prefill row LSE")
+    # one-query prefill with a length mask is the same decode step
+    o1, l1 = orc.attn_fwd(q_dec[:, :, None, :], kc, vc, causal=True, scale=0.2,
+                          kv_seqlens=lens, lib=lib)
+    _close(o1[:, :, 0], od, 1e-15, "Sq=1 bottom-right causal vs decode")
+    _close(l1[:, :, 0], ld, 1e-15, "Sq=1 bottom-right causal vs decode LSE")
+
+
+def pin_split_combine(lib):
+    B, Hq, Hkv, Smax, D = 3, 4, 1, 37, 8
+    q = _rand((B, Hq, D), 111, -3, 3)
+    kc = _rand((B, Hkv, Smax, D), 112, -3, 3)
+    vc = _rand((B, Hkv, Smax, D), 113)
+    lens = [37, 5, 0]
+    od, ld = orc.decode(q, kc, vc, lens, scale=0.6, lib=lib)
+    for split in (1, 4, 7, 16, 37, 64):
+        o, lse, op, lp = orc.decode_split(q, kc, vc, lens, scale=0.6, split=split, lib=lib)
+        _close(o, od, 1e-13, f"split {split} O")
+        _close(lse, ld, 1e-13, f"split {split} LSE")
+        # splits past the sequence end are empty
+        nsplit = op.shape[2]
+        for b in range(B):
+            for s in range(nsplit):
+                if s * split >= lens[b]:
+                    assert np.all(np.isneginf(lp[b, :, s])) and np.all(op[b, :, s] == 0)
+
+
+def pin_row_subset(lib):
+    B, Hq, Hkv, S, D = 1, 4, 2, 40, 8
+    q = _rand((B, Hq, S, D), 121)
+    k = _rand((B, Hkv, S, D), 122)
+    v = _rand((B, Hkv, S, D), 123)
+    rows = workloads.sample_rows(B, Hq, S, 6, seed=5).numpy()
+    o_all, l_all = orc.attn_fwd(q, k, v, causal=True, scale=0.3, lib=lib)
+    o_sub, l_sub = orc.attn_fwd(q, k, v, causal=True, scale=0.3, rows=rows, lib=lib)
+    for b in range(B):
+        for h in range(Hq):
+            assert np.array_equal(o_sub[b, h], o_all[b, h, rows[b, h]])
+            assert np.array_equal(l_sub[b, h], l_all[b, h, rows[b, h]])
+
+
+ALL_PINS = [pin_golden, pin_brute_force, pin_rows_sum_to_one, pin_equal_value_rows,
+            pin_causal_row0, pin_single_key, pin_scale_zero, pin_gqa_equals_repeated_mha,
+            pin_decode_equals_last_prefill_row, pin_split_combine, pin_row_subset]

@@ -1,0 +1,143 @@
+"""Seeded synthetic inputs for the attention path.
+
+Shared by the tests (which feed both the HIP library and the CPU oracle
+with the same bits) and by the benchmark.  This module holds no attention
+arithmetic: it only draws random numbers and rounds them to bf16.
+
+Recipe (one place, so both sides see identical bits):
+  * ``torch.Generator().manual_seed(seed)`` on the CPU;
+  * prefill: draw Q, then K, then V with ``randn`` in fp32, multiply K by
+    ``k_mult`` (a power of two, so exact), round to bf16 (round to nearest
+    even);
+  * decode: draw the lengths first (integers uniform in [lmin, lmax],
+    inclusive), then q, then the K and V caches.
+
+The workloads stand in for the paper's flash / grouped-query attention
+benchmark items (Table 2), whose shapes the paper does not give; they use
+N(0,1) values, causal masking and 1/sqrt(D) scaling.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import torch
+
+
+@dataclass(frozen=True)
+class PrefillConfig:
+    name: str
+    B: int
+    Hq: int
+    Hkv: int
+    S: int
+    D: int
+    seed: int
+    k_mult: float = 1.0
+    out_fp32: bool = False
+    sample_rows: int = 0  # 0: check every row; else rows per head
+    causal: bool = True
+
+    @property
+    def scale(self) -> float:
+        return float(torch.tensor(1.0 / math.sqrt(self.D), dtype=torch.float32))
+
+    @property
+    def pairs_per_head(self) -> int:
+        # unmasked (query, key) pairs of one causal head
+        return self.S * (self.S + 1) // 2 if self.causal else self.S * self.S
+
+    @property
+    def flops(self) -> int:
+        # 4*D per unmasked pair per query head (QK^T and PV, 2 FLOP per MAC)
+        return 4 * self.D * self.pairs_per_head * self.B * self.Hq
+
+
+@dataclass(frozen=True)
+class DecodeConfig:
+    name: str
+    B: int
+    Hq: int
+    Hkv: int
+    Smax: int
+    D: int
+    seed: int
+    lmin: int = 512
+    lmax: int = 4096
+    split: int = 0  # 0: library default
+
+    @property
+    def scale(self) -> float:
+        return float(torch.tensor(1.0 / math.sqrt(self.D), dtype=torch.float32))
+
+
+# Workload table.  The first entry is the small case the oracle checks in
+# full in well under a second; the next three are prefill workloads of
+# growing length (MHA at 2k, grouped heads at 8k with a sharpened softmax,
+# grouped heads at 32k), the last one a ragged decode batch.
+CONFIGS = {
+    "c1_mha_s128_d64": PrefillConfig("c1_mha_s128_d64", B=1, Hq=2, Hkv=2, S=128, D=64,
+                                     seed=1001, out_fp32=True),
+    "c2_mha_s2k": PrefillConfig("c2_mha_s2k", B=4, Hq=16, Hkv=16, S=2048, D=128, seed=1002),
+    "c3_gqa_s8k_k2": PrefillConfig("c3_gqa_s8k_k2", B=2, Hq=32, Hkv=8, S=8192, D=128,
+                                   seed=1003, k_mult=2.0),
+    "c4_gqa_s32k": PrefillConfig("c4_gqa_s32k", B=1, Hq=32, Hkv=8, S=32768, D=128,
+                                 seed=1004, sample_rows=256),
+    "c5_decode_b64": DecodeConfig("c5_decode_b64", B=64, Hq=32, Hkv=8, Smax=4096, D=128,
+                                  seed=1005),
+}
+
+
+def _gen(seed: int) -> torch.Generator:
+    g = torch.Generator(device="cpu")
+    g.manual_seed(int(seed))
+    return g
+
+
+def prefill_inputs(B: int, Hq: int, Hkv: int, Sq: int, Skv: int, D: int, seed: int,
+                   k_mult: float = 1.0):
+    """bf16 CPU tensors q [B,Hq,Sq,D], k and v [B,Hkv,Skv,D]."""
+    g = _gen(seed)
+    q = torch.randn((B, Hq, Sq, D), generator=g, dtype=torch.float32)
+    k = torch.randn((B, Hkv, Skv, D), generator=g, dtype=torch.float32)
+    v = torch.randn((B, Hkv, Skv, D), generator=g, dtype=torch.float32)
+    if k_mult != 1.0:
+        k = k * float(k_mult)
+    return q.to(torch.bfloat16), k.to(torch.bfloat16), v.to(torch.bfloat16)
+
+
+def decode_inputs(B: int, Hq: int, Hkv: int, Smax: int, D: int, seed: int,
+                  lmin: int = 512, lmax: int = 4096):
+    """(q [B,Hq,D] bf16, k_cache/v_cache [B,Hkv,Smax,D] bf16, lens int32 [B])."""
+    g = _gen(seed)
+    lens = torch.randint(lmin, lmax + 1, (B,), generator=g, dtype=torch.int64).to(torch.int32)
+    q = torch.randn((B, Hq, D), generator=g, dtype=torch.float32)
+    kc = torch.randn((B, Hkv, Smax, D), generator=g, dtype=torch.float32)
+    vc = torch.randn((B, Hkv, Smax, D), generator=g, dtype=torch.float32)
+    return q.to(torch.bfloat16), kc.to(torch.bfloat16), vc.to(torch.bfloat16), lens
+
+
+def sample_rows(B: int, Hq: int, S: int, nrows: int, seed: int) -> torch.Tensor:
+    """int32 [B,Hq,nrows] of query rows: 0 and S-1 plus nrows-2 distinct
+    rows drawn from a per-(b, hq) seeded permutation."""
+    out = torch.empty((B, Hq, nrows), dtype=torch.int32)
+    for b in range(B):
+        for h in range(Hq):
+            g = _gen(seed * 1_000_003 + b * 1009 + h)
+            perm = torch.randperm(S, generator=g)
+            extra = [int(x) for x in perm.tolist() if 0 < int(x) < S - 1][: nrows - 2]
+            rows = sorted([0, S - 1] + extra)
+            out[b, h] = torch.tensor(rows, dtype=torch.int32)
+    return out
+
+
+def config_inputs(cfg):
+    """Inputs of a table entry."""
+    if isinstance(cfg, DecodeConfig):
+        return decode_inputs(cfg.B, cfg.Hq, cfg.Hkv, cfg.Smax, cfg.D, cfg.seed, cfg.lmin, cfg.lmax)
+    return prefill_inputs(cfg.B, cfg.Hq, cfg.Hkv, cfg.S, cfg.S, cfg.D, cfg.seed, cfg.k_mult)
+
+
+def bits(t: torch.Tensor):
+    """bf16 tensor -> numpy uint16 of the same bits (for the oracle)."""
+    return t.contiguous().view(torch.int16).numpy().view("uint16")
