@@ -1,0 +1,193 @@
+"""Fused causal grouped-query attention for MI355X (gfx950).
+
+Thin ctypes binding of ``libmk_attn.so`` (C ABI in ``include/mk_attn.h``).
+The functions named like the C entry points take torch tensors where the C
+call takes device pointers and otherwise mirror its argument list; they do
+argument marshalling only -- every step of the computation runs in the HIP
+kernels.  ``fwd`` and ``decode`` are conveniences that allocate the outputs
+with torch and call those entry points.
+
+There is no fallback: when the library is missing, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libmk_attn.so")
+
+MK_STATUS = {0: "MK_OK", 1: "MK_ERR_NULL", 2: "MK_ERR_SHAPE", 3: "MK_ERR_UNSUPPORTED",
+             4: "MK_ERR_ALIGN", 5: "MK_ERR_WORKSPACE", 6: "MK_ERR_HIP", 7: "MK_ERR_ARG"}
+
+# every symbol include/mk_attn.h declares
+EXPORTS = ("mk_attn_fwd", "mk_attn_fwd_o32", "mk_attn_decode_workspace_bytes",
+           "mk_attn_decode", "mk_attn_decode_default_split", "mk_status_str",
+           "mk_attn_version")
+
+
+class MkAttnError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(msg)
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: the HIP library has not been built "
+                "(run __graft_entry__.build() or python paper_2609_04523_amd/build.py)")
+        h = ctypes.CDLL(LIB_PATH)
+        vp, i, f, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+        h.mk_attn_fwd.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, vp, vp]
+        h.mk_attn_fwd.restype = i
+        h.mk_attn_fwd_o32.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, vp, vp]
+        h.mk_attn_fwd_o32.restype = i
+        h.mk_attn_decode_workspace_bytes.argtypes = [i, i, i, i, i]
+        h.mk_attn_decode_workspace_bytes.restype = sz
+        h.mk_attn_decode.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, f, vp, i, vp, sz, vp]
+        h.mk_attn_decode.restype = i
+        h.mk_attn_decode_default_split.argtypes = []
+        h.mk_attn_decode_default_split.restype = i
+        h.mk_status_str.argtypes = [i]
+        h.mk_status_str.restype = ctypes.c_char_p
+        h.mk_attn_version.argtypes = []
+        h.mk_attn_version.restype = i
+        _lib = h
+    return _lib
+
+
+def mk_status_str(status: int) -> str:
+    return lib().mk_status_str(int(status)).decode()
+
+
+def mk_attn_version() -> int:
+    return lib().mk_attn_version()
+
+
+def mk_attn_decode_default_split() -> int:
+    return lib().mk_attn_decode_default_split()
+
+
+def mk_attn_decode_workspace_bytes(B: int, Hq: int, Smax: int, D: int, split: int = 0) -> int:
+    return lib().mk_attn_decode_workspace_bytes(B, Hq, Smax, D, split)
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise MkAttnError(rc, mk_status_str(rc))
+
+
+def _ptr(t):
+    """Device pointer of a tensor (None -> NULL).  Plain ints pass through."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def mk_attn_fwd(q, k, v, o, lse, B, Hq, Hkv, Sq, Skv, D, causal, scale, kv_seqlens=None,
+                stream=None):
+    _check(lib().mk_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, Hq, Hkv, Sq,
+                             Skv, D, int(causal), float(scale), _ptr(kv_seqlens),
+                             _stream(stream)))
+
+
+def mk_attn_fwd_o32(q, k, v, o, lse, B, Hq, Hkv, Sq, Skv, D, causal, scale, kv_seqlens=None,
+                    stream=None):
+    _check(lib().mk_attn_fwd_o32(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, Hq, Hkv,
+                                 Sq, Skv, D, int(causal), float(scale), _ptr(kv_seqlens),
+                                 _stream(stream)))
+
+
+def mk_attn_decode(q, k_cache, v_cache, o, lse, B, Hq, Hkv, Smax, D, scale, kv_seqlens,
+                   split, workspace, workspace_bytes, stream=None):
+    _check(lib().mk_attn_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(o), _ptr(lse), B,
+                                Hq, Hkv, Smax, D, float(scale), _ptr(kv_seqlens), int(split),
+                                _ptr(workspace), int(workspace_bytes), _stream(stream)))
+
+
+# ---------------------------------------------------------------------------
+# conveniences: allocate outputs with torch, then call the entry points above
+# ---------------------------------------------------------------------------
+def _require(t, name, dtype, ndim):
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a device tensor")
+    if t.dtype != dtype or t.dim() != ndim or not t.is_contiguous():
+        raise TypeError(f"{name} must be a contiguous {ndim}-d {dtype} tensor")
+
+
+def fwd(q, k, v, *, causal: bool = True, scale: float | None = None, kv_seqlens=None,
+        out_fp32: bool = False, with_lse: bool = True, stream=None):
+    """q [B,Hq,Sq,D], k/v [B,Hkv,Skv,D] bf16 -> (o [B,Hq,Sq,D], lse [B,Hq,Sq] or None)."""
+    import torch
+    _require(q, "q", torch.bfloat16, 4)
+    _require(k, "k", torch.bfloat16, 4)
+    _require(v, "v", torch.bfloat16, 4)
+    B, Hq, Sq, D = q.shape
+    _, Hkv, Skv, _ = k.shape
+    if scale is None:
+        scale = D ** -0.5
+    if kv_seqlens is not None:
+        _require(kv_seqlens, "kv_seqlens", torch.int32, 1)
+    o = torch.empty((B, Hq, Sq, D), device=q.device,
+                    dtype=torch.float32 if out_fp32 else torch.bfloat16)
+    lse = torch.empty((B, Hq, Sq), device=q.device, dtype=torch.float32) if with_lse else None
+    entry = mk_attn_fwd_o32 if out_fp32 else mk_attn_fwd
+    entry(q, k, v, o, lse, B, Hq, Hkv, Sq, Skv, D, causal, scale, kv_seqlens, stream)
+    return o, lse
+
+
+def decode(q, k_cache, v_cache, kv_seqlens, *, scale: float | None = None, split: int = 0,
+           workspace=None, with_lse: bool = True, stream=None):
+    """q [B,Hq,D], caches [B,Hkv,Smax,D] bf16, kv_seqlens int32 [B] -> (o, lse)."""
+    import torch
+    _require(q, "q", torch.bfloat16, 3)
+    _require(k_cache, "k_cache", torch.bfloat16, 4)
+    _require(v_cache, "v_cache", torch.bfloat16, 4)
+    _require(kv_seqlens, "kv_seqlens", torch.int32, 1)
+    B, Hq, D = q.shape
+    _, Hkv, Smax, _ = k_cache.shape
+    if scale is None:
+        scale = D ** -0.5
+    need = mk_attn_decode_workspace_bytes(B, Hq, Smax, D, split)
+    if workspace is None:
+        workspace = torch.empty(need, device=q.device, dtype=torch.uint8)
+    o = torch.empty((B, Hq, D), device=q.device, dtype=torch.bfloat16)
+    lse = torch.empty((B, Hq), device=q.device, dtype=torch.float32) if with_lse else None
+    mk_attn_decode(q, k_cache, v_cache, o, lse, B, Hq, Hkv, Smax, D, scale, kv_seqlens, split,
+                   workspace, workspace.numel() * workspace.element_size(), stream)
+    return o, lse
+
+
+def decode_partials(workspace, B: int, Hq: int, Smax: int, D: int, split: int = 0):
+    """Views of a decode workspace: (o_part [B,Hq,nsplit,D], lse_part [B,Hq,nsplit]) fp32.
+
+    Splits at or past a sequence's end are not written by the library."""
+    import torch
+    if split == 0:
+        split = mk_attn_decode_default_split()
+    nsplit = -(-Smax // split)
+    n_o = B * Hq * nsplit * D
+    lse_off = -(-(n_o * 4) // 256) * 256
+    flat = workspace.view(torch.uint8)
+    o_part = flat[: n_o * 4].view(torch.float32).view(B, Hq, nsplit, D)
+    lse_part = flat[lse_off: lse_off + B * Hq * nsplit * 4].view(torch.float32).view(B, Hq, nsplit)
+    return o_part, lse_part

@@ -1,0 +1,137 @@
+"""C-ABI boundary on the CPU: the library loads, exports what the header
+declares, and rejects every invalid argument on the host before any HIP
+call (so none of these calls touches a GPU)."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2609_04523_amd as mk
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                      "mk_attn.h")
+
+# fake device addresses: never dereferenced, only checked for NULL/alignment
+P = 0x10000
+P_ODD = 0x10002
+F = ctypes.c_void_p
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(mk.LIB_PATH):
+        from paper_2609_04523_amd import build
+        build.build()
+    return mk.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_]+\s*\*?\s*(mk_[a-z0-9_]+)\s*\(",
+                                 text, re.M)))
+
+
+def test_header_declares_the_python_exports():
+    assert sorted(mk.EXPORTS) == declared_functions()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_version_and_status_strings(lib):
+    assert mk.mk_attn_version() == 1
+    names = ["MK_OK", "MK_ERR_NULL", "MK_ERR_SHAPE", "MK_ERR_UNSUPPORTED", "MK_ERR_ALIGN",
+             "MK_ERR_WORKSPACE", "MK_ERR_HIP", "MK_ERR_ARG"]
+    for code, name in enumerate(names):
+        assert mk.mk_status_str(code).startswith(name)
+        assert mk.MK_STATUS[code] == name
+    assert "UNKNOWN" in mk.mk_status_str(99)
+    assert "UNKNOWN" in mk.mk_status_str(-1)
+
+
+def fwd_rc(lib, *, q=P, k=P, v=P, o=P, lse=None, B=1, Hq=2, Hkv=1, Sq=8, Skv=8, D=128,
+           causal=1, scale=0.125, seqlens=None, o32=False):
+    fn = lib.mk_attn_fwd_o32 if o32 else lib.mk_attn_fwd
+    return fn(q, k, v, o, lse, B, Hq, Hkv, Sq, Skv, D, causal, scale, seqlens, None)
+
+
+@pytest.mark.parametrize("o32", [False, True])
+def test_fwd_validation(lib, o32):
+    r = lambda **kw: fwd_rc(lib, o32=o32, **kw)
+    for name in ("q", "k", "v", "o"):
+        assert r(**{name: None}) == 1
+    for name in ("B", "Hq", "Hkv", "Sq", "Skv"):
+        assert r(**{name: 0}) == 2
+        assert r(**{name: -3}) == 2
+    assert r(D=0) == 2
+    assert r(Hq=3, Hkv=2) == 2
+    for D in (32, 96, 256, 80):
+        assert r(D=D) == 3
+    for name in ("q", "k", "v", "o"):
+        assert r(**{name: P_ODD}) == 4
+    assert r(lse=P + 2) == 4
+    assert r(seqlens=P + 1) == 4
+    assert r(causal=2) == 7
+    assert r(causal=-1) == 7
+    for s in (math.inf, -math.inf, math.nan):
+        assert r(scale=s) == 7
+    # too many workgroups for one launch
+    assert r(B=65536, Hq=65536, Hkv=1, Sq=1) == 2
+
+
+def dec_rc(lib, *, q=P, kc=P, vc=P, o=P, lse=None, B=2, Hq=8, Hkv=2, Smax=512, D=128,
+           scale=0.1, seqlens=P, split=0, ws=P, ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = lib.mk_attn_decode_workspace_bytes(max(B, 1), max(Hq, 1), max(Smax, 1),
+                                                      D, max(split, 0))
+    return lib.mk_attn_decode(q, kc, vc, o, lse, B, Hq, Hkv, Smax, D, scale, seqlens, split, ws,
+                              ws_bytes, None)
+
+
+def test_decode_validation(lib):
+    for name in ("q", "kc", "vc", "o", "seqlens"):
+        assert dec_rc(lib, **{name: None}) == 1
+    for name in ("B", "Hq", "Hkv", "Smax"):
+        assert dec_rc(lib, **{name: 0}) == 2
+    assert dec_rc(lib, Hq=6, Hkv=4) == 2
+    assert dec_rc(lib, B=70000) == 2
+    assert dec_rc(lib, D=96) == 3
+    assert dec_rc(lib, Hq=34, Hkv=2) == 3  # group of 17 query heads
+    assert dec_rc(lib, split=-1, ws_bytes=1 << 30) == 7
+    assert dec_rc(lib, scale=math.nan) == 7
+    for name in ("q", "kc", "vc", "o"):
+        assert dec_rc(lib, **{name: P_ODD}) == 4
+    assert dec_rc(lib, seqlens=P + 2) == 4
+    assert dec_rc(lib, lse=P + 1) == 4
+    assert dec_rc(lib, ws=None) == 5
+    need = lib.mk_attn_decode_workspace_bytes(2, 8, 512, 128, 0)
+    assert dec_rc(lib, ws_bytes=need - 1) == 5
+    assert dec_rc(lib, ws=P + 16) == 4  # workspace must be 256-byte aligned
+
+
+def test_decode_workspace_size(lib):
+    split = mk.mk_attn_decode_default_split()
+    assert split > 0
+    B, Hq, Smax, D = 64, 32, 4096, 128
+    nsplit = -(-Smax // split)
+    o_bytes = B * Hq * nsplit * D * 4
+    lse_bytes = B * Hq * nsplit * 4
+    rnd = lambda x: -(-x // 256) * 256
+    assert lib.mk_attn_decode_workspace_bytes(B, Hq, Smax, D, 0) == rnd(o_bytes) + rnd(lse_bytes)
+    assert lib.mk_attn_decode_workspace_bytes(B, Hq, Smax, D, split) == \
+        lib.mk_attn_decode_workspace_bytes(B, Hq, Smax, D, 0)
+    # split 1000 -> 5 splits over 4096 keys
+    assert lib.mk_attn_decode_workspace_bytes(1, 1, 4096, 64, 1000) == rnd(5 * 64 * 4) + rnd(5 * 4)
+    assert lib.mk_attn_decode_workspace_bytes(0, 1, 1, 64, 0) == 0
+    assert lib.mk_attn_decode_workspace_bytes(1, 1, 1, 64, -1) == 0
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(mk, "_lib", None)
+    monkeypatch.setattr(mk, "LIB_PATH", str(tmp_path / "libmk_attn.so"))
+    with pytest.raises(RuntimeError, match="has not been built"):
+        mk.lib()
