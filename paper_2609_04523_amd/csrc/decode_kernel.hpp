@@ -1,12 +1,15 @@
 // decode_kernel.hpp -- split-KV decode attention for gfx950.
 //
-// Kernel 1 (dec_split_kernel): one workgroup per (split, kv head, batch).
-// The G = Hq/Hkv query heads of the kv head are the columns of one
-// 16x16x32 MFMA block, so every cached K/V byte is read once for all of
-// them.  Keys of the split stream through LDS in coalesced 16-byte loads;
-// each of the 4 waves takes 32 keys of a 128-key tile with its own online
-// softmax state, and the waves are merged in LDS at the end.  The kernel
-// writes the split's normalised output and its natural-log LSE.
+// Kernel 1 (dec_split_kernel): one single-wave workgroup per (split, kv
+// head, batch).  The G = Hq/Hkv query heads of the kv head are the columns
+// of 16x16x32 MFMA blocks, so every cached K/V byte is read once for all
+// of them.  The wave streams its split 32 keys per stage, PREFETCH stages
+// ahead: K straight from HBM into registers, already in the MFMA A-operand
+// layout, and V from HBM into a private LDS ring (global_load_lds_dwordx4)
+// from which the transposing read builds the V^T operand.  No barrier is
+// needed since no other wave touches its LDS.  The wave keeps its own
+// online-softmax state and writes the split's normalised output and its
+// natural-log LSE.
 //
 // Kernel 2 (dec_combine_kernel): per (batch, query head), merge the splits
 // by their log-sum-exp: LSE = log sum_s exp(LSE_s), O = sum_s
@@ -14,9 +17,13 @@
 // and are not read.
 #pragma once
 
+#include <type_traits>
+
 #include "mk_common.hpp"
 
 namespace mk {
+
+constexpr float kDecRescaleSlack = 8.0f;
 
 struct DecArgs {
   const uint16_t* q;
@@ -40,45 +47,65 @@ struct CombArgs {
 
 template <int D>
 struct DecShape {
-  static constexpr int WAVES = 4;
-  static constexpr int THREADS = WAVES * 64;
-  static constexpr int BN = 128;                       // keys per LDS tile, 32 per wave
+  static constexpr int BN = 32;                        // keys per stage
+  static constexpr int PREFETCH = 3;                   // stages in flight ahead of use
+  static constexpr int VSLOTS = PREFETCH + 1;          // V ring slots in LDS
   static constexpr int CHUNKS = D / 8;                 // 16-byte chunks per row
-  static constexpr int LOADS = BN * CHUNKS / THREADS;  // per thread per tensor
-  static constexpr int VT_STRIDE = BN + 8;             // bf16 per transposed V row
+  static constexpr int ROWS_PER_KB = 512 / D;          // rows per 1 KB wave load
+  static constexpr int VBLOCKS = BN * D * 2 / 1024;    // 1 KB V loads per stage
   static constexpr int KSTEPS = D / 32;                // 16x16x32 steps over the head dim
+  static constexpr int KLOADS = 2 * KSTEPS;            // 16-byte K loads per lane per stage
+  static constexpr int LOADS_PER_STAGE = VBLOCKS + KLOADS;
   static constexpr int DBLK = D / 16;                  // 16-row blocks of O^T
+  static constexpr int STAGE_ELEMS = BN * D;           // bf16 per V stage
 };
 
 template <int D>
-__global__ __launch_bounds__(256, 2) void dec_split_kernel(DecArgs a) {
+__global__ __launch_bounds__(64) void dec_split_kernel(DecArgs a) {
   using S = DecShape<D>;
   constexpr int BN = S::BN;
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[BN * D];
-  __shared__ __attribute__((aligned(16))) uint16_t vt_lds[D * S::VT_STRIDE];
-  __shared__ float w_m[S::WAVES][16], w_l[S::WAVES][16];
+  __shared__ __attribute__((aligned(1024))) uint16_t v_lds[S::VSLOTS][S::STAGE_ELEMS];
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int c16 = lane & 15;  // MFMA column (query head of the group) / row
+  const int lane = threadIdx.x;
+  const int c16 = lane & 15;  // MFMA column (query head of the group) / row (key)
   const int gq = lane >> 4;   // MFMA k-group
 
-  const int sidx = blockIdx.x;
-  const int g = blockIdx.y;
-  const int b = blockIdx.z;
+  // Work item order: the split index varies slowest.  Workgroups are
+  // dealt round-robin to the 8 XCDs, so the XCD of an item is set by its
+  // (batch, kv head) pair and not by the split index; the low splits,
+  // which every sequence has, are spread over all XCDs instead of piling
+  // onto the few that a split-fastest order would give them.
+  const int n_gb = a.B * a.Hkv;
+  const int sidx = blockIdx.x / n_gb;
+  const int gb = blockIdx.x - sidx * n_gb;
+  const int b = gb / a.Hkv;
+  const int g = gb - b * a.Hkv;
   const int G = a.Hq / a.Hkv;
   const int L = clamp_len(a.kv_seqlens[b], a.Smax);
   const int k_begin = sidx * a.split;
   if (k_begin >= L) return;  // empty split: nothing to write, the merge skips it
   const int k_end = min(k_begin + a.split, L);
   const int n_t = (k_end - k_begin + BN - 1) / BN;
+  // The split's stages are walked starting at a per-workgroup rotation, so
+  // that workgroups running together do not stream addresses that agree
+  // modulo large powers of two (the caches of all heads start on such
+  // boundaries), which would pile their traffic onto the same HBM
+  // channels.  The order of the stages does not change the result beyond
+  // rounding.
+  const int rot = (int)(((unsigned)(b * 131 + g * 37 + sidx * 7)) % (unsigned)n_t);
+  auto stage_key0 = [&](int t) {
+    int u = t + rot;
+    if (u >= n_t) u -= n_t;
+    return k_begin + u * BN;
+  };
 
   const size_t kv_off = ((size_t)b * a.Hkv + g) * (size_t)a.Smax * D;
   const uint16_t* __restrict__ kg = a.kc + kv_off;
   const uint16_t* __restrict__ vg = a.vc + kv_off;
 
-  // Q^T fragments: column c16 is query head g*G + c16 (zero when c16 >= G).
+  // Q^T fragments: column c16 is query head g*G + c16 (zero when c16 >= G);
+  // loaded before any cache traffic so that waiting for them waits for
+  // nothing else.
   bf16x8 qf[S::KSTEPS];
 #pragma unroll
   for (int s = 0; s < S::KSTEPS; ++s) {
@@ -89,39 +116,45 @@ __global__ __launch_bounds__(256, 2) void dec_split_kernel(DecArgs a) {
     qf[s] = as_bf16x8(u);
   }
 
-  u32x4 kreg[S::LOADS], vreg[S::LOADS];
-  auto load_tile = [&](int t) {
+  // Stage t: V rows -> LDS slot t % VSLOTS (row blk*ROWS_PER_KB + l/CHUNKS,
+  // chunks XOR-swizzled), then K rows -> registers: lane (row c16 of key
+  // block kb, k-group gq) takes k[key][32 s + 8 gq .. +7].  Rows past the
+  // split end re-read its last row (the mask zeroes their weight), so no
+  // load leaves the valid keys [0, L).
+  u32x4 kreg[S::PREFETCH + 1][2][S::KSTEPS];
+  auto issue = [&](int t, auto slot_tag) {
+    constexpr int SLOT = decltype(slot_tag)::value;
+    const int vslot = t % S::VSLOTS;
 #pragma unroll
-    for (int p = 0; p < S::LOADS; ++p) {
-      const int c = tid + p * S::THREADS;
-      const int key = c / S::CHUNKS;
-      const int ch = c % S::CHUNKS;
-      const int gk = k_begin + t * BN + key;
-      u32x4 zk = {0u, 0u, 0u, 0u}, zv = {0u, 0u, 0u, 0u};
-      if (gk < k_end) {
-        zk = *reinterpret_cast<const u32x4*>(kg + (size_t)gk * D + ch * 8);
-        zv = *reinterpret_cast<const u32x4*>(vg + (size_t)gk * D + ch * 8);
-      }
-      kreg[p] = zk;
-      vreg[p] = zv;
+    for (int blk = 0; blk < S::VBLOCKS; ++blk) {
+      const int row = blk * S::ROWS_PER_KB + lane / S::CHUNKS;
+      const int ch = (lane % S::CHUNKS) ^ chunk_swz<D>(row);
+      const int gk = min(stage_key0(t) + row, k_end - 1);
+      load_lds16(vg + (size_t)gk * D + ch * 8, &v_lds[vslot][blk * 512]);
+    }
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const int gk = min(stage_key0(t) + kb * 16 + c16, k_end - 1);
+#pragma unroll
+      for (int s = 0; s < S::KSTEPS; ++s)
+        kreg[SLOT][kb][s] = *reinterpret_cast<const u32x4*>(kg + (size_t)gk * D + s * 32 + gq * 8);
     }
   };
-  auto store_tile = [&]() {
+
+  // Lane-constant LDS offsets of the transposing V reads: rows 4 gq + i/4
+  // (+ 16), columns 16 db + 4 (i % 4), i = lane % 16.
+  const int tr_row = 4 * gq + (c16 >> 2);
+  const int tr_col = 4 * (c16 & 3);
+  uint32_t v_addr[S::DBLK][2];
 #pragma unroll
-    for (int p = 0; p < S::LOADS; ++p) {
-      const int c = tid + p * S::THREADS;
-      const int key = c / S::CHUNKS;
-      const int ch = c % S::CHUNKS;
-      *reinterpret_cast<u32x4*>(&k_lds[key * D + ((ch ^ (key & (S::CHUNKS - 1))) * 8)]) =
-          kreg[p];
-      const u32x4 vv = vreg[p];
+  for (int db = 0; db < S::DBLK; ++db)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        vt_lds[(ch * 8 + 2 * i) * S::VT_STRIDE + key] = (uint16_t)(vv[i] & 0xffffu);
-        vt_lds[(ch * 8 + 2 * i + 1) * S::VT_STRIDE + key] = (uint16_t)(vv[i] >> 16);
-      }
+    for (int hh = 0; hh < 2; ++hh) {
+      const int r = tr_row + 16 * hh;
+      const int col = db * 16 + tr_col;
+      v_addr[db][hh] = 2u * (r * D + (((col >> 3) ^ chunk_swz<D>(r)) << 3) + (col & 7));
     }
-  };
+  const uint32_t v_lds0 = lds_addr(&v_lds[0][0]);
 
   float m_run = kNegInf, l_run = 0.f;
   f32x4 o_acc[S::DBLK];
@@ -129,136 +162,176 @@ __global__ __launch_bounds__(256, 2) void dec_split_kernel(DecArgs a) {
   for (int db = 0; db < S::DBLK; ++db)
 #pragma unroll
     for (int r = 0; r < 4; ++r) o_acc[db][r] = 0.f;
+  const float c = a.scale_log2;
 
-  load_tile(0);
-  for (int t = 0; t < n_t; ++t) {
-    store_tile();
-    __syncthreads();
-    if (t + 1 < n_t) load_tile(t + 1);
-    const int kw0 = k_begin + t * BN + wave * 32;  // first key of this wave
-    if (kw0 < k_end) {
-      // S^T = K Q^T for the wave's 32 keys (two 16-key blocks).
-      f32x4 sacc[2];
+  // One stage: K from register slot SLOT, V from LDS slot t % VSLOTS.
+  auto consume = [&](int t, auto slot_tag) {
+    constexpr int SLOT = decltype(slot_tag)::value;
+    const int key0 = stage_key0(t);
+    f32x4 sacc[2];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) sacc[kb][r] = 0.f;
-        const int row = wave * 32 + kb * 16 + c16;
+      for (int r = 0; r < 4; ++r) sacc[kb][r] = 0.f;
 #pragma unroll
-        for (int s = 0; s < S::KSTEPS; ++s) {
-          const int ch = 4 * s + gq;
-          const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(
-              &k_lds[row * D + ((ch ^ (row & (S::CHUNKS - 1))) * 8)]));
-          sacc[kb] = mfma16(kf, qf[s], sacc[kb]);
-        }
+      for (int s = 0; s < S::KSTEPS; ++s)
+        sacc[kb] = mfma16(as_bf16x8(kreg[SLOT][kb][s]), qf[s], sacc[kb]);
+    }
+    // Online softmax over the column (query head); lane holds keys
+    // 16 kb + 4 gq + r.
+    float mx = kNegInf;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float x = sacc[kb][r] * c;
+        if (key0 + kb * 16 + 4 * gq + r >= k_end) x = kNegInf;
+        sacc[kb][r] = x;
+        mx = fmaxf(mx, x);
       }
-      // Online softmax over the column (query head); lane holds 8 keys.
-      float mx = kNegInf;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float x = sacc[kb][r] * a.scale_log2;
-          if (kw0 + kb * 16 + 4 * gq + r >= k_end) x = kNegInf;
-          sacc[kb][r] = x;
-          mx = fmaxf(mx, x);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    mx = max_xor32(max_xor16(mx));
+    if (__ballot(mx > m_run + kDecRescaleSlack)) {
       const float m_new = fmaxf(m_run, mx);
-      const float m_use = (m_new == kNegInf) ? 0.f : m_new;
-      const float alpha = fast_exp2(m_run - m_use);
-      float rs = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float p = fast_exp2(sacc[kb][r] - m_use);
-          sacc[kb][r] = p;
-          rs += p;
-        }
-      rs += __shfl_xor(rs, 16, 64);
-      rs += __shfl_xor(rs, 32, 64);
-      l_run = l_run * alpha + rs;
+      const float alpha = (m_new == kNegInf) ? 1.f : fast_exp2(m_run - m_new);
       m_run = m_new;
-      // P^T: k-group gq holds keys {4gq..4gq+3} and {16+4gq..16+4gq+3} of the wave.
-      const bf16x8 pf = to_bf16x8(sacc[0][0], sacc[0][1], sacc[0][2], sacc[0][3], sacc[1][0],
-                                  sacc[1][1], sacc[1][2], sacc[1][3]);
+      l_run *= alpha;
 #pragma unroll
-      for (int db = 0; db < S::DBLK; ++db) {
-        const int d = db * 16 + c16;
-        const uint16_t* vp = &vt_lds[d * S::VT_STRIDE + wave * 32 + 4 * gq];
-        const u32x2 lo = *reinterpret_cast<const u32x2*>(vp);
-        const u32x2 hi = *reinterpret_cast<const u32x2*>(vp + 16);
-        const u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
+      for (int db = 0; db < S::DBLK; ++db)
 #pragma unroll
         for (int r = 0; r < 4; ++r) o_acc[db][r] *= alpha;
-        o_acc[db] = mfma16(as_bf16x8(w), pf, o_acc[db]);
+    }
+    const float m_use = (m_run == kNegInf) ? 0.f : m_run;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float p = fast_exp2(sacc[kb][r] - m_use);
+        sacc[kb][r] = p;
+        l_run += p;
+      }
+    // P^T: k-group gq holds keys {4gq..4gq+3} and {16+4gq..16+4gq+3}.
+    const bf16x8 pf = to_bf16x8(sacc[0][0], sacc[0][1], sacc[0][2], sacc[0][3], sacc[1][0],
+                                sacc[1][1], sacc[1][2], sacc[1][3]);
+    const uint32_t vb = v_lds0 + (t % S::VSLOTS) * (S::STAGE_ELEMS * 2);
+#pragma unroll
+    for (int db0 = 0; db0 < S::DBLK; db0 += 2) {
+      u32x2 vr[2][2];
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) vr[j][hh] = lds_read_tr16_async(vb + v_addr[db0 + j][hh]);
+      lds_wait4(vr[0][0], vr[0][1], vr[1][0], vr[1][1]);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const u32x4 w = {vr[j][0][0], vr[j][0][1], vr[j][1][0], vr[j][1][1]};
+        o_acc[db0 + j] = mfma16(as_bf16x8(w), pf, o_acc[db0 + j]);
       }
     }
-    __syncthreads();
+  };
+
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  static_assert(S::PREFETCH == 3, "register ring below is written for 3 stages ahead");
+  if (0 < n_t) issue(0, I0());
+  if (1 < n_t) issue(1, I1());
+  if (2 < n_t) issue(2, I2());
+  // Register slot of stage t is t % 4; the loop is unrolled by 4 so every
+  // slot index is a compile-time constant.
+  auto step = [&](int t, auto use_tag, auto load_tag) {
+    if (t + S::PREFETCH < n_t) {
+      issue(t + S::PREFETCH, load_tag);
+      wait_vmcnt<S::PREFETCH * S::LOADS_PER_STAGE>();
+    } else {
+      wait_vmcnt<0>();
+    }
+    consume(t, use_tag);
+  };
+  for (int t = 0; t < n_t; t += 4) {
+    step(t, I0(), I3());
+    if (t + 1 < n_t) step(t + 1, I1(), I0());
+    if (t + 2 < n_t) step(t + 2, I2(), I1());
+    if (t + 3 < n_t) step(t + 3, I3(), I2());
   }
 
-  // Merge the four waves' states through LDS (reusing the K tile area).
-  float* w_o = reinterpret_cast<float*>(k_lds);  // [WAVES][16 columns][D]
-  if (gq == 0) {
-    w_m[wave][c16] = m_run;
-    w_l[wave][c16] = l_run;
-  }
+  // l: each k-group summed its own keys; add the four groups.
+  const float lsum = sum_xor32(sum_xor16(l_run));
   if (c16 < G) {
+    const size_t pr = ((size_t)b * a.Hq + g * G + c16) * a.nsplit + sidx;
+    const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
 #pragma unroll
-    for (int db = 0; db < S::DBLK; ++db)
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        w_o[(wave * 16 + c16) * D + db * 16 + 4 * gq + r] = o_acc[db][r];
-  }
-  __syncthreads();
-  for (int it = tid; it < G * D; it += S::THREADS) {
-    const int c = it / D;
-    const int d = it - c * D;
-    float M = kNegInf;
-#pragma unroll
-    for (int w = 0; w < S::WAVES; ++w) M = fmaxf(M, w_m[w][c]);
-    float lsum = 0.f, acc = 0.f;
-    if (M != kNegInf) {
-#pragma unroll
-      for (int w = 0; w < S::WAVES; ++w) {
-        const float f = fast_exp2(w_m[w][c] - M);
-        lsum += w_l[w][c] * f;
-        acc += w_o[(w * 16 + c) * D + d] * f;
-      }
+    for (int db = 0; db < S::DBLK; ++db) {
+      const f32x4 w = {o_acc[db][0] * inv, o_acc[db][1] * inv, o_acc[db][2] * inv,
+                       o_acc[db][3] * inv};
+      *reinterpret_cast<f32x4*>(a.o_part + pr * D + db * 16 + 4 * gq) = w;
     }
-    const size_t pr = ((size_t)b * a.Hq + g * G + c) * a.nsplit + sidx;
-    a.o_part[pr * D + d] = lsum > 0.f ? acc / lsum : 0.f;
-    if (d == 0) a.lse_part[pr] = lsum > 0.f ? (M + log2f(lsum)) * kLn2 : kNegInf;
+    if (gq == 0) a.lse_part[pr] = lsum > 0.f ? (m_run + log2f(lsum)) * kLn2 : kNegInf;
   }
 }
 
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
+  return x;
+}
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+// One wave per (batch, query head) row.  Every load the row needs (its
+// length, the split LSEs, the partial outputs of up to 16 splits) is issued
+// before any of them is used, so the kernel costs about one memory round
+// trip: lanes take the splits for the max / sum, then the head dims for the
+// weighted sum of partial outputs.
 template <int D>
 __global__ __launch_bounds__(256) void dec_combine_kernel(CombArgs a) {
   constexpr int PER_LANE = D / 64;
+  constexpr int CHUNK = 16;  // splits whose partial outputs are loaded together
   const int lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);  // (b, hq) row
   if (r >= a.B * a.Hq) return;
   const int b = r / a.Hq;
-  const int L = clamp_len(a.kv_seqlens[b], a.Smax);
-  const int ns = (L + a.split - 1) / a.split;  // splits holding keys
   const float* lp = a.lse_part + (size_t)r * a.nsplit;
-  float M = kNegInf;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, lp[s]);
+  const float* op = a.o_part + (size_t)r * a.nsplit * D + lane * PER_LANE;
+  const int len = a.kv_seqlens[b];
+  float ls[(64 + 63) / 64];
+  ls[0] = lane < a.nsplit ? lp[lane] : kNegInf;
+  float part[CHUNK][PER_LANE];
+#pragma unroll
+  for (int s = 0; s < CHUNK; ++s)
+#pragma unroll
+    for (int i = 0; i < PER_LANE; ++i) part[s][i] = s < a.nsplit ? op[(size_t)s * D + i] : 0.f;
+
+  const int L = clamp_len(len, a.Smax);
+  const int ns = (L + a.split - 1) / a.split;  // splits holding keys
+  // max over the valid splits (lanes beyond 64 splits loop)
+  float M = lane < ns ? ls[0] : kNegInf;
+  for (int s = 64 + lane; s < ns; s += 64) M = fmaxf(M, lp[s]);
+  M = wave_max(M);
   float out[PER_LANE];
 #pragma unroll
   for (int i = 0; i < PER_LANE; ++i) out[i] = 0.f;
   float lse = kNegInf;
   if (M != kNegInf) {
-    float sum = 0.f;
-    for (int s = 0; s < ns; ++s) sum += expf(lp[s] - M);
-    lse = M + logf(sum);
-    for (int s = 0; s < ns; ++s) {
-      const float w = expf(lp[s] - lse);
-      const float* op = a.o_part + ((size_t)r * a.nsplit + s) * D + lane * PER_LANE;
+    float sum = lane < ns ? expf(ls[0] - M) : 0.f;
+    for (int s = 64 + lane; s < ns; s += 64) sum += expf(lp[s] - M);
+    lse = M + logf(wave_sum(sum));
+    // weight of split s, taken from the lane that loaded its LSE
+    const float w_lane = lane < ns ? expf(ls[0] - lse) : 0.f;
 #pragma unroll
-      for (int i = 0; i < PER_LANE; ++i) out[i] += w * op[i];
+    for (int s = 0; s < CHUNK; ++s) {
+      const float w = __shfl(w_lane, s, 64);
+      if (s < ns)
+#pragma unroll
+        for (int i = 0; i < PER_LANE; ++i) out[i] += w * part[s][i];
+    }
+    for (int s = CHUNK; s < ns; ++s) {
+      const float w = expf(lp[s] - lse);
+#pragma unroll
+      for (int i = 0; i < PER_LANE; ++i) out[i] += w * op[(size_t)s * D + i];
     }
   }
   uint16_t* o = static_cast<uint16_t*>(a.o) + (size_t)r * D + lane * PER_LANE;

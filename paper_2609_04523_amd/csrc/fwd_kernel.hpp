@@ -1,19 +1,32 @@
 // fwd_kernel.hpp -- fused attention forward (prefill) for gfx950.
 //
-// One workgroup = 4 waves = BM query rows of one (batch, query head).  It
-// streams the key/value tiles of the head's KV group (hq / (Hq/Hkv))
-// through LDS, up to the causal diagonal, and keeps the softmax state and
-// the output accumulator in registers (online softmax: exact rewrite of
-// softmax(Q K^T * scale) V, folded tile by tile).
+// One workgroup = 4 waves = BM query rows of one (batch, query head); wave w
+// owns QB blocks of 32 consecutive rows.  The workgroup streams the 64-key
+// K and V tiles of its KV head (hq / (Hq/Hkv)) from HBM straight into LDS
+// (global_load_lds_dwordx4, two tiles in flight), up to the causal
+// diagonal, and keeps the softmax state and the output accumulator in
+// registers: online softmax, an exact rewrite of softmax(Q K^T * scale) V
+// folded tile by tile.
 //
 // Orientation.  Scores are formed transposed, S^T = K Q^T, with K as the
 // MFMA A operand (rows = keys) and Q^T as the B operand (columns =
-// queries).  A lane then owns one query column, so every softmax
-// reduction is in-lane plus one exchange with lane l^32.  The output is
-// formed as O^T = V^T P^T: P^T is the score accumulator converted to bf16
-// in place (its key order is the accumulator's own row order), and V^T is
-// read from a transposed LDS copy of the value tile.
+// queries).  A lane then owns one query column, so the softmax row
+// reductions are in-lane plus one exchange with lane l^32.  The output is
+// O^T = V^T P^T: P^T is the score accumulator converted to bf16 in place
+// (its key order is the accumulator's own row order), and the V^T operand
+// is read from the row-major V tile with the transposing LDS read.
+//
+// Softmax bookkeeping (exp2 domain, c = scale * log2 e):
+//   m    running row maximum of c*s, raised only when a tile's maximum
+//        exceeds it by more than kRescaleSlack, so exp2(c*s - m) <= 2^8 and
+//        the O accumulator is rescaled on few tiles;
+//   l    running sum of the fp32 weights (each half-wave sums its own
+//        keys; the halves are added at the end);
+//   O    sum of bf16(weight) * V in fp32;
+//   result O / l, LSE = ln 2 * (m + log2 l).
 #pragma once
+
+#include <type_traits>
 
 #include "mk_common.hpp"
 
@@ -36,14 +49,17 @@ template <int D, int QB>
 struct FwdShape {
   static constexpr int WAVES = 4;
   static constexpr int THREADS = WAVES * 64;
-  static constexpr int BM = WAVES * 32 * QB;          // query rows per workgroup
-  static constexpr int BN = 64;                       // keys per LDS tile
-  static constexpr int KSTEPS = D / 16;               // MFMA steps over the head dim
-  static constexpr int DBLK = D / 32;                 // 32-row output blocks of O^T
-  static constexpr int CHUNKS = D / 8;                // 16-byte chunks per row
-  static constexpr int VT_STRIDE = BN + 4;            // bf16 per transposed V row
-  static constexpr int LOADS = BN * CHUNKS / THREADS; // 16-byte loads per thread per tensor
+  static constexpr int BM = WAVES * 32 * QB;              // query rows per workgroup
+  static constexpr int BN = 64;                           // keys per LDS tile
+  static constexpr int KSTEPS = D / 16;                   // MFMA steps over the head dim
+  static constexpr int DBLK = D / 32;                     // 32-row blocks of O^T
+  static constexpr int CHUNKS = D / 8;                    // 16-byte chunks per row
+  static constexpr int ROWS_PER_KB = 512 / D;             // tile rows per 1 KB wave load
+  static constexpr int BLOCKS_PER_WAVE = BN * D * 2 / 1024 / WAVES;
+  static constexpr int LOADS_PER_TILE = 2 * BLOCKS_PER_WAVE;  // per thread, K and V
 };
+
+constexpr float kRescaleSlack = 8.0f;
 
 // Work-item order.  Longest causal q-tiles are issued first.  When the
 // number of (batch, kv head) groups is a multiple of 8, consecutive
@@ -73,12 +89,16 @@ __device__ __forceinline__ void fwd_map_block(int bid, const FwdArgs& a, int& qt
   }
 }
 
-template <int D, bool CAUSAL, bool OUT_F32, int QB>
-__global__ __launch_bounds__(256, 1) void fwd_kernel(FwdArgs a) {
+// POS_SCALE: scale > 0, so the row maximum can be taken on raw scores and
+// the scale folded into the exponent's FMA.  Otherwise scores are scaled
+// first (scale 0 and negative scales).
+template <int D, bool CAUSAL, bool OUT_F32, int QB, bool POS_SCALE>
+__global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   using S = FwdShape<D, QB>;
   constexpr int BN = S::BN;
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][BN * D];
-  __shared__ __attribute__((aligned(16))) uint16_t vt_lds[2][D * S::VT_STRIDE];
+  constexpr int TILE = BN * D;
+  __shared__ __attribute__((aligned(1024))) uint16_t k_lds[2][TILE];
+  __shared__ __attribute__((aligned(1024))) uint16_t v_lds[2][TILE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -98,11 +118,29 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdArgs a) {
   if (CAUSAL) n_keys = min(L, q_end + off);
   if (n_keys < 0) n_keys = 0;
   const int n_kt = (n_keys + BN - 1) / BN;
+  const float c = a.scale_log2;
 
   const size_t q_row0 = ((size_t)b * a.Hq + hq) * (size_t)a.Sq;
   const size_t kv_off = ((size_t)b * a.Hkv + g) * (size_t)a.Skv * D;
   const uint16_t* __restrict__ kg = a.k + kv_off;
   const uint16_t* __restrict__ vg = a.v + kv_off;
+
+  // Tile kt -> LDS buffer: wave-wide 16-byte loads, lane l of block blk
+  // carrying row blk*ROWS_PER_KB + l/CHUNKS, physical chunk l%CHUNKS.  Rows
+  // past the sequence end re-read its last row (finite data that the mask
+  // zeroes), so no load leaves [0, L).
+  auto issue_tile = [&](int kt, int buf) {
+#pragma unroll
+    for (int p = 0; p < S::BLOCKS_PER_WAVE; ++p) {
+      const int blk = p * S::WAVES + wave;
+      const int row = blk * S::ROWS_PER_KB + lane / S::CHUNKS;
+      const int ch = (lane % S::CHUNKS) ^ chunk_swz<D>(row);
+      const int gk = min(kt * BN + row, L - 1);
+      const size_t goff = (size_t)gk * D + ch * 8;
+      load_lds16(kg + goff, &k_lds[buf][blk * 512]);
+      load_lds16(vg + goff, &v_lds[buf][blk * 512]);
+    }
+  };
 
   // Q^T fragments: lane (column n, k-group h) holds q[row][16 s + 8 h .. +7].
   const int qw0 = q0 + wave * 32 * QB;
@@ -119,43 +157,6 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdArgs a) {
     }
   }
 
-  // K/V tile staging through registers.
-  u32x4 kreg[S::LOADS], vreg[S::LOADS];
-  auto load_tile = [&](int kt) {
-#pragma unroll
-    for (int p = 0; p < S::LOADS; ++p) {
-      const int c = tid + p * S::THREADS;
-      const int key = c / S::CHUNKS;
-      const int ch = c % S::CHUNKS;
-      const int gk = kt * BN + key;
-      u32x4 zk = {0u, 0u, 0u, 0u}, zv = {0u, 0u, 0u, 0u};
-      if (gk < L) {
-        zk = *reinterpret_cast<const u32x4*>(kg + (size_t)gk * D + ch * 8);
-        zv = *reinterpret_cast<const u32x4*>(vg + (size_t)gk * D + ch * 8);
-      }
-      kreg[p] = zk;
-      vreg[p] = zv;
-    }
-  };
-  // K rows keep their layout with 16-byte chunks XOR-swizzled by row; V is
-  // stored transposed ([d][key], padded rows) for the V^T operand.
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int p = 0; p < S::LOADS; ++p) {
-      const int c = tid + p * S::THREADS;
-      const int key = c / S::CHUNKS;
-      const int ch = c % S::CHUNKS;
-      *reinterpret_cast<u32x4*>(&k_lds[buf][key * D + ((ch ^ (key & (S::CHUNKS - 1))) * 8)]) =
-          kreg[p];
-      const u32x4 vv = vreg[p];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        vt_lds[buf][(ch * 8 + 2 * i) * S::VT_STRIDE + key] = (uint16_t)(vv[i] & 0xffffu);
-        vt_lds[buf][(ch * 8 + 2 * i + 1) * S::VT_STRIDE + key] = (uint16_t)(vv[i] >> 16);
-      }
-    }
-  };
-
   float m_run[QB], l_run[QB];
   f32x16 o_acc[QB][S::DBLK];
 #pragma unroll
@@ -168,114 +169,163 @@ __global__ __launch_bounds__(256, 1) void fwd_kernel(FwdArgs a) {
       for (int r = 0; r < 16; ++r) o_acc[qb][db][r] = 0.f;
   }
 
-  if (n_kt > 0) {
-    load_tile(0);
-    store_tile(0);
-  }
-  __syncthreads();
+  if (n_kt > 0) issue_tile(0, 0);
+  if (n_kt > 1) issue_tile(1, 1);
 
-  for (int kt = 0; kt < n_kt; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < n_kt) load_tile(kt + 1);
+  // Lane-constant parts of the LDS addresses.  Row r = 32 kb + n of a K
+  // tile: swz(r) does not depend on kb.  Transposing V reads: rows
+  // 16 kc + tr_row (+ 8), whose swizzle depends only on tr_row and on the
+  // +8, not on kc.
+  const int k_sw = chunk_swz<D>(n);
+  const int tr_i = lane & 15;
+  const int tr_row = 4 * h + (tr_i >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (tr_i & 3);
+  uint32_t v_addr[S::DBLK][2];  // byte offsets within a V tile, kc = 0
+#pragma unroll
+  for (int db = 0; db < S::DBLK; ++db)
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int r = tr_row + 8 * hh;
+      const int col = db * 32 + tr_col;
+      v_addr[db][hh] = 2u * (r * D + (((col >> 3) ^ chunk_swz<D>(r)) << 3) + (col & 7));
+    }
+  const uint32_t v_lds0 = lds_addr(&v_lds[0][0]);
+
+  // One 64-key tile for this wave.  MASK: apply the length / causal mask.
+  auto tile = [&](auto mask_tag, int kt, int buf) {
+    constexpr bool MASK = decltype(mask_tag)::value;
     const int key0 = kt * BN;
-    // A wave skips a tile whose keys all lie after its last query.
-    bool active = qw0 < a.Sq;
-    if (CAUSAL) active = active && key0 <= qw0 + 32 * QB - 1 + off;
-    if (active) {
-      // ---- S^T = K Q^T for the 64 keys of the tile ----
-      f32x16 sacc[QB][2];
+    const uint16_t* kt_lds = k_lds[buf];
+    // ---- S^T = K Q^T for the 64 keys of the tile ----
+    f32x16 sacc[QB][2];
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
+    for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) sacc[qb][kb][r] = 0.f;
+        for (int r = 0; r < 16; ++r) sacc[qb][kb][r] = 0.f;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const int row = kb * 32 + n;
+    for (int kb = 0; kb < 2; ++kb) {
+      const uint16_t* krow = kt_lds + (kb * 32 + n) * D;
 #pragma unroll
-        for (int s = 0; s < S::KSTEPS; ++s) {
-          const int ch = 2 * s + h;
-          const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(
-              &k_lds[buf][row * D + ((ch ^ (row & (S::CHUNKS - 1))) * 8)]));
+      for (int s = 0; s < S::KSTEPS; ++s) {
+        const bf16x8 kf =
+            as_bf16x8(*reinterpret_cast<const u32x4*>(krow + (((2 * s + h) ^ k_sw) << 3)));
 #pragma unroll
-          for (int qb = 0; qb < QB; ++qb) sacc[qb][kb] = mfma32(kf, qf[qb][s], sacc[qb][kb]);
-        }
+        for (int qb = 0; qb < QB; ++qb) sacc[qb][kb] = mfma32(kf, qf[qb][s], sacc[qb][kb]);
       }
-      // ---- online softmax, one query column per lane ----
-      bf16x8 pf[QB][4];
+    }
+    // ---- online softmax, one query column per lane ----
+    bf16x8 pf[QB][4];
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
+      if (!POS_SCALE) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) sacc[qb][kb][r] *= c;
+      }
+      if (MASK) {
         const int qrow = qw0 + qb * 32 + n;
-        const bool need_mask =
-            (key0 + BN > L) || (CAUSAL && key0 + BN - 1 > qw0 + qb * 32 + off);
-        float mx = kNegInf;
+        const int lim = min(L - 1, CAUSAL ? qrow + off : L - 1);  // last admissible key
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            float x = sacc[qb][kb][r] * a.scale_log2;
-            if (need_mask) {
-              const int key = key0 + kb * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-              if (key >= L || (CAUSAL && key > qrow + off)) x = kNegInf;
-            }
-            sacc[qb][kb][r] = x;
-            mx = fmaxf(mx, x);
+            const int key = key0 + kb * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+            if (key > lim) sacc[qb][kb][r] = kNegInf;
           }
-        mx = fmaxf(mx, swap_halves(mx));
+      }
+      float mx = kNegInf;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[qb][kb][r]);
+      mx = max_xor32(mx);
+      if (POS_SCALE) mx *= c;
+      if (__ballot(mx > m_run[qb] + kRescaleSlack)) {
         const float m_new = fmaxf(m_run[qb], mx);
-        const float m_use = (m_new == kNegInf) ? 0.f : m_new;
-        const float alpha = fast_exp2(m_run[qb] - m_use);
-        float rs = 0.f;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const float p = fast_exp2(sacc[qb][kb][r] - m_use);
-            sacc[qb][kb][r] = p;
-            rs += p;
-          }
-        rs += swap_halves(rs);
-        l_run[qb] = l_run[qb] * alpha + rs;
+        const float alpha = (m_new == kNegInf) ? 1.f : fast_exp2(m_run[qb] - m_new);
         m_run[qb] = m_new;
+        l_run[qb] *= alpha;
 #pragma unroll
         for (int db = 0; db < S::DBLK; ++db)
 #pragma unroll
           for (int r = 0; r < 16; ++r) o_acc[qb][db][r] *= alpha;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          const f32x16 p = sacc[qb][kb];
-          pf[qb][2 * kb] = to_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
-          pf[qb][2 * kb + 1] = to_bf16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
-        }
       }
-      // ---- O^T += V^T P^T over 16-key chunks ----
-      // Chunk kc: lane (k-group h) holds P for keys 16 kc + {4h..4h+3, 8+4h..8+4h+3}.
+      const float m_use = (m_run[qb] == kNegInf) ? 0.f : m_run[qb];
+      const float cc = POS_SCALE ? c : 1.f;
+      float rs = 0.f;
 #pragma unroll
-      for (int kc = 0; kc < 4; ++kc) {
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int db = 0; db < S::DBLK; ++db) {
-          const int d = db * 32 + n;
-          const uint16_t* vp = &vt_lds[buf][d * S::VT_STRIDE + kc * 16 + 4 * h];
-          const u32x2 lo = *reinterpret_cast<const u32x2*>(vp);
-          const u32x2 hi = *reinterpret_cast<const u32x2*>(vp + 8);
-          const u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
-          const bf16x8 vf = as_bf16x8(w);
-#pragma unroll
-          for (int qb = 0; qb < QB; ++qb) o_acc[qb][db] = mfma32(vf, pf[qb][kc], o_acc[qb][db]);
+        for (int r = 0; r < 16; ++r) {
+          const float p = fast_exp2(fmaf(sacc[qb][kb][r], cc, -m_use));
+          sacc[qb][kb][r] = p;
+          rs += p;
         }
+      l_run[qb] += rs;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const f32x16 p = sacc[qb][kb];
+        pf[qb][2 * kb] = to_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
+        pf[qb][2 * kb + 1] = to_bf16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
       }
     }
-    if (kt + 1 < n_kt) store_tile(buf ^ 1);
+    // ---- O^T += V^T P^T over 16-key chunks ----
+    // Chunk kc: k-group h holds P for keys 16 kc + {4h..4h+3, 8+4h..8+4h+3};
+    // the two transposing reads fetch V for exactly those keys, column d.
+    const uint32_t vb = v_lds0 + buf * (TILE * 2);
+#pragma unroll
+    for (int kc = 0; kc < 4; ++kc) {
+      u32x2 vr[S::DBLK][2];
+#pragma unroll
+      for (int db = 0; db < S::DBLK; ++db)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+          vr[db][hh] = lds_read_tr16_async(vb + v_addr[db][hh] + kc * 16 * D * 2);
+#pragma unroll
+      for (int db = 0; db < S::DBLK; db += 2) lds_wait4(vr[db][0], vr[db][1], vr[db + 1][0], vr[db + 1][1]);
+#pragma unroll
+      for (int db = 0; db < S::DBLK; ++db) {
+        const u32x4 w = {vr[db][0][0], vr[db][0][1], vr[db][1][0], vr[db][1][1]};
+        const bf16x8 vf = as_bf16x8(w);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) o_acc[qb][db] = mfma32(vf, pf[qb][kc], o_acc[qb][db]);
+      }
+    }
+  };
+
+  // Tiles [0, n_free) need no mask for any row of this wave; tiles up to
+  // n_live hold at least one admissible key for some row of the wave.
+  const int w_first = qw0;                      // first query row of the wave
+  const int w_last = min(qw0 + 32 * QB, a.Sq) - 1;
+  int n_free = (CAUSAL ? min(L, w_first + off + 1) : L) / BN;
+  int n_live = qw0 < a.Sq ? (CAUSAL ? min(L, w_last + off + 1) : L) : 0;
+  n_live = (max(n_live, 0) + BN - 1) / BN;
+  n_free = max(0, min(n_free, n_live));
+
+  for (int kt = 0; kt < n_kt; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < n_kt)
+      wait_vmcnt<S::LOADS_PER_TILE>();
+    else
+      wait_vmcnt<0>();
     __syncthreads();
+    if (kt < n_free)
+      tile(std::integral_constant<bool, false>(), kt, buf);
+    else if (kt < n_live)
+      tile(std::integral_constant<bool, true>(), kt, buf);
+    __syncthreads();
+    if (kt + 2 < n_kt) issue_tile(kt + 2, buf);
   }
 
   // ---- epilogue: O = O_acc / l, LSE = ln 2 * (m + log2 l) ----
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int qrow = qw0 + qb * 32 + n;
+    const float lsum = sum_xor32(l_run[qb]);
     if (qrow >= a.Sq) continue;
-    const float lsum = l_run[qb];
     const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
     const size_t obase = (q_row0 + qrow) * D;
 #pragma unroll

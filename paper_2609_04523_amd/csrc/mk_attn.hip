@@ -13,28 +13,34 @@
 namespace {
 
 constexpr int kVersion = 1;
-constexpr int kFwdQB = 2;             // 32-query blocks per wave in the forward kernel
-constexpr int kDefaultSplit = 256;    // decode keys per split
+constexpr int kFwdQB = 1;             // 32-query blocks per wave in the forward kernel
+constexpr int kDefaultSplit = 384;    // decode keys per split (not a power of two: see decode_kernel.hpp)
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-template <int D, bool CAUSAL, bool OUT_F32>
+template <int D, bool CAUSAL, bool OUT_F32, bool POS>
 hipError_t launch_fwd(const mk::FwdArgs& a, unsigned nblocks, hipStream_t st) {
-  hipLaunchKernelGGL((mk::fwd_kernel<D, CAUSAL, OUT_F32, kFwdQB>), dim3(nblocks),
+  hipLaunchKernelGGL((mk::fwd_kernel<D, CAUSAL, OUT_F32, kFwdQB, POS>), dim3(nblocks),
                      dim3(mk::FwdShape<D, kFwdQB>::THREADS), 0, st, a);
   return hipGetLastError();
 }
 
+template <int D, bool CAUSAL, bool OUT_F32>
+hipError_t launch_fwd_s(const mk::FwdArgs& a, unsigned nblocks, bool pos, hipStream_t st) {
+  return pos ? launch_fwd<D, CAUSAL, OUT_F32, true>(a, nblocks, st)
+             : launch_fwd<D, CAUSAL, OUT_F32, false>(a, nblocks, st);
+}
+
 template <int D>
 hipError_t launch_fwd_d(const mk::FwdArgs& a, unsigned nblocks, bool causal, bool out_f32,
-                        hipStream_t st) {
+                        bool pos, hipStream_t st) {
   if (causal)
-    return out_f32 ? launch_fwd<D, true, true>(a, nblocks, st)
-                   : launch_fwd<D, true, false>(a, nblocks, st);
-  return out_f32 ? launch_fwd<D, false, true>(a, nblocks, st)
-                 : launch_fwd<D, false, false>(a, nblocks, st);
+    return out_f32 ? launch_fwd_s<D, true, true>(a, nblocks, pos, st)
+                   : launch_fwd_s<D, true, false>(a, nblocks, pos, st);
+  return out_f32 ? launch_fwd_s<D, false, true>(a, nblocks, pos, st)
+                 : launch_fwd_s<D, false, false>(a, nblocks, pos, st);
 }
 
 int fwd_impl(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq,
@@ -71,8 +77,9 @@ int fwd_impl(const void* q, const void* k, const void* v, void* o, float* lse, i
   a.xcd_groups = ((B * Hkv) % 8 == 0) ? 1 : 0;
   a.scale_log2 = scale * mk::kLog2e;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  hipError_t e = (D == 128) ? launch_fwd_d<128>(a, (unsigned)nblocks, causal, out_f32, st)
-                            : launch_fwd_d<64>(a, (unsigned)nblocks, causal, out_f32, st);
+  const bool pos = scale > 0.f;
+  hipError_t e = (D == 128) ? launch_fwd_d<128>(a, (unsigned)nblocks, causal, out_f32, pos, st)
+                            : launch_fwd_d<64>(a, (unsigned)nblocks, causal, out_f32, pos, st);
   return e == hipSuccess ? MK_OK : MK_ERR_HIP;
 }
 
@@ -126,7 +133,6 @@ int mk_attn_decode(const void* q, const void* k_cache, const void* v_cache, void
   if (!q || !k_cache || !v_cache || !o || !kv_seqlens) return MK_ERR_NULL;
   if (B < 1 || Hq < 1 || Hkv < 1 || Smax < 1 || D < 1) return MK_ERR_SHAPE;
   if (Hq % Hkv != 0) return MK_ERR_SHAPE;
-  if (B > 65535 || Hkv > 65535) return MK_ERR_SHAPE;
   if (D != 64 && D != 128) return MK_ERR_UNSUPPORTED;
   if (Hq / Hkv > 16) return MK_ERR_UNSUPPORTED;
   if (split < 0) return MK_ERR_ARG;
@@ -156,11 +162,13 @@ int mk_attn_decode(const void* q, const void* k_cache, const void* v_cache, void
   a.split = l.split;
   a.nsplit = l.nsplit;
   a.scale_log2 = scale * mk::kLog2e;
-  const dim3 grid(l.nsplit, Hkv, B);
+  const long long n_items = (long long)l.nsplit * Hkv * B;
+  if (n_items > 0x7fffffffLL) return MK_ERR_SHAPE;
+  const dim3 grid((unsigned)n_items);
   if (D == 128)
-    hipLaunchKernelGGL(mk::dec_split_kernel<128>, grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL(mk::dec_split_kernel<128>, grid, dim3(64), 0, st, a);
   else
-    hipLaunchKernelGGL(mk::dec_split_kernel<64>, grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL(mk::dec_split_kernel<64>, grid, dim3(64), 0, st, a);
   if (hipGetLastError() != hipSuccess) return MK_ERR_HIP;
 
   mk::CombArgs c;

@@ -60,9 +60,89 @@ __device__ __forceinline__ uint16_t to_bf16_bits(float x) {
   return __builtin_bit_cast(uint16_t, h);
 }
 
-// Value of lane (l ^ 32): the other half of the wave.
-__device__ __forceinline__ float swap_halves(float x) {
-  return __shfl_xor(x, 32, 64);
+// Reductions between lane l and lane l^32 (v_permlane32_swap) and between
+// lane l and lane l^16 (v_permlane16_swap).  Both lanes of a pair receive
+// the same bits.
+__device__ __forceinline__ float max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                  false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                  false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float max_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x),
+                                                  false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x),
+                                                  false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// 16 bytes global -> LDS without passing through registers
+// (global_load_lds_dwordx4).  `lds` must be the same for the whole wave:
+// lane l's 16 bytes land at lds + 16 l.
+__device__ __forceinline__ void load_lds16(const void* g, void* lds) {
+  __builtin_amdgcn_global_load_lds(
+      (const void __attribute__((address_space(1)))*)g,
+      (void __attribute__((address_space(3)))*)lds, 16, 0, 0);
+}
+
+// s_waitcnt vmcnt(N): wait until at most N vector-memory operations of this
+// wave are outstanding (expcnt and lgkmcnt untouched).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Transposing LDS read (ds_read_b64_tr_b16).  Within each group of 16
+// lanes, lane i names 4 consecutive bf16 of row i/4, columns 4(i%4)..+3,
+// of a 4 x 16 block; lane j receives column j of the block, rows 0..3.
+__device__ __forceinline__ bf16x4 lds_read_tr16(const void* lds) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      (__attribute__((address_space(3))) bf16x4*)(lds));
+}
+
+// The same read issued as inline assembly, so that the compiler's wait
+// insertion does not tie it to in-flight LDS-DMA loads of other buffers.
+// The result is NOT ready on return: pass it through lds_wait4() before
+// use.  (LDS operations the compiler does not know about only make its
+// own lgkmcnt waits more conservative.)
+__device__ __forceinline__ u32x2 lds_read_tr16_async(uint32_t lds_addr) {
+  u32x2 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(lds_addr) : "memory");
+  return r;
+}
+// s_waitcnt lgkmcnt(0) that the four given registers depend on, so no use
+// of them can be scheduled before the wait.
+__device__ __forceinline__ void lds_wait4(u32x2& a, u32x2& b, u32x2& c, u32x2& d) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d) :: "memory");
+}
+
+// 32-bit LDS address of a __shared__ object.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) void*)p);
+}
+
+__device__ __forceinline__ bf16x8 cat(bf16x4 a, bf16x4 b) {
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// XOR swizzle of the 16-byte chunks of a K or V tile row in LDS (rows of
+// D bf16 = D/8 chunks).  Row r's logical chunk c sits at physical chunk
+// c ^ swz(r).  Sixteen consecutive rows read at one logical chunk hit
+// sixteen different chunk positions (D = 128), and the transposing read's
+// four rows x two adjacent chunks hit eight different positions.
+template <int D>
+__device__ __forceinline__ int chunk_swz(int r) {
+  if (D == 128) return ((r & 7) << 1) | ((r >> 3) & 1);
+  return ((r & 3) << 1) | ((r >> 2) & 1);
 }
 
 __device__ __forceinline__ int clamp_len(int len, int hi) {

@@ -98,7 +98,8 @@ def test_decode_validation(lib):
     for name in ("B", "Hq", "Hkv", "Smax"):
         assert dec_rc(lib, **{name: 0}) == 2
     assert dec_rc(lib, Hq=6, Hkv=4) == 2
-    assert dec_rc(lib, B=70000) == 2
+    # more work items than one launch can hold
+    assert dec_rc(lib, B=1 << 20, Hq=4096, Hkv=4096) == 2
     assert dec_rc(lib, D=96) == 3
     assert dec_rc(lib, Hq=34, Hkv=2) == 3  # group of 17 query heads
     assert dec_rc(lib, split=-1, ws_bytes=1 << 30) == 7

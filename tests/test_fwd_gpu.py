@@ -91,13 +91,16 @@ def test_fwd_config4_sampled_rows():
 
 
 # ---------------------------------------------------------------- invariants
-def test_causal_row0_is_v0_exactly():
+def test_causal_row0_is_v0():
+    # Row 0 sees key 0 alone: weight exp2(c*s - m) with m = c*s up to the
+    # rounding of one fp32 product, so O = v_0 to a few fp32 ulps.
     B, Hq, Hkv, S, D = 2, 8, 2, 300, 128
     q, k, v = workloads.prefill_inputs(B, Hq, Hkv, S, S, D, seed=7)
     o, lse = run_fwd(q, k, v, causal=True, scale=0.0883883, out_fp32=True)
     G = Hq // Hkv
     for h in range(Hq):
-        assert torch.equal(o[:, h, 0].cpu(), v[:, h // G, 0].float()), "row 0 != v_0"
+        assert torch.allclose(o[:, h, 0].cpu(), v[:, h // G, 0].float(), rtol=1e-6, atol=0), \
+            "row 0 != v_0"
     qf, kf = q.double(), k.double()
     s0 = torch.stack([(qf[:, h, 0] * kf[:, h // G, 0]).sum(-1) for h in range(Hq)], 1)
     ref = s0 * float(np.float32(0.0883883))
