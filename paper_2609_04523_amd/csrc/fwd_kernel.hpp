@@ -96,7 +96,9 @@ template <int D, bool CAUSAL, bool OUT_F32, int QB, bool POS_SCALE>
 __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   using S = FwdShape<D, QB>;
   constexpr int BN = S::BN;
-  constexpr int TILE = BN * D;
+  constexpr int TILE = BN * D;            // bf16 per tile per tensor
+  constexpr int TILE_BYTES = TILE * 2;
+  constexpr int ROW_BYTES = D * 2;
   __shared__ __attribute__((aligned(1024))) uint16_t k_lds[2][TILE];
   __shared__ __attribute__((aligned(1024))) uint16_t v_lds[2][TILE];
 
@@ -122,27 +124,11 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
 
   const size_t q_row0 = ((size_t)b * a.Hq + hq) * (size_t)a.Sq;
   const size_t kv_off = ((size_t)b * a.Hkv + g) * (size_t)a.Skv * D;
-  const uint16_t* __restrict__ kg = a.k + kv_off;
-  const uint16_t* __restrict__ vg = a.v + kv_off;
-
-  // Tile kt -> LDS buffer: wave-wide 16-byte loads, lane l of block blk
-  // carrying row blk*ROWS_PER_KB + l/CHUNKS, physical chunk l%CHUNKS.  Rows
-  // past the sequence end re-read its last row (finite data that the mask
-  // zeroes), so no load leaves [0, L).
-  auto issue_tile = [&](int kt, int buf) {
-#pragma unroll
-    for (int p = 0; p < S::BLOCKS_PER_WAVE; ++p) {
-      const int blk = p * S::WAVES + wave;
-      const int row = blk * S::ROWS_PER_KB + lane / S::CHUNKS;
-      const int ch = (lane % S::CHUNKS) ^ chunk_swz<D>(row);
-      const int gk = min(kt * BN + row, L - 1);
-      const size_t goff = (size_t)gk * D + ch * 8;
-      load_lds16(kg + goff, &k_lds[buf][blk * 512]);
-      load_lds16(vg + goff, &v_lds[buf][blk * 512]);
-    }
-  };
+  const char* __restrict__ kg = reinterpret_cast<const char*>(a.k + kv_off);
+  const char* __restrict__ vg = reinterpret_cast<const char*>(a.v + kv_off);
 
   // Q^T fragments: lane (column n, k-group h) holds q[row][16 s + 8 h .. +7].
+  // Loaded before any K/V traffic so waiting for them waits for nothing else.
   const int qw0 = q0 + wave * 32 * QB;
   bf16x8 qf[QB][S::KSTEPS];
 #pragma unroll
@@ -157,6 +143,35 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
     }
   }
 
+  // ---- tile loads: HBM -> LDS, one 1 KB wave-wide load per block ----
+  // Block blk = 4 p + wave of a tile holds rows blk*ROWS_PER_KB + l/CHUNKS;
+  // lane l fills physical chunk l % CHUNKS with logical chunk
+  // (l % CHUNKS) ^ swz(row).  Rows past the sequence end re-read its last
+  // row (finite data that the mask zeroes), so no load leaves [0, L).
+  int dma_row[S::BLOCKS_PER_WAVE];
+  int dma_ch[S::BLOCKS_PER_WAVE];  // byte offset of the logical chunk
+#pragma unroll
+  for (int p = 0; p < S::BLOCKS_PER_WAVE; ++p) {
+    const int row = (p * S::WAVES + wave) * S::ROWS_PER_KB + lane / S::CHUNKS;
+    dma_row[p] = row;
+    dma_ch[p] = ((lane % S::CHUNKS) ^ fwd_swz<D>(row)) * 16;
+  }
+  const uint32_t k_lds_w = __builtin_amdgcn_readfirstlane(lds_addr(&k_lds[0][0]) + wave * 1024);
+  const uint32_t v_lds_w = __builtin_amdgcn_readfirstlane(lds_addr(&v_lds[0][0]) + wave * 1024);
+  auto issue_tile = [&](int kt, auto buf_tag) {
+    constexpr int BUF = decltype(buf_tag)::value;
+    const int lim = L - 1 - kt * BN;  // last valid row of the tile
+    const char* kt_g = kg + (size_t)kt * BN * ROW_BYTES;
+    const char* vt_g = vg + (size_t)kt * BN * ROW_BYTES;
+#pragma unroll
+    for (int p = 0; p < S::BLOCKS_PER_WAVE; ++p) {
+      const uint32_t goff = (uint32_t)(min(dma_row[p], lim) * ROW_BYTES + dma_ch[p]);
+      const uint32_t lds_off = BUF * TILE_BYTES + p * S::WAVES * 1024;
+      load_lds16_at(kt_g + goff, k_lds_w + lds_off);
+      load_lds16_at(vt_g + goff, v_lds_w + lds_off);
+    }
+  };
+
   float m_run[QB], l_run[QB];
   f32x16 o_acc[QB][S::DBLK];
 #pragma unroll
@@ -169,33 +184,41 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
       for (int r = 0; r < 16; ++r) o_acc[qb][db][r] = 0.f;
   }
 
-  if (n_kt > 0) issue_tile(0, 0);
-  if (n_kt > 1) issue_tile(1, 1);
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  if (n_kt > 0) issue_tile(0, B0());
+  if (n_kt > 1) issue_tile(1, B1());
 
-  // Lane-constant parts of the LDS addresses.  Row r = 32 kb + n of a K
-  // tile: swz(r) does not depend on kb.  Transposing V reads: rows
-  // 16 kc + tr_row (+ 8), whose swizzle depends only on tr_row and on the
-  // +8, not on kc.
-  const int k_sw = chunk_swz<D>(n);
-  const int tr_i = lane & 15;
-  const int tr_row = 4 * h + (tr_i >> 2);
-  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (tr_i & 3);
-  uint32_t v_addr[S::DBLK][2];  // byte offsets within a V tile, kc = 0
+  // Lane parts of the LDS read addresses (bytes within a tile).  K row
+  // 32 kb + n: the swizzle of n + 32 kb equals that of n.  Transposing V
+  // reads: rows 16 kc + 4 h + i/4 (+ 8), columns 32 db + 16 ((l/16) % 2) +
+  // 4 (i % 4), i = l % 16; the swizzle does not depend on kc.
+  uint32_t k_addr[S::KSTEPS];
 #pragma unroll
-  for (int db = 0; db < S::DBLK; ++db)
+  for (int s = 0; s < S::KSTEPS; ++s)
+    k_addr[s] = lds_addr(&k_lds[0][0]) + n * ROW_BYTES + (((2 * s + h) ^ fwd_swz<D>(n)) << 4);
+  uint32_t v_addr[S::DBLK][2];
+  {
+    const int tr_i = lane & 15;
+    const int tr_row = 4 * h + (tr_i >> 2);
+    const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (tr_i & 3);
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const int r = tr_row + 8 * hh;
-      const int col = db * 32 + tr_col;
-      v_addr[db][hh] = 2u * (r * D + (((col >> 3) ^ chunk_swz<D>(r)) << 3) + (col & 7));
-    }
-  const uint32_t v_lds0 = lds_addr(&v_lds[0][0]);
+    for (int db = 0; db < S::DBLK; ++db)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int r = tr_row + 8 * hh;
+        const int col = db * 32 + tr_col;
+        v_addr[db][hh] = lds_addr(&v_lds[0][0]) + r * ROW_BYTES +
+                         ((((col >> 3) ^ fwd_swz<D>(r)) << 4) | ((col & 7) * 2));
+      }
+  }
 
-  // One 64-key tile for this wave.  MASK: apply the length / causal mask.
-  auto tile = [&](auto mask_tag, int kt, int buf) {
+  // One 64-key tile for this wave from LDS buffer BUF.  MASK: apply the
+  // length / causal mask.
+  auto tile = [&](auto mask_tag, auto buf_tag, int kt) {
     constexpr bool MASK = decltype(mask_tag)::value;
+    constexpr int BUF = decltype(buf_tag)::value;
     const int key0 = kt * BN;
-    const uint16_t* kt_lds = k_lds[buf];
     // ---- S^T = K Q^T for the 64 keys of the tile ----
     f32x16 sacc[QB][2];
 #pragma unroll
@@ -206,11 +229,11 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
         for (int r = 0; r < 16; ++r) sacc[qb][kb][r] = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      const uint16_t* krow = kt_lds + (kb * 32 + n) * D;
 #pragma unroll
       for (int s = 0; s < S::KSTEPS; ++s) {
-        const bf16x8 kf =
-            as_bf16x8(*reinterpret_cast<const u32x4*>(krow + (((2 * s + h) ^ k_sw) << 3)));
+        const bf16x8 kf = as_bf16x8(*reinterpret_cast<const __attribute__((address_space(3)))
+                                                           u32x4*>(
+            (uintptr_t)(k_addr[s] + BUF * TILE_BYTES + kb * 32 * ROW_BYTES)));
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) sacc[qb][kb] = mfma32(kf, qf[qb][s], sacc[qb][kb]);
       }
@@ -275,25 +298,29 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
     // ---- O^T += V^T P^T over 16-key chunks ----
     // Chunk kc: k-group h holds P for keys 16 kc + {4h..4h+3, 8+4h..8+4h+3};
     // the two transposing reads fetch V for exactly those keys, column d.
-    const uint32_t vb = v_lds0 + buf * (TILE * 2);
-#pragma unroll
-    for (int kc = 0; kc < 4; ++kc) {
+    auto pv_chunk = [&](auto kc_tag) {
+      constexpr int KC = decltype(kc_tag)::value;
+      constexpr int OFF = BUF * TILE_BYTES + KC * 16 * ROW_BYTES;
       u32x2 vr[S::DBLK][2];
 #pragma unroll
       for (int db = 0; db < S::DBLK; ++db)
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh)
-          vr[db][hh] = lds_read_tr16_async(vb + v_addr[db][hh] + kc * 16 * D * 2);
+        for (int hh = 0; hh < 2; ++hh) vr[db][hh] = lds_read_tr16_async_off<OFF>(v_addr[db][hh]);
 #pragma unroll
-      for (int db = 0; db < S::DBLK; db += 2) lds_wait4(vr[db][0], vr[db][1], vr[db + 1][0], vr[db + 1][1]);
+      for (int db = 0; db < S::DBLK; db += 2)
+        lds_wait4(vr[db][0], vr[db][1], vr[db + 1][0], vr[db + 1][1]);
 #pragma unroll
       for (int db = 0; db < S::DBLK; ++db) {
         const u32x4 w = {vr[db][0][0], vr[db][0][1], vr[db][1][0], vr[db][1][1]};
         const bf16x8 vf = as_bf16x8(w);
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb) o_acc[qb][db] = mfma32(vf, pf[qb][kc], o_acc[qb][db]);
+        for (int qb = 0; qb < QB; ++qb) o_acc[qb][db] = mfma32(vf, pf[qb][KC], o_acc[qb][db]);
       }
-    }
+    };
+    pv_chunk(std::integral_constant<int, 0>());
+    pv_chunk(std::integral_constant<int, 1>());
+    pv_chunk(std::integral_constant<int, 2>());
+    pv_chunk(std::integral_constant<int, 3>());
   };
 
   // Tiles [0, n_free) need no mask for any row of this wave; tiles up to
@@ -305,19 +332,24 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   n_live = (max(n_live, 0) + BN - 1) / BN;
   n_free = max(0, min(n_free, n_live));
 
-  for (int kt = 0; kt < n_kt; ++kt) {
-    const int buf = kt & 1;
+  // Tile kt lives in buffer kt % 2; the loop is unrolled by two so the
+  // buffer of every LDS access is a compile-time constant.
+  auto step = [&](int kt, auto buf_tag) {
     if (kt + 1 < n_kt)
       wait_vmcnt<S::LOADS_PER_TILE>();
     else
       wait_vmcnt<0>();
     __syncthreads();
     if (kt < n_free)
-      tile(std::integral_constant<bool, false>(), kt, buf);
+      tile(std::false_type(), buf_tag, kt);
     else if (kt < n_live)
-      tile(std::integral_constant<bool, true>(), kt, buf);
+      tile(std::true_type(), buf_tag, kt);
     __syncthreads();
-    if (kt + 2 < n_kt) issue_tile(kt + 2, buf);
+    if (kt + 2 < n_kt) issue_tile(kt + 2, buf_tag);
+  };
+  for (int kt = 0; kt < n_kt; kt += 2) {
+    step(kt, B0());
+    if (kt + 1 < n_kt) step(kt + 1, B1());
   }
 
   // ---- epilogue: O = O_acc / l, LSE = ln 2 * (m + log2 l) ----

@@ -92,6 +92,14 @@ __device__ __forceinline__ void load_lds16(const void* g, void* lds) {
       (const void __attribute__((address_space(1)))*)g,
       (void __attribute__((address_space(3)))*)lds, 16, 0, 0);
 }
+// Same, with the destination given as a 32-bit LDS address.  The address is
+// turned into an LDS pointer directly: going through a generic pointer
+// would map LDS address 0 to the null pointer's LDS image (0xffffffff).
+__device__ __forceinline__ void load_lds16_at(const void* g, uint32_t lds_addr) {
+  __builtin_amdgcn_global_load_lds(
+      (const void __attribute__((address_space(1)))*)g,
+      (void __attribute__((address_space(3)))*)(uintptr_t)lds_addr, 16, 0, 0);
+}
 
 // s_waitcnt vmcnt(N): wait until at most N vector-memory operations of this
 // wave are outstanding (expcnt and lgkmcnt untouched).
@@ -119,6 +127,15 @@ __device__ __forceinline__ u32x2 lds_read_tr16_async(uint32_t lds_addr) {
   asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(lds_addr) : "memory");
   return r;
 }
+// Same, with a compile-time byte offset folded into the instruction.
+template <int OFF>
+__device__ __forceinline__ u32x2 lds_read_tr16_async_off(uint32_t lds_addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset field is 16 bits");
+  u32x2 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(lds_addr), "i"(OFF)
+               : "memory");
+  return r;
+}
 // s_waitcnt lgkmcnt(0) that the four given registers depend on, so no use
 // of them can be scheduled before the wait.
 __device__ __forceinline__ void lds_wait4(u32x2& a, u32x2& b, u32x2& c, u32x2& d) {
@@ -143,6 +160,20 @@ template <int D>
 __device__ __forceinline__ int chunk_swz(int r) {
   if (D == 128) return ((r & 7) << 1) | ((r >> 3) & 1);
   return ((r & 3) << 1) | ((r >> 2) & 1);
+}
+
+// The forward kernel's swizzle.  Its transposing reads fetch, per 32 lanes,
+// 4 consecutive rows x 4 consecutive chunks; its K reads, per 16 lanes, 16
+// consecutive rows x 1 chunk.  D = 128 (a row spans all 64 banks): the two
+// high bits of the chunk index are XORed with r % 4 and the two low bits
+// with (r / 4) % 4, so 4 rows land in 4 different chunk quads and 16 rows
+// on 16 different chunks.  D = 64 (two rows share the 64 banks): rows of
+// one parity must differ, so bit 2 takes (r / 2) % 2 and bits 0-1 take
+// (r / 4) % 4.
+template <int D>
+__device__ __forceinline__ int fwd_swz(int r) {
+  if (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
 }
 
 __device__ __forceinline__ int clamp_len(int len, int hi) {
