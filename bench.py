@@ -58,6 +58,95 @@ def read_traffic(summary_name: str, digest: str):
     return float(m_t.group(1))
 
 
+# ---------------------------------------------------------------------------
+# rocprofv3 summaries (text files committed under profiles/)
+# ---------------------------------------------------------------------------
+def _find_db(path: str) -> str:
+    import glob
+    if path.endswith(".db"):
+        return path
+    hits = sorted(glob.glob(os.path.join(path, "**", "*.db"), recursive=True))
+    if not hits:
+        raise SystemExit(f"no rocprofv3 database under {path}")
+    return hits[0]
+
+
+def _short(name: str) -> str:
+    return name.split("(")[0].replace("void ", "")
+
+
+def summarize_trace(path: str, command: str) -> str:
+    """Markdown table of per-kernel durations from a --kernel-trace run."""
+    import sqlite3
+    db = sqlite3.connect(_find_db(path))
+    rows = db.execute("select name, duration from kernels").fetchall()
+    agg = {}
+    for name, dur in rows:
+        agg.setdefault(_short(name), []).append(dur / 1e3)  # ns -> us
+    total = sum(sum(v) for v in agg.values())
+    out = ["# rocprofv3 kernel trace", "", f"command: `{command}`", "",
+           f"kernel_source_digest: {kernel_source_digest()}", "",
+           "| kernel | calls | avg us | min us | max us | % of GPU time |",
+           "|---|---|---|---|---|---|"]
+    for k, v in sorted(agg.items(), key=lambda kv: -sum(kv[1])):
+        out.append(f"| `{k}` | {len(v)} | {sum(v) / len(v):.2f} | {min(v):.2f} | {max(v):.2f} | "
+                   f"{100 * sum(v) / total:.1f} |")
+    return "\n".join(out) + "\n"
+
+
+def _pmc_per_kernel(path: str, counter: str):
+    import sqlite3
+    db = sqlite3.connect(_find_db(path))
+    rows = db.execute("select dispatch_id, name, counter_name, counter_value from pmc_events "
+                      "where counter_name = ?", (counter,)).fetchall()
+    per_disp = {}
+    for disp, name, _, val in rows:
+        key = (disp, _short(name))
+        per_disp[key] = per_disp.get(key, 0.0) + val
+    per_kernel = {}
+    for (disp, name), val in per_disp.items():
+        per_kernel.setdefault(name, []).append(val)
+    return per_kernel
+
+
+def summarize_pmc(fetch_path: str, write_path: str, kernels, calib_bytes: int,
+                  commands) -> str:
+    """Per-launch HBM bytes of `kernels` (summed: one launch of the path)
+    from FETCH_SIZE / WRITE_SIZE runs, each scaled by what the counter reads
+    for the plain device copy of calib_bytes in the same run."""
+    fetch = _pmc_per_kernel(fetch_path, "FETCH_SIZE")
+    write = _pmc_per_kernel(write_path, "WRITE_SIZE")
+    copy = [k for k in fetch if "copyBuffer" in k]
+    if not copy:
+        raise SystemExit("no calibration copy kernel in the FETCH_SIZE run")
+    # the calibration copy is the largest copyBuffer dispatch
+    f_copy = max(fetch[copy[0]])
+    w_copy = max(write[copy[0]])
+    f_fac = (calib_bytes / 1024) / f_copy
+    w_fac = (calib_bytes / 1024) / w_copy
+    out = ["# rocprofv3 HBM traffic counters", ""]
+    for c in commands:
+        out.append(f"command: `{c}`")
+    out += ["", f"kernel_source_digest: {kernel_source_digest()}", "",
+            f"calibration: plain device copy of {calib_bytes} bytes reads FETCH_SIZE = "
+            f"{f_copy:.1f} KiB and WRITE_SIZE = {w_copy:.1f} KiB per dispatch; "
+            f"scale factors fetch x{f_fac:.4f}, write x{w_fac:.4f}", "",
+            "| kernel | launches | FETCH_SIZE KiB/launch | WRITE_SIZE KiB/launch | "
+            "scaled read bytes | scaled write bytes |", "|---|---|---|---|---|---|"]
+    total = 0.0
+    for k in kernels:
+        name = [n for n in fetch if k in n]
+        if not name:
+            raise SystemExit(f"kernel {k} not in the counter runs")
+        fv, wv = fetch[name[0]], write[name[0]]
+        f_avg, w_avg = sum(fv) / len(fv), sum(wv) / len(wv)
+        rb, wb = f_avg * 1024 * f_fac, w_avg * 1024 * w_fac
+        total += rb + wb
+        out.append(f"| `{name[0]}` | {len(fv)} | {f_avg:.1f} | {w_avg:.1f} | {rb:.4g} | {wb:.4g} |")
+    out += ["", f"hbm_bytes_per_launch: {total:.6g}", ""]
+    return "\n".join(out)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -67,11 +156,28 @@ def main():
     ap.add_argument("--decode", default="c5_decode_b64")
     ap.add_argument("--split", type=int, default=0, help="decode keys per split (0 = default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=96,
-                    help="query rows per head timed for the CPU oracle baseline")
+    ap.add_argument("--cpu-rows", type=int, default=0,
+                    help="query rows per head timed for the CPU oracle baseline (0: all)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this size (counter calibration)")
+    ap.add_argument("--summarize-trace", metavar="DIR",
+                    help="print a summary of a rocprofv3 --kernel-trace output and exit")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="print per-launch HBM bytes from FETCH_SIZE / WRITE_SIZE runs and exit")
+    ap.add_argument("--kernels", default="fwd_kernel",
+                    help="comma-separated kernel name fragments for --summarize-pmc")
+    ap.add_argument("--command", action="append", default=[],
+                    help="command line(s) recorded in a summary")
     args = ap.parse_args()
+
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace, "; ".join(args.command)), end="")
+        return
+    if args.summarize_pmc:
+        print(summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1],
+                            args.kernels.split(","), args.calib_copy_mib << 20, args.command),
+              end="")
+        return
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -140,23 +246,24 @@ def main():
     torch.cuda.synchronize()
 
     K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    # One event at every kernel boundary: ev[2i] before prefill i, ev[2i+1]
+    # between prefill i and decode i, ev[2i+2] after decode i (and before
+    # prefill i+1), so each launch is bracketed by exactly two markers.
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * K + 1)]
     log(f"[bench] timing {K} steps")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    ev[0].record(stream)
     for i in range(K):
-        e = ev[i]
-        e[0].record(stream)
         prefill()
-        e[1].record(stream)
-        e[2].record(stream)
+        ev[2 * i + 1].record(stream)
         decode(i)
-        e[3].record(stream)
+        ev[2 * i + 2].record(stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / K
-    t_pre = [e[0].elapsed_time(e[1]) for e in ev]   # ms
-    t_dec = [e[2].elapsed_time(e[3]) for e in ev]
+    t_pre = [ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(K)]  # ms
+    t_dec = [ev[2 * i + 1].elapsed_time(ev[2 * i + 2]) for i in range(K)]
     pre_ms = sum(t_pre) / K
     dec_ms = sum(t_dec) / K
     flops = pcfg.flops
@@ -222,25 +329,29 @@ def main():
 
     if not args.no_cpu_baseline:
         from oracle import oracle as orc  # timed CPU baseline only
-        nrows = min(args.cpu_rows, pcfg.S)
-        rows = workloads.sample_rows(pcfg.B, pcfg.Hq, pcfg.S, nrows, seed=pcfg.seed + 7)
         qh, kh, vh = workloads.config_inputs(pcfg)
         qb, kb, vb = workloads.bits(qh), workloads.bits(kh), workloads.bits(vh)
         threads = orc.default_threads()
-        log(f"[bench] cpu oracle baseline: {nrows} rows/head on {threads} threads")
+        if args.cpu_rows and args.cpu_rows < pcfg.S:
+            rows = workloads.sample_rows(pcfg.B, pcfg.Hq, pcfg.S, args.cpu_rows,
+                                         seed=pcfg.seed + 7)
+            pairs = int((rows.long() + 1).sum())  # causal row i sees i+1 keys
+            rows_np, what = rows.numpy(), f"{args.cpu_rows} seeded query rows per head"
+        else:
+            rows_np, what = None, "every query row"
+            pairs = pcfg.B * pcfg.Hq * pcfg.pairs_per_head
+        log(f"[bench] cpu oracle baseline: {what} on {threads} threads")
         c0 = time.perf_counter()
-        orc.attn_fwd(qb, kb, vb, causal=True, scale=pcfg.scale, rows=rows.numpy(),
-                     threads=threads)
+        orc.attn_fwd(qb, kb, vb, causal=True, scale=pcfg.scale, rows=rows_np, threads=threads)
         c1 = time.perf_counter()
-        pairs = int((rows.long() + 1).sum())  # row i sees i+1 keys
         cpu_tflops = 4 * pcfg.D * pairs / (c1 - c0) / 1e12
         result["cpu_baseline"] = {
             "value": cpu_tflops,
             "unit": "TFLOP/s",
             "cores": threads,
             "kind": "oracle",
-            "sample": (f"{nrows} seeded query rows per head of {pcfg.name} "
-                       f"({pairs} query-key pairs, {c1 - c0:.2f} s)"),
+            "sample": (f"{what} of {pcfg.name} ({pairs} query-key pairs, fp64, "
+                       f"{c1 - c0:.2f} s)"),
         }
     print(json.dumps(result), flush=True)
 
