@@ -3,13 +3,14 @@
 // Kernel 1 (dec_split_kernel): one single-wave workgroup per (split, kv
 // head, batch).  The G = Hq/Hkv query heads of the kv head are the columns
 // of 16x16x32 MFMA blocks, so every cached K/V byte is read once for all
-// of them.  The wave streams its split 32 keys per stage, PREFETCH stages
-// ahead: K straight from HBM into registers, already in the MFMA A-operand
-// layout, and V from HBM into a private LDS ring (global_load_lds_dwordx4)
-// from which the transposing read builds the V^T operand.  No barrier is
-// needed since no other wave touches its LDS.  The wave keeps its own
-// online-softmax state and writes the split's normalised output and its
-// natural-log LSE.
+// of them.  The wave streams its split 32 keys per stage through a private
+// ring of STAGES LDS slots, loading K and V HBM -> LDS with coalesced 1 KB
+// wave loads (global_load_lds_dwordx4) STAGES-1 stages ahead of use; no
+// barrier is needed since no other wave touches its LDS.  All LDS reads are
+// issued as inline assembly and waited on right before use, so no loaded
+// register lives across an iteration (the compiler's own waits would
+// otherwise serialise the prefetch).  The wave keeps its own online-softmax
+// state and writes the split's normalised output and natural-log LSE.
 //
 // Kernel 2 (dec_combine_kernel): per (batch, query head), merge the splits
 // by their log-sum-exp: LSE = log sum_s exp(LSE_s), O = sum_s
@@ -48,23 +49,24 @@ struct CombArgs {
 template <int D>
 struct DecShape {
   static constexpr int BN = 32;                        // keys per stage
-  static constexpr int PREFETCH = 3;                   // stages in flight ahead of use
-  static constexpr int VSLOTS = PREFETCH + 1;          // V ring slots in LDS
+  static constexpr int STAGES = 3;                     // LDS ring slots
   static constexpr int CHUNKS = D / 8;                 // 16-byte chunks per row
+  static constexpr int ROW_BYTES = D * 2;
   static constexpr int ROWS_PER_KB = 512 / D;          // rows per 1 KB wave load
-  static constexpr int VBLOCKS = BN * D * 2 / 1024;    // 1 KB V loads per stage
+  static constexpr int BLOCKS = BN * ROW_BYTES / 1024; // 1 KB loads per tensor per stage
+  static constexpr int LOADS_PER_STAGE = 2 * BLOCKS;   // K and V
   static constexpr int KSTEPS = D / 32;                // 16x16x32 steps over the head dim
-  static constexpr int KLOADS = 2 * KSTEPS;            // 16-byte K loads per lane per stage
-  static constexpr int LOADS_PER_STAGE = VBLOCKS + KLOADS;
   static constexpr int DBLK = D / 16;                  // 16-row blocks of O^T
-  static constexpr int STAGE_ELEMS = BN * D;           // bf16 per V stage
+  static constexpr int TILE_BYTES = BN * ROW_BYTES;    // one tensor, one stage
+  static constexpr int SLOT_BYTES = 2 * TILE_BYTES;    // K then V
 };
 
 template <int D>
 __global__ __launch_bounds__(64) void dec_split_kernel(DecArgs a) {
   using S = DecShape<D>;
   constexpr int BN = S::BN;
-  __shared__ __attribute__((aligned(1024))) uint16_t v_lds[S::VSLOTS][S::STAGE_ELEMS];
+  constexpr int RB = S::ROW_BYTES;
+  __shared__ __attribute__((aligned(1024))) char kv_lds[S::STAGES * S::SLOT_BYTES];
 
   const int lane = threadIdx.x;
   const int c16 = lane & 15;  // MFMA column (query head of the group) / row (key)
@@ -88,10 +90,8 @@ __global__ __launch_bounds__(64) void dec_split_kernel(DecArgs a) {
   const int n_t = (k_end - k_begin + BN - 1) / BN;
   // The split's stages are walked starting at a per-workgroup rotation, so
   // that workgroups running together do not stream addresses that agree
-  // modulo large powers of two (the caches of all heads start on such
-  // boundaries), which would pile their traffic onto the same HBM
-  // channels.  The order of the stages does not change the result beyond
-  // rounding.
+  // modulo large powers of two.  The order of the stages does not change
+  // the result beyond rounding.
   const int rot = (int)(((unsigned)(b * 131 + g * 37 + sidx * 7)) % (unsigned)n_t);
   auto stage_key0 = [&](int t) {
     int u = t + rot;
@@ -100,8 +100,8 @@ __global__ __launch_bounds__(64) void dec_split_kernel(DecArgs a) {
   };
 
   const size_t kv_off = ((size_t)b * a.Hkv + g) * (size_t)a.Smax * D;
-  const uint16_t* __restrict__ kg = a.kc + kv_off;
-  const uint16_t* __restrict__ vg = a.vc + kv_off;
+  const char* __restrict__ kg = reinterpret_cast<const char*>(a.kc + kv_off);
+  const char* __restrict__ vg = reinterpret_cast<const char*>(a.vc + kv_off);
 
   // Q^T fragments: column c16 is query head g*G + c16 (zero when c16 >= G);
   // loaded before any cache traffic so that waiting for them waits for
@@ -116,45 +116,54 @@ __global__ __launch_bounds__(64) void dec_split_kernel(DecArgs a) {
     qf[s] = as_bf16x8(u);
   }
 
-  // Stage t: V rows -> LDS slot t % VSLOTS (row blk*ROWS_PER_KB + l/CHUNKS,
-  // chunks XOR-swizzled), then K rows -> registers: lane (row c16 of key
-  // block kb, k-group gq) takes k[key][32 s + 8 gq .. +7].  Rows past the
-  // split end re-read its last row (the mask zeroes their weight), so no
-  // load leaves the valid keys [0, L).
-  u32x4 kreg[S::PREFETCH + 1][2][S::KSTEPS];
-  auto issue = [&](int t, auto slot_tag) {
-    constexpr int SLOT = decltype(slot_tag)::value;
-    const int vslot = t % S::VSLOTS;
+  // Stage t -> ring slot t % STAGES: K rows, then V rows, each tile row
+  // blk*ROWS_PER_KB + l/CHUNKS with its 16-byte chunks XOR-swizzled.  Rows
+  // past the split end re-read its last row (the mask zeroes their
+  // weight), so no load leaves the valid keys [0, L).
+  const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(kv_lds));
+  const int dma_row = lane / S::CHUNKS;
+  constexpr int ROW_STEP = S::ROWS_PER_KB;  // rows per 1 KB block
+  auto issue = [&](int t) {
+    const uint32_t slot = lds0 + (uint32_t)(t % S::STAGES) * S::SLOT_BYTES;
+    const int key0 = stage_key0(t);
+    const int lim = k_end - 1 - key0;  // last valid row of the stage
+    const char* kt_g = kg + (size_t)key0 * RB;
+    const char* vt_g = vg + (size_t)key0 * RB;
 #pragma unroll
-    for (int blk = 0; blk < S::VBLOCKS; ++blk) {
-      const int row = blk * S::ROWS_PER_KB + lane / S::CHUNKS;
-      const int ch = (lane % S::CHUNKS) ^ chunk_swz<D>(row);
-      const int gk = min(stage_key0(t) + row, k_end - 1);
-      load_lds16(vg + (size_t)gk * D + ch * 8, &v_lds[vslot][blk * 512]);
-    }
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const int gk = min(stage_key0(t) + kb * 16 + c16, k_end - 1);
-#pragma unroll
-      for (int s = 0; s < S::KSTEPS; ++s)
-        kreg[SLOT][kb][s] = *reinterpret_cast<const u32x4*>(kg + (size_t)gk * D + s * 32 + gq * 8);
+    for (int blk = 0; blk < S::BLOCKS; ++blk) {
+      const int row = min(dma_row + blk * ROW_STEP, lim);
+      const int ch = ((lane % S::CHUNKS) ^ chunk_swz<D>(dma_row + blk * ROW_STEP)) * 16;
+      const uint32_t goff = (uint32_t)(row * RB + ch);
+      load_lds16_at(kt_g + goff, slot + blk * 1024);
+      load_lds16_at(vt_g + goff, slot + S::TILE_BYTES + blk * 1024);
     }
   };
 
-  // Lane-constant LDS offsets of the transposing V reads: rows 4 gq + i/4
-  // (+ 16), columns 16 db + 4 (i % 4), i = lane % 16.
-  const int tr_row = 4 * gq + (c16 >> 2);
-  const int tr_col = 4 * (c16 & 3);
-  uint32_t v_addr[S::DBLK][2];
+  // Lane parts of the LDS read addresses within a slot.  K: row 16 kb +
+  // c16, logical chunk 4 s + gq.  V (transposing): rows 4 gq + c16/4 (+ 16),
+  // columns 16 db + 4 (c16 % 4).
+  uint32_t k_addr[2][S::KSTEPS];
 #pragma unroll
-  for (int db = 0; db < S::DBLK; ++db)
+  for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const int r = tr_row + 16 * hh;
-      const int col = db * 16 + tr_col;
-      v_addr[db][hh] = 2u * (r * D + (((col >> 3) ^ chunk_swz<D>(r)) << 3) + (col & 7));
+    for (int s = 0; s < S::KSTEPS; ++s) {
+      const int r = kb * 16 + c16;
+      k_addr[kb][s] = r * RB + (((4 * s + gq) ^ chunk_swz<D>(r)) << 4);
     }
-  const uint32_t v_lds0 = lds_addr(&v_lds[0][0]);
+  uint32_t v_addr[S::DBLK][2];
+  {
+    const int tr_row = 4 * gq + (c16 >> 2);
+    const int tr_col = 4 * (c16 & 3);
+#pragma unroll
+    for (int db = 0; db < S::DBLK; ++db)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int r = tr_row + 16 * hh;
+        const int col = db * 16 + tr_col;
+        v_addr[db][hh] = S::TILE_BYTES + r * RB +
+                         ((((col >> 3) ^ chunk_swz<D>(r)) << 4) | ((col & 7) * 2));
+      }
+  }
 
   float m_run = kNegInf, l_run = 0.f;
   f32x4 o_acc[S::DBLK];
@@ -164,18 +173,25 @@ __global__ __launch_bounds__(64) void dec_split_kernel(DecArgs a) {
     for (int r = 0; r < 4; ++r) o_acc[db][r] = 0.f;
   const float c = a.scale_log2;
 
-  // One stage: K from register slot SLOT, V from LDS slot t % VSLOTS.
-  auto consume = [&](int t, auto slot_tag) {
-    constexpr int SLOT = decltype(slot_tag)::value;
+  auto consume = [&](int t) {
+    const uint32_t slot = lds0 + (uint32_t)(t % S::STAGES) * S::SLOT_BYTES;
     const int key0 = stage_key0(t);
+    // S^T = K Q^T for the 32 keys of the stage (two 16-key blocks).
     f32x4 sacc[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
+      u32x4 kf[S::KSTEPS];
+#pragma unroll
+      for (int s = 0; s < S::KSTEPS; ++s) kf[s] = lds_read_b128_async_off<0>(slot + k_addr[kb][s]);
+      static_assert(S::KSTEPS == 2 || S::KSTEPS == 4, "head dim 64 or 128");
+      if constexpr (S::KSTEPS == 4)
+        lds_wait_b128x4(kf[0], kf[1], kf[2], kf[3]);
+      else
+        lds_wait_b128x2(kf[0], kf[1]);
 #pragma unroll
       for (int r = 0; r < 4; ++r) sacc[kb][r] = 0.f;
 #pragma unroll
-      for (int s = 0; s < S::KSTEPS; ++s)
-        sacc[kb] = mfma16(as_bf16x8(kreg[SLOT][kb][s]), qf[s], sacc[kb]);
+      for (int s = 0; s < S::KSTEPS; ++s) sacc[kb] = mfma16(as_bf16x8(kf[s]), qf[s], sacc[kb]);
     }
     // Online softmax over the column (query head); lane holds keys
     // 16 kb + 4 gq + r.
@@ -212,14 +228,13 @@ __global__ __launch_bounds__(64) void dec_split_kernel(DecArgs a) {
     // P^T: k-group gq holds keys {4gq..4gq+3} and {16+4gq..16+4gq+3}.
     const bf16x8 pf = to_bf16x8(sacc[0][0], sacc[0][1], sacc[0][2], sacc[0][3], sacc[1][0],
                                 sacc[1][1], sacc[1][2], sacc[1][3]);
-    const uint32_t vb = v_lds0 + (t % S::VSLOTS) * (S::STAGE_ELEMS * 2);
 #pragma unroll
     for (int db0 = 0; db0 < S::DBLK; db0 += 2) {
       u32x2 vr[2][2];
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) vr[j][hh] = lds_read_tr16_async(vb + v_addr[db0 + j][hh]);
+        for (int hh = 0; hh < 2; ++hh) vr[j][hh] = lds_read_tr16_async(slot + v_addr[db0 + j][hh]);
       lds_wait4(vr[0][0], vr[0][1], vr[1][0], vr[1][1]);
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
@@ -229,30 +244,22 @@ __global__ __launch_bounds__(64) void dec_split_kernel(DecArgs a) {
     }
   };
 
-  using I0 = std::integral_constant<int, 0>;
-  using I1 = std::integral_constant<int, 1>;
-  using I2 = std::integral_constant<int, 2>;
-  using I3 = std::integral_constant<int, 3>;
-  static_assert(S::PREFETCH == 3, "register ring below is written for 3 stages ahead");
-  if (0 < n_t) issue(0, I0());
-  if (1 < n_t) issue(1, I1());
-  if (2 < n_t) issue(2, I2());
-  // Register slot of stage t is t % 4; the loop is unrolled by 4 so every
-  // slot index is a compile-time constant.
-  auto step = [&](int t, auto use_tag, auto load_tag) {
-    if (t + S::PREFETCH < n_t) {
-      issue(t + S::PREFETCH, load_tag);
-      wait_vmcnt<S::PREFETCH * S::LOADS_PER_STAGE>();
+  static_assert(S::STAGES == 3, "the wait counts below assume two stages ahead");
+  issue(0);
+  if (1 < n_t) issue(1);
+  for (int t = 0; t < n_t; ++t) {
+    // Before stage t is read, only the stages issued after it may still be
+    // loading.  Slot (t+2) % 3 held stage t-1, whose reads all completed
+    // in the previous iteration.
+    if (t + 2 < n_t) {
+      issue(t + 2);
+      wait_vmcnt<2 * S::LOADS_PER_STAGE>();
+    } else if (t + 1 < n_t) {
+      wait_vmcnt<S::LOADS_PER_STAGE>();
     } else {
       wait_vmcnt<0>();
     }
-    consume(t, use_tag);
-  };
-  for (int t = 0; t < n_t; t += 4) {
-    step(t, I0(), I3());
-    if (t + 1 < n_t) step(t + 1, I1(), I0());
-    if (t + 2 < n_t) step(t + 2, I2(), I1());
-    if (t + 3 < n_t) step(t + 3, I3(), I2());
+    consume(t);
   }
 
   // l: each k-group summed its own keys; add the four groups.

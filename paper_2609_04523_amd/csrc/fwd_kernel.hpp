@@ -148,14 +148,13 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   // lane l fills physical chunk l % CHUNKS with logical chunk
   // (l % CHUNKS) ^ swz(row).  Rows past the sequence end re-read its last
   // row (finite data that the mask zeroes), so no load leaves [0, L).
-  int dma_row[S::BLOCKS_PER_WAVE];
-  int dma_ch[S::BLOCKS_PER_WAVE];  // byte offset of the logical chunk
-#pragma unroll
-  for (int p = 0; p < S::BLOCKS_PER_WAVE; ++p) {
-    const int row = (p * S::WAVES + wave) * S::ROWS_PER_KB + lane / S::CHUNKS;
-    dma_row[p] = row;
-    dma_ch[p] = ((lane % S::CHUNKS) ^ fwd_swz<D>(row)) * 16;
-  }
+  // The rows a lane loads are dma_row + ROW_STEP * p, and they all share
+  // one swizzle (it depends on the row modulo 16 at D = 128 and on bits 1-3
+  // of the row at D = 64, which the step leaves unchanged).
+  constexpr int ROW_STEP = S::WAVES * S::ROWS_PER_KB;
+  static_assert(ROW_STEP % 16 == 0, "row step must preserve the swizzle");
+  const int dma_row = wave * S::ROWS_PER_KB + lane / S::CHUNKS;
+  const int dma_ch = ((lane % S::CHUNKS) ^ fwd_swz<D>(dma_row)) * 16;  // byte offset
   const uint32_t k_lds_w = __builtin_amdgcn_readfirstlane(lds_addr(&k_lds[0][0]) + wave * 1024);
   const uint32_t v_lds_w = __builtin_amdgcn_readfirstlane(lds_addr(&v_lds[0][0]) + wave * 1024);
   auto issue_tile = [&](int kt, auto buf_tag) {
@@ -165,7 +164,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
     const char* vt_g = vg + (size_t)kt * BN * ROW_BYTES;
 #pragma unroll
     for (int p = 0; p < S::BLOCKS_PER_WAVE; ++p) {
-      const uint32_t goff = (uint32_t)(min(dma_row[p], lim) * ROW_BYTES + dma_ch[p]);
+      const uint32_t goff = (uint32_t)(min(dma_row, lim - p * ROW_STEP) * ROW_BYTES + dma_ch) +
+                            p * ROW_STEP * ROW_BYTES;
       const uint32_t lds_off = BUF * TILE_BYTES + p * S::WAVES * 1024;
       load_lds16_at(kt_g + goff, k_lds_w + lds_off);
       load_lds16_at(vt_g + goff, v_lds_w + lds_off);

@@ -136,6 +136,23 @@ __device__ __forceinline__ u32x2 lds_read_tr16_async_off(uint32_t lds_addr) {
                : "memory");
   return r;
 }
+// 16-byte LDS read issued as inline assembly (same contract as the
+// transposing read above: pass the result through a tied wait before use).
+template <int OFF>
+__device__ __forceinline__ u32x4 lds_read_b128_async_off(uint32_t lds_addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset field is 16 bits");
+  u32x4 r;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(lds_addr), "i"(OFF) : "memory");
+  return r;
+}
+// s_waitcnt lgkmcnt(0) that the given registers depend on.
+__device__ __forceinline__ void lds_wait_b128x4(u32x4& a, u32x4& b, u32x4& c, u32x4& d) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d) :: "memory");
+}
+__device__ __forceinline__ void lds_wait_b128x2(u32x4& a, u32x4& b) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b) :: "memory");
+}
+
 // s_waitcnt lgkmcnt(0) that the four given registers depend on, so no use
 // of them can be scheduled before the wait.
 __device__ __forceinline__ void lds_wait4(u32x2& a, u32x2& b, u32x2& c, u32x2& d) {
