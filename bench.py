@@ -3,7 +3,7 @@
 One step = one pass over the whole path on resident synthetic inputs:
   * the fused causal attention forward on the prefill workload
     (causal MHA B=4 H=16 S=2048 D=128 bf16 by default), then
-  * the split-KV decode (split kernel + LSE merge) on the ragged decode
+  * the split-KV decode (equal-work part kernel + LSE merge kernel) on the ragged decode
     batch (B=64 Hq=32 Hkv=8 D=128, lengths in [512, 4096]), alternating
     between two copies of the cache so the 256 MB last-level cache cannot
     hand the previous step's cache to the next one.
@@ -154,7 +154,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--prefill", default="c2_mha_s2k")
     ap.add_argument("--decode", default="c5_decode_b64")
-    ap.add_argument("--split", type=int, default=0, help="decode keys per split (0 = default)")
+    ap.add_argument("--parts", type=int, default=0, help="decode parts (0 = library default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="query rows per head timed for the CPU oracle baseline (0: all)")
@@ -211,7 +211,7 @@ def main():
     lens_d = lens.to(dev)
     B, Hq, D = qd.shape
     Hkv, Smax = dcfg.Hkv, dcfg.Smax
-    ws_bytes = mk.mk_attn_decode_workspace_bytes(B, Hq, Smax, D, args.split)
+    ws_bytes = mk.mk_attn_decode_workspace_bytes(Hq, Hkv, D, args.parts)
     ws = torch.empty(ws_bytes, device=dev, dtype=torch.uint8)
     od = torch.empty((B, Hq, D), device=dev, dtype=torch.bfloat16)
     lsed = torch.empty((B, Hq), device=dev, dtype=torch.float32)
@@ -227,7 +227,7 @@ def main():
     def decode(i):
         kcc, vcc = caches[i & 1]
         mk.mk_attn_decode(qd, kcc, vcc, od, lsed, B, Hq, Hkv, Smax, D, dcfg.scale, lens_d,
-                          args.split, ws, ws_bytes, stream)
+                          args.parts, ws, ws_bytes, stream)
 
     if args.calib_copy_mib:
         n = args.calib_copy_mib << 20
@@ -276,7 +276,7 @@ def main():
 
     digest = kernel_source_digest()
     traffic_pre = read_traffic(f"fwd_kernel_{pcfg.name}_counters.md", digest)
-    traffic_dec = read_traffic(f"dec_split_kernel_{dcfg.name}_counters.md", digest)
+    traffic_dec = read_traffic(f"dec_part_kernel_{dcfg.name}_counters.md", digest)
 
     result = {
         "metric": "attention fwd TFLOP/s and % bf16 MFMA peak (prefill); HBM GB/s (decode)",
@@ -296,7 +296,7 @@ def main():
                          f"Hkv={pcfg.Hkv} S={pcfg.S} D={pcfg.D} bf16 in, "
                          f"{'fp32' if pcfg.out_fp32 else 'bf16'} O + fp32 LSE; then "
                          f"{dcfg.name}: decode B={B} Hq={Hq} Hkv={Hkv} D={D} "
-                         f"lengths U[{dcfg.lmin},{dcfg.lmax}] split-KV + LSE merge"),
+                         f"lengths U[{dcfg.lmin},{dcfg.lmax}] split-KV (equal-work parts) + LSE merge"),
             "prefill_flops_per_step": flops,
             "decode_bytes_per_step": dec_bytes,
             "decode_sum_kv_len": sum_l,

@@ -50,7 +50,7 @@ typedef enum {
     MK_ERR_ALIGN = 4,       /* a pointer is not aligned as required */
     MK_ERR_WORKSPACE = 5,   /* decode workspace missing or too small */
     MK_ERR_HIP = 6,         /* the HIP runtime refused a launch */
-    MK_ERR_ARG = 7          /* non-finite scale, bad causal flag or split */
+    MK_ERR_ARG = 7          /* non-finite scale, bad causal flag or part count */
 } mk_status;
 
 /*
@@ -80,37 +80,53 @@ int mk_attn_fwd_o32(const void *q, const void *k, const void *v, float *o, float
                     int causal, float scale, const int *kv_seqlens, void *stream);
 
 /*
- * Bytes of caller-owned device workspace mk_attn_decode needs for these
- * sizes: per-split partial outputs [B, Hq, nsplit, D] fp32 and their
- * LSEs [B, Hq, nsplit] fp32, nsplit = ceil(Smax / split), each region
- * 256-byte aligned.  split = 0 selects the library default (the value
- * mk_attn_decode would use).  Returns 0 for invalid sizes.
- */
-size_t mk_attn_decode_workspace_bytes(int B, int Hq, int Smax, int D, int split);
-
-/*
- * Decode step: one query token per sequence against a key/value cache,
- * split along the keys, each split attended on its own, and the splits
- * merged by their log-sum-exp (two kernels on `stream`).
+ * Decode step: one query token per sequence against a key/value cache
+ * (the decode step of the paper's paged-attention workloads, Table 2),
+ * computed as split-KV attention whose per-split results are merged by
+ * their log-sum-exp.  The splits are cut so that every wave streams the
+ * same number of cache bytes: the keys of all (batch, kv head) pairs, in
+ * 32-key stages, are laid end to end (pair b * Hkv + g after pair
+ * b * Hkv + g - 1) and this stream is cut into n_parts equal parts, one
+ * wave each.  A pair that lies inside one part is attended and written by
+ * that wave alone; a pair cut by part boundaries is attended piecewise and
+ * its pieces are merged by a second kernel.  Two kernels on `stream`.
  *   q                 [B, Hq, D] bf16
  *   k_cache, v_cache  [B, Hkv, Smax, D] bf16; positions >= L_b are never read
  *   o                 [B, Hq, D] bf16 (written)
- *   lse               [B, Hq] fp32 (written), or NULL to skip
+ *   lse               [B, Hq] fp32 natural-log LSE (written), or NULL to skip
  *   kv_seqlens        device int32 [B] (required), clamped into [0, Smax];
- *                     query (b, hq) attends to keys [0, L_b)
- *   Hq / Hkv must be at most 16.
- *   split             keys per split, a multiple of 64 (0 = default)
- *   workspace         device buffer of workspace_bytes >=
- *                     mk_attn_decode_workspace_bytes(B, Hq, Smax, D, split)
- * The workspace must not be shared by overlapping calls.
+ *                     query (b, hq) attends to keys [0, L_b); L_b = 0 gives
+ *                     O = 0, LSE = -inf
+ *   Hq / Hkv must be at most 16; B * Hq and B * Hkv * ceil(Smax / 32) must
+ *   fit in 31 bits (MK_ERR_SHAPE otherwise).
+ *   n_parts           waves the key stream is cut into, 1 .. 2^20
+ *                     (0 = mk_attn_decode_default_parts(Hq, Hkv, D));
+ *                     any value gives the same result up to rounding
+ *   workspace         device buffer, 256-byte aligned, of workspace_bytes >=
+ *                     mk_attn_decode_workspace_bytes(Hq, Hkv, D, n_parts);
+ *                     its contents need no initialisation and are left
+ *                     undefined
+ * The workspace must not be shared by calls that may overlap in time.
  */
 int mk_attn_decode(const void *q, const void *k_cache, const void *v_cache, void *o,
                    float *lse, int B, int Hq, int Hkv, int Smax, int D, float scale,
-                   const int *kv_seqlens, int split, void *workspace,
+                   const int *kv_seqlens, int n_parts, void *workspace,
                    size_t workspace_bytes, void *stream);
 
-/* Default keys per split used when split = 0. */
-int mk_attn_decode_default_split(void);
+/*
+ * Bytes of decode workspace for these sizes: per part, two partial outputs
+ * [2, G, D] fp32 (the part's first and last piece, G = Hq / Hkv) and their
+ * LSEs [2, G] fp32, the two regions 256-byte aligned.  n_parts = 0 selects
+ * the default.  Independent of B and Smax.  Returns 0 for invalid sizes.
+ */
+size_t mk_attn_decode_workspace_bytes(int Hq, int Hkv, int D, int n_parts);
+
+/*
+ * Parts used when n_parts = 0: 256 compute units times the single-wave
+ * workgroups one compute unit holds at once (bounded by LDS), or 0 for
+ * invalid sizes.
+ */
+int mk_attn_decode_default_parts(int Hq, int Hkv, int D);
 
 /* Static string naming a status code ("MK_OK", ...); never NULL. */
 const char *mk_status_str(int status);

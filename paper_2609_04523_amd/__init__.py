@@ -17,12 +17,14 @@ import os
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libmk_attn.so")
 
+DECODE_MAX_PARTS = 1 << 20  # largest n_parts
+
 MK_STATUS = {0: "MK_OK", 1: "MK_ERR_NULL", 2: "MK_ERR_SHAPE", 3: "MK_ERR_UNSUPPORTED",
              4: "MK_ERR_ALIGN", 5: "MK_ERR_WORKSPACE", 6: "MK_ERR_HIP", 7: "MK_ERR_ARG"}
 
 # every symbol include/mk_attn.h declares
 EXPORTS = ("mk_attn_fwd", "mk_attn_fwd_o32", "mk_attn_decode_workspace_bytes",
-           "mk_attn_decode", "mk_attn_decode_default_split", "mk_status_str",
+           "mk_attn_decode", "mk_attn_decode_default_parts", "mk_status_str",
            "mk_attn_version")
 
 
@@ -49,12 +51,12 @@ def lib():
         h.mk_attn_fwd.restype = i
         h.mk_attn_fwd_o32.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, vp, vp]
         h.mk_attn_fwd_o32.restype = i
-        h.mk_attn_decode_workspace_bytes.argtypes = [i, i, i, i, i]
+        h.mk_attn_decode_workspace_bytes.argtypes = [i, i, i, i]
         h.mk_attn_decode_workspace_bytes.restype = sz
         h.mk_attn_decode.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, f, vp, i, vp, sz, vp]
         h.mk_attn_decode.restype = i
-        h.mk_attn_decode_default_split.argtypes = []
-        h.mk_attn_decode_default_split.restype = i
+        h.mk_attn_decode_default_parts.argtypes = [i, i, i]
+        h.mk_attn_decode_default_parts.restype = i
         h.mk_status_str.argtypes = [i]
         h.mk_status_str.restype = ctypes.c_char_p
         h.mk_attn_version.argtypes = []
@@ -71,12 +73,12 @@ def mk_attn_version() -> int:
     return lib().mk_attn_version()
 
 
-def mk_attn_decode_default_split() -> int:
-    return lib().mk_attn_decode_default_split()
+def mk_attn_decode_default_parts(Hq: int, Hkv: int, D: int) -> int:
+    return lib().mk_attn_decode_default_parts(Hq, Hkv, D)
 
 
-def mk_attn_decode_workspace_bytes(B: int, Hq: int, Smax: int, D: int, split: int = 0) -> int:
-    return lib().mk_attn_decode_workspace_bytes(B, Hq, Smax, D, split)
+def mk_attn_decode_workspace_bytes(Hq: int, Hkv: int, D: int, n_parts: int = 0) -> int:
+    return lib().mk_attn_decode_workspace_bytes(Hq, Hkv, D, n_parts)
 
 
 def _check(rc: int):
@@ -117,9 +119,9 @@ def mk_attn_fwd_o32(q, k, v, o, lse, B, Hq, Hkv, Sq, Skv, D, causal, scale, kv_s
 
 
 def mk_attn_decode(q, k_cache, v_cache, o, lse, B, Hq, Hkv, Smax, D, scale, kv_seqlens,
-                   split, workspace, workspace_bytes, stream=None):
+                   n_parts, workspace, workspace_bytes, stream=None):
     _check(lib().mk_attn_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(o), _ptr(lse), B,
-                                Hq, Hkv, Smax, D, float(scale), _ptr(kv_seqlens), int(split),
+                                Hq, Hkv, Smax, D, float(scale), _ptr(kv_seqlens), int(n_parts),
                                 _ptr(workspace), int(workspace_bytes), _stream(stream)))
 
 
@@ -155,7 +157,7 @@ def fwd(q, k, v, *, causal: bool = True, scale: float | None = None, kv_seqlens=
     return o, lse
 
 
-def decode(q, k_cache, v_cache, kv_seqlens, *, scale: float | None = None, split: int = 0,
+def decode(q, k_cache, v_cache, kv_seqlens, *, scale: float | None = None, n_parts: int = 0,
            workspace=None, with_lse: bool = True, stream=None):
     """q [B,Hq,D], caches [B,Hkv,Smax,D] bf16, kv_seqlens int32 [B] -> (o, lse)."""
     import torch
@@ -167,27 +169,28 @@ def decode(q, k_cache, v_cache, kv_seqlens, *, scale: float | None = None, split
     _, Hkv, Smax, _ = k_cache.shape
     if scale is None:
         scale = D ** -0.5
-    need = mk_attn_decode_workspace_bytes(B, Hq, Smax, D, split)
+    need = mk_attn_decode_workspace_bytes(Hq, Hkv, D, n_parts)
     if workspace is None:
         workspace = torch.empty(need, device=q.device, dtype=torch.uint8)
     o = torch.empty((B, Hq, D), device=q.device, dtype=torch.bfloat16)
     lse = torch.empty((B, Hq), device=q.device, dtype=torch.float32) if with_lse else None
-    mk_attn_decode(q, k_cache, v_cache, o, lse, B, Hq, Hkv, Smax, D, scale, kv_seqlens, split,
+    mk_attn_decode(q, k_cache, v_cache, o, lse, B, Hq, Hkv, Smax, D, scale, kv_seqlens, n_parts,
                    workspace, workspace.numel() * workspace.element_size(), stream)
     return o, lse
 
 
-def decode_partials(workspace, B: int, Hq: int, Smax: int, D: int, split: int = 0):
-    """Views of a decode workspace: (o_part [B,Hq,nsplit,D], lse_part [B,Hq,nsplit]) fp32.
+def decode_partials(workspace, Hq: int, Hkv: int, D: int, n_parts: int = 0):
+    """Views of a decode workspace: (o_part [P,2,G,D], lse_part [P,2,G]) fp32.
 
-    Splits at or past a sequence's end are not written by the library."""
+    Slot 0 of part w holds its first piece and slot 1 its last, when that
+    piece is part of a cut pair (see include/mk_attn.h); other entries are
+    not written by the library."""
     import torch
-    if split == 0:
-        split = mk_attn_decode_default_split()
-    nsplit = -(-Smax // split)
-    n_o = B * Hq * nsplit * D
+    P = n_parts if n_parts else mk_attn_decode_default_parts(Hq, Hkv, D)
+    G = Hq // Hkv
+    n_o = P * 2 * G * D
     lse_off = -(-(n_o * 4) // 256) * 256
     flat = workspace.view(torch.uint8)
-    o_part = flat[: n_o * 4].view(torch.float32).view(B, Hq, nsplit, D)
-    lse_part = flat[lse_off: lse_off + B * Hq * nsplit * 4].view(torch.float32).view(B, Hq, nsplit)
+    o_part = flat[: n_o * 4].view(torch.float32).view(P, 2, G, D)
+    lse_part = flat[lse_off: lse_off + P * 2 * G * 4].view(torch.float32).view(P, 2, G)
     return o_part, lse_part

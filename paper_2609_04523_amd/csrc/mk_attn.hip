@@ -12,9 +12,11 @@
 
 namespace {
 
-constexpr int kVersion = 1;
+constexpr int kVersion = 2;
 constexpr int kFwdQB = 1;             // 32-query blocks per wave in the forward kernel
-constexpr int kDefaultSplit = 384;    // decode keys per split (not a power of two: see decode_kernel.hpp)
+constexpr int kComputeUnits = 256;    // MI355X
+constexpr int kLdsPerCu = 160 * 1024; // gfx950
+constexpr int kMaxParts = 1 << 20;    // decode parts per call
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -83,22 +85,46 @@ int fwd_impl(const void* q, const void* k, const void* v, void* o, float* lse, i
   return e == hipSuccess ? MK_OK : MK_ERR_HIP;
 }
 
+// Decode workspace: o_part [P, 2, G, D] fp32, then lse_part [P, 2, G]
+// fp32 at a 256-byte aligned offset.
 struct DecLayout {
-  int split, nsplit;
+  int parts;
   size_t o_bytes, lse_off, total;
 };
 
-bool dec_layout(int B, int Hq, int Smax, int D, int split, DecLayout* out) {
-  if (B < 1 || Hq < 1 || Smax < 1 || D < 1 || split < 0) return false;
-  if (split == 0) split = kDefaultSplit;
+// ring-slot variant (16-byte Q chunks per 1 KB load) of a head dim and group
+int dec_qblocks(int D, int G) {
+  const int rows_per_kb = 512 / D;
+  const int need = (G + rows_per_kb - 1) / rows_per_kb;
+  return need <= 1 ? 1 : (need <= 2 ? 2 : 4);
+}
+
+int dec_lds_bytes(int D, int G) {
+  return 3 * (2 * mk::kDecStageKeys * D * 2 + dec_qblocks(D, G) * 1024);
+}
+
+int dec_default_parts(int D, int G) {
+  const int per_cu = kLdsPerCu / dec_lds_bytes(D, G);
+  return kComputeUnits * (per_cu < 1 ? 1 : per_cu);
+}
+
+bool dec_layout(int Hq, int Hkv, int D, int n_parts, DecLayout* out) {
+  if (Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || (D != 64 && D != 128)) return false;
+  if (n_parts < 0 || n_parts > kMaxParts) return false;
+  const int G = Hq / Hkv;
+  if (G > 16) return false;
   DecLayout l;
-  l.split = split;
-  l.nsplit = (Smax + split - 1) / split;
-  l.o_bytes = (size_t)B * Hq * l.nsplit * D * sizeof(float);
+  l.parts = n_parts == 0 ? dec_default_parts(D, G) : n_parts;
+  l.o_bytes = (size_t)l.parts * 2 * G * D * sizeof(float);
   l.lse_off = round_up(l.o_bytes, 256);
-  l.total = l.lse_off + round_up((size_t)B * Hq * l.nsplit * sizeof(float), 256);
+  l.total = l.lse_off + round_up((size_t)l.parts * 2 * G * sizeof(float), 256);
   *out = l;
   return true;
+}
+
+template <int D, int QB>
+void launch_dec(const mk::DecArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((mk::dec_part_kernel<D, QB>), dim3(a.P), dim3(64), 0, st, a);
 }
 
 }  // namespace
@@ -119,30 +145,38 @@ int mk_attn_fwd_o32(const void* q, const void* k, const void* v, float* o, float
                   true);
 }
 
-size_t mk_attn_decode_workspace_bytes(int B, int Hq, int Smax, int D, int split) {
+size_t mk_attn_decode_workspace_bytes(int Hq, int Hkv, int D, int n_parts) {
   DecLayout l;
-  if (!dec_layout(B, Hq, Smax, D, split, &l)) return 0;
+  if (!dec_layout(Hq, Hkv, D, n_parts, &l)) return 0;
   return l.total;
 }
 
-int mk_attn_decode_default_split(void) { return kDefaultSplit; }
+int mk_attn_decode_default_parts(int Hq, int Hkv, int D) {
+  DecLayout l;
+  if (!dec_layout(Hq, Hkv, D, 0, &l)) return 0;
+  return l.parts;
+}
 
 int mk_attn_decode(const void* q, const void* k_cache, const void* v_cache, void* o, float* lse,
                    int B, int Hq, int Hkv, int Smax, int D, float scale, const int* kv_seqlens,
-                   int split, void* workspace, size_t workspace_bytes, void* stream) {
+                   int n_parts, void* workspace, size_t workspace_bytes, void* stream) {
   if (!q || !k_cache || !v_cache || !o || !kv_seqlens) return MK_ERR_NULL;
   if (B < 1 || Hq < 1 || Hkv < 1 || Smax < 1 || D < 1) return MK_ERR_SHAPE;
   if (Hq % Hkv != 0) return MK_ERR_SHAPE;
+  // stage indices and (batch, head) rows are 32-bit in the kernels
+  const long long max_stages = (long long)B * Hkv * ((Smax + mk::kDecStageKeys - 1) /
+                                                     mk::kDecStageKeys);
+  if ((long long)B * Hq > 0x7fffffffLL || max_stages > 0x7fffffffLL) return MK_ERR_SHAPE;
   if (D != 64 && D != 128) return MK_ERR_UNSUPPORTED;
   if (Hq / Hkv > 16) return MK_ERR_UNSUPPORTED;
-  if (split < 0) return MK_ERR_ARG;
+  if (n_parts < 0 || n_parts > kMaxParts) return MK_ERR_ARG;
   if (!isfinite(scale)) return MK_ERR_ARG;
   if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(o, 16) ||
       !aligned(kv_seqlens, 4))
     return MK_ERR_ALIGN;
   if (lse && !aligned(lse, 4)) return MK_ERR_ALIGN;
   DecLayout l;
-  if (!dec_layout(B, Hq, Smax, D, split, &l)) return MK_ERR_SHAPE;
+  if (!dec_layout(Hq, Hkv, D, n_parts, &l)) return MK_ERR_SHAPE;
   if (!workspace || workspace_bytes < l.total) return MK_ERR_WORKSPACE;
   if (!aligned(workspace, 256)) return MK_ERR_ALIGN;
 
@@ -152,6 +186,8 @@ int mk_attn_decode(const void* q, const void* k_cache, const void* v_cache, void
   a.q = static_cast<const uint16_t*>(q);
   a.kc = static_cast<const uint16_t*>(k_cache);
   a.vc = static_cast<const uint16_t*>(v_cache);
+  a.o = static_cast<uint16_t*>(o);
+  a.lse = lse;
   a.o_part = reinterpret_cast<float*>(ws);
   a.lse_part = reinterpret_cast<float*>(ws + l.lse_off);
   a.kv_seqlens = kv_seqlens;
@@ -159,34 +195,23 @@ int mk_attn_decode(const void* q, const void* k_cache, const void* v_cache, void
   a.Hq = Hq;
   a.Hkv = Hkv;
   a.Smax = Smax;
-  a.split = l.split;
-  a.nsplit = l.nsplit;
+  a.P = l.parts;
   a.scale_log2 = scale * mk::kLog2e;
-  const long long n_items = (long long)l.nsplit * Hkv * B;
-  if (n_items > 0x7fffffffLL) return MK_ERR_SHAPE;
-  const dim3 grid((unsigned)n_items);
-  if (D == 128)
-    hipLaunchKernelGGL(mk::dec_split_kernel<128>, grid, dim3(64), 0, st, a);
-  else
-    hipLaunchKernelGGL(mk::dec_split_kernel<64>, grid, dim3(64), 0, st, a);
+  const int qb = dec_qblocks(D, Hq / Hkv);
+  if (D == 128) {
+    if (qb == 1) launch_dec<128, 1>(a, st);
+    else if (qb == 2) launch_dec<128, 2>(a, st);
+    else launch_dec<128, 4>(a, st);
+  } else {
+    if (qb == 1) launch_dec<64, 1>(a, st);
+    else launch_dec<64, 2>(a, st);
+  }
   if (hipGetLastError() != hipSuccess) return MK_ERR_HIP;
-
-  mk::CombArgs c;
-  c.o_part = a.o_part;
-  c.lse_part = a.lse_part;
-  c.kv_seqlens = kv_seqlens;
-  c.o = o;
-  c.lse = lse;
-  c.B = B;
-  c.Hq = Hq;
-  c.Smax = Smax;
-  c.split = l.split;
-  c.nsplit = l.nsplit;
-  const unsigned cblocks = (unsigned)((B * Hq + 3) / 4);
+  const unsigned mblocks = (unsigned)(((long long)B * Hq + 3) / 4);  // one wave per row
   if (D == 128)
-    hipLaunchKernelGGL(mk::dec_combine_kernel<128>, dim3(cblocks), dim3(256), 0, st, c);
+    hipLaunchKernelGGL(mk::dec_merge_kernel<128>, dim3(mblocks), dim3(256), 0, st, a);
   else
-    hipLaunchKernelGGL(mk::dec_combine_kernel<64>, dim3(cblocks), dim3(256), 0, st, c);
+    hipLaunchKernelGGL(mk::dec_merge_kernel<64>, dim3(mblocks), dim3(256), 0, st, a);
   return hipGetLastError() == hipSuccess ? MK_OK : MK_ERR_HIP;
 }
 
@@ -199,7 +224,7 @@ const char* mk_status_str(int status) {
     case MK_ERR_ALIGN: return "MK_ERR_ALIGN: a pointer is not aligned as required";
     case MK_ERR_WORKSPACE: return "MK_ERR_WORKSPACE: decode workspace missing or too small";
     case MK_ERR_HIP: return "MK_ERR_HIP: the HIP runtime refused a launch";
-    case MK_ERR_ARG: return "MK_ERR_ARG: non-finite scale, bad causal flag or split";
+    case MK_ERR_ARG: return "MK_ERR_ARG: non-finite scale, bad causal flag or part count";
     default: return "MK_ERR_UNKNOWN: not an mk_status value";
   }
 }

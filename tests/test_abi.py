@@ -43,7 +43,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert mk.mk_attn_version() == 1
+    assert mk.mk_attn_version() == 2
     names = ["MK_OK", "MK_ERR_NULL", "MK_ERR_SHAPE", "MK_ERR_UNSUPPORTED", "MK_ERR_ALIGN",
              "MK_ERR_WORKSPACE", "MK_ERR_HIP", "MK_ERR_ARG"]
     for code, name in enumerate(names):
@@ -84,11 +84,10 @@ def test_fwd_validation(lib, o32):
 
 
 def dec_rc(lib, *, q=P, kc=P, vc=P, o=P, lse=None, B=2, Hq=8, Hkv=2, Smax=512, D=128,
-           scale=0.1, seqlens=P, split=0, ws=P, ws_bytes=None):
+           scale=0.1, seqlens=P, parts=0, ws=P, ws_bytes=None):
     if ws_bytes is None:
-        ws_bytes = lib.mk_attn_decode_workspace_bytes(max(B, 1), max(Hq, 1), max(Smax, 1),
-                                                      D, max(split, 0))
-    return lib.mk_attn_decode(q, kc, vc, o, lse, B, Hq, Hkv, Smax, D, scale, seqlens, split, ws,
+        ws_bytes = lib.mk_attn_decode_workspace_bytes(max(Hq, 1), max(Hkv, 1), D, max(parts, 0))
+    return lib.mk_attn_decode(q, kc, vc, o, lse, B, Hq, Hkv, Smax, D, scale, seqlens, parts, ws,
                               ws_bytes, None)
 
 
@@ -98,37 +97,54 @@ def test_decode_validation(lib):
     for name in ("B", "Hq", "Hkv", "Smax"):
         assert dec_rc(lib, **{name: 0}) == 2
     assert dec_rc(lib, Hq=6, Hkv=4) == 2
-    # more work items than one launch can hold
+    # (batch, head) rows or key stages past 32-bit indexing
     assert dec_rc(lib, B=1 << 20, Hq=4096, Hkv=4096) == 2
+    assert dec_rc(lib, B=1 << 16, Hq=8, Hkv=2, Smax=1 << 20) == 2
     assert dec_rc(lib, D=96) == 3
     assert dec_rc(lib, Hq=34, Hkv=2) == 3  # group of 17 query heads
-    assert dec_rc(lib, split=-1, ws_bytes=1 << 30) == 7
+    assert dec_rc(lib, parts=-1, ws_bytes=1 << 30) == 7
+    assert dec_rc(lib, parts=mk.DECODE_MAX_PARTS + 1, ws_bytes=1 << 40) == 7
     assert dec_rc(lib, scale=math.nan) == 7
     for name in ("q", "kc", "vc", "o"):
         assert dec_rc(lib, **{name: P_ODD}) == 4
     assert dec_rc(lib, seqlens=P + 2) == 4
     assert dec_rc(lib, lse=P + 1) == 4
     assert dec_rc(lib, ws=None) == 5
-    need = lib.mk_attn_decode_workspace_bytes(2, 8, 512, 128, 0)
+    need = lib.mk_attn_decode_workspace_bytes(8, 2, 128, 0)
     assert dec_rc(lib, ws_bytes=need - 1) == 5
+    assert dec_rc(lib, parts=100, ws_bytes=lib.mk_attn_decode_workspace_bytes(8, 2, 128, 99)) == 5
     assert dec_rc(lib, ws=P + 16) == 4  # workspace must be 256-byte aligned
 
 
+def test_decode_default_parts(lib):
+    # 256 compute units x the single-wave workgroups whose LDS ring (three
+    # slots of K and V for 32 keys plus the group's query rows in 1 KB
+    # loads) fits in 160 KiB
+    def expect(G, D):
+        q_kb = -(-G // (512 // D))
+        q_kb = 1 if q_kb <= 1 else (2 if q_kb <= 2 else 4)
+        ring = 3 * (2 * 32 * D * 2 + q_kb * 1024)
+        return 256 * max(1, (160 * 1024) // ring)
+    for Hq, Hkv, D in ((32, 8, 128), (8, 1, 128), (16, 1, 128), (4, 4, 64), (16, 1, 64)):
+        assert mk.mk_attn_decode_default_parts(Hq, Hkv, D) == expect(Hq // Hkv, D)
+    assert mk.mk_attn_decode_default_parts(32, 8, 128) == 768
+    assert mk.mk_attn_decode_default_parts(34, 2, 128) == 0
+    assert mk.mk_attn_decode_default_parts(6, 4, 128) == 0
+    assert mk.mk_attn_decode_default_parts(8, 2, 96) == 0
+
+
 def test_decode_workspace_size(lib):
-    split = mk.mk_attn_decode_default_split()
-    assert split > 0
-    B, Hq, Smax, D = 64, 32, 4096, 128
-    nsplit = -(-Smax // split)
-    o_bytes = B * Hq * nsplit * D * 4
-    lse_bytes = B * Hq * nsplit * 4
     rnd = lambda x: -(-x // 256) * 256
-    assert lib.mk_attn_decode_workspace_bytes(B, Hq, Smax, D, 0) == rnd(o_bytes) + rnd(lse_bytes)
-    assert lib.mk_attn_decode_workspace_bytes(B, Hq, Smax, D, split) == \
-        lib.mk_attn_decode_workspace_bytes(B, Hq, Smax, D, 0)
-    # split 1000 -> 5 splits over 4096 keys
-    assert lib.mk_attn_decode_workspace_bytes(1, 1, 4096, 64, 1000) == rnd(5 * 64 * 4) + rnd(5 * 4)
-    assert lib.mk_attn_decode_workspace_bytes(0, 1, 1, 64, 0) == 0
-    assert lib.mk_attn_decode_workspace_bytes(1, 1, 1, 64, -1) == 0
+    for Hq, Hkv, D, P in ((32, 8, 128, 768), (16, 1, 64, 3), (4, 4, 128, 1)):
+        G = Hq // Hkv
+        want = rnd(P * 2 * G * D * 4) + rnd(P * 2 * G * 4)
+        assert lib.mk_attn_decode_workspace_bytes(Hq, Hkv, D, P) == want
+    assert lib.mk_attn_decode_workspace_bytes(32, 8, 128, 0) == \
+        lib.mk_attn_decode_workspace_bytes(32, 8, 128, 768)
+    assert lib.mk_attn_decode_workspace_bytes(0, 1, 64, 0) == 0
+    assert lib.mk_attn_decode_workspace_bytes(8, 2, 64, -1) == 0
+    assert lib.mk_attn_decode_workspace_bytes(8, 2, 80, 0) == 0
+    assert lib.mk_attn_decode_workspace_bytes(8, 2, 64, mk.DECODE_MAX_PARTS + 1) == 0
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):

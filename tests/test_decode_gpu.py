@@ -27,13 +27,13 @@ def poison_padding(cache: torch.Tensor, lens) -> torch.Tensor:
     return c
 
 
-def run_decode(q, kc, vc, lens, *, scale, split=0, return_ws=False):
+def run_decode(q, kc, vc, lens, *, scale, n_parts=0, return_ws=False):
     sl = torch.as_tensor(np.asarray(lens, dtype=np.int32)).to(DEV)
     B, Hq, D = q.shape
-    Smax = kc.shape[2]
-    ws = torch.empty(mk.mk_attn_decode_workspace_bytes(B, Hq, Smax, D, split), device=DEV,
+    Hkv = kc.shape[1]
+    ws = torch.empty(mk.mk_attn_decode_workspace_bytes(Hq, Hkv, D, n_parts), device=DEV,
                      dtype=torch.uint8)
-    o, lse = mk.decode(q.to(DEV), kc.to(DEV), vc.to(DEV), sl, scale=scale, split=split,
+    o, lse = mk.decode(q.to(DEV), kc.to(DEV), vc.to(DEV), sl, scale=scale, n_parts=n_parts,
                        workspace=ws)
     torch.cuda.synchronize()
     return (o, lse, ws) if return_ws else (o, lse)
@@ -53,14 +53,15 @@ def test_decode_config5_full_with_poisoned_padding():
     assert_parity(cfg.name, o, lse, o_ref, lse_ref)
 
 
-@pytest.mark.parametrize("split", [0, 64, 100, 512, 1000, 4096])
-def test_decode_split_lengths(split):
+@pytest.mark.parametrize("n_parts", [0, 1, 7, 100, 768, 5000])
+def test_decode_part_counts(n_parts):
+    # 5000 parts exceed the 1992 stages of this input: most parts are empty
     B, Hq, Hkv, Smax, D = 8, 32, 8, 2048, 128
     q, kc, vc, lens = workloads.decode_inputs(B, Hq, Hkv, Smax, D, seed=21, lmin=1, lmax=Smax)
     scale = D ** -0.5
-    o, lse = run_decode(q, kc, vc, lens, scale=scale, split=split)
+    o, lse = run_decode(q, kc, vc, lens, scale=scale, n_parts=n_parts)
     o_ref, lse_ref = oracle_decode(q, kc, vc, lens, scale)
-    assert_parity(f"split{split}", o, lse, o_ref, lse_ref)
+    assert_parity(f"parts{n_parts}", o, lse, o_ref, lse_ref)
 
 
 # name, B, Hq, Hkv, Smax, D, lens
@@ -71,6 +72,10 @@ SHAPES = [
     ("gqa4_lengths_edge", 4, 8, 2, 512, 128, [0, 1, 511, 512]),
     ("clamped_lengths", 3, 8, 2, 256, 128, [-7, 100000, 129]),
     ("single_key_cache", 2, 4, 1, 1, 128, [1, 1]),
+    ("all_empty", 2, 8, 2, 64, 128, [0, 0]),
+    ("many_short", 70, 4, 2, 40, 128, [(7 * b) % 41 for b in range(70)]),
+    ("gqa6_d128", 3, 12, 2, 300, 128, [300, 33, 150]),
+    ("gqa12_d64", 2, 12, 1, 200, 64, [1, 200]),
 ]
 
 
@@ -87,20 +92,92 @@ def test_decode_shapes(case):
     assert_parity(name, o, lse, o_ref, lse_ref)
 
 
-def test_decode_partials_match_oracle_split_steps():
+def stream_parts(T, P):
+    """Part boundaries the library documents: P equal parts, part w holding
+    stages [floor(w T / P), floor((w + 1) T / P))."""
+    return [(w * T // P, (w + 1) * T // P) for w in range(P)]
+
+
+def stream_pieces(lens, Hkv, Smax, P):
+    """Pieces of the stage stream: the 32-key stages of pairs (b, g), pair
+    after pair, cut at the part boundaries.  Yields (part, slot, b, g, key0,
+    key1, whole) per piece; slot 0 is a part's first piece, 1 its last."""
+    nts = [-(-max(0, min(int(L), Smax)) // 32) for L in lens]
+    T = Hkv * sum(nts)
+    pairs, A = [], 0
+    for b, nt in enumerate(nts):
+        for g in range(Hkv):
+            if nt:
+                pairs.append((A, A + nt, b, g))
+            A += nt
+    for p, (s0, s1) in enumerate(stream_parts(T, P)):
+        pieces = [(max(a0, s0), min(a1, s1), a0, a1, b, g) for a0, a1, b, g in pairs
+                  if a0 < s1 and a1 > s0]
+        for i, (p0, p1, a0, a1, b, g) in enumerate(pieces):
+            L = max(0, min(int(lens[b]), Smax))
+            yield (p, 0 if i == 0 else 1, b, g, 32 * (p0 - a0), min(32 * (p1 - a0), L),
+                   p0 == a0 and p1 == a1)
+
+
+def test_decode_pieces_match_oracle_on_their_keys():
+    # every cut piece in the workspace is the attention of its query heads
+    # over exactly its own keys
     B, Hq, Hkv, Smax, D = 4, 8, 2, 1500, 128
+    G = Hq // Hkv
     q, kc, vc, lens = workloads.decode_inputs(B, Hq, Hkv, Smax, D, seed=22, lmin=1, lmax=Smax)
     scale = D ** -0.5
-    split = 256
-    o, lse, ws = run_decode(q, kc, vc, lens, scale=scale, split=split, return_ws=True)
-    o_part, lse_part = mk.decode_partials(ws, B, Hq, Smax, D, split)
-    _, _, op_ref, lp_ref = orc.decode_split(workloads.bits(q), workloads.bits(kc),
-                                            workloads.bits(vc), lens.numpy(), scale=scale,
-                                            split=split)
-    for b in range(B):
-        ns = -(-int(lens[b]) // split)
-        assert_parity(f"partials b{b}", o_part[b, :, :ns], lse_part[b, :, :ns],
-                      op_ref[b, :, :ns], lp_ref[b, :, :ns])
+    P = 37
+    o, lse, ws = run_decode(q, kc, vc, lens, scale=scale, n_parts=P, return_ws=True)
+    o_part, lse_part = mk.decode_partials(ws, Hq, Hkv, D, P)
+    n_cut = 0
+    for p, slot, b, g, k0, k1, whole in stream_pieces(lens.tolist(), Hkv, Smax, P):
+        if whole:
+            continue
+        n_cut += 1
+        qs = q[b:b + 1, g * G:(g + 1) * G]
+        o_ref, lse_ref = oracle_decode(qs, kc[b:b + 1, g:g + 1, k0:k1].contiguous(),
+                                       vc[b:b + 1, g:g + 1, k0:k1].contiguous(), [k1 - k0],
+                                       scale)
+        assert_parity(f"piece p{p} s{slot} b{b} g{g} [{k0},{k1})", o_part[p, slot][None],
+                      lse_part[p, slot][None], o_ref, lse_ref)
+    assert n_cut > P // 2
+
+
+@pytest.mark.parametrize("n_parts", [3, 50])
+def test_decode_many_sequences_few_parts(n_parts):
+    # 130 sequences: the stream is located across several 64-sequence
+    # chunks and each part walks through many sequences, empty ones included
+    B, Hq, Hkv, Smax, D = 130, 8, 2, 300, 64
+    g = torch.Generator().manual_seed(31)
+    lens = torch.randint(0, Smax + 1, (B,), generator=g).tolist()
+    lens[5] = lens[64] = lens[129] = 0
+    q = torch.randn((B, Hq, D), generator=g).to(torch.bfloat16)
+    kc = torch.randn((B, Hkv, Smax, D), generator=g).to(torch.bfloat16)
+    vc = torch.randn((B, Hkv, Smax, D), generator=g).to(torch.bfloat16)
+    scale = D ** -0.5
+    o, lse = run_decode(q, poison_padding(kc, lens), poison_padding(vc, lens), lens, scale=scale,
+                        n_parts=n_parts)
+    o_ref, lse_ref = oracle_decode(q, kc, vc, lens, scale)
+    assert_parity(f"B130 parts{n_parts}", o, lse, o_ref, lse_ref)
+
+
+def test_decode_workspace_reuse_and_uninitialised_partials():
+    # one workspace, filled with NaN, for calls of different part counts:
+    # the library needs no initialised workspace contents
+    B, Hq, Hkv, Smax, D = 6, 16, 4, 900, 128
+    q, kc, vc, lens = workloads.decode_inputs(B, Hq, Hkv, Smax, D, seed=25, lmin=0, lmax=Smax)
+    scale = D ** -0.5
+    P_max = 200
+    ws = torch.empty(mk.mk_attn_decode_workspace_bytes(Hq, Hkv, D, P_max), device=DEV,
+                     dtype=torch.uint8)
+    ws.view(torch.float32).fill_(float("nan"))
+    o_ref, lse_ref = oracle_decode(q, kc, vc, lens, scale)
+    sl = lens.to(DEV)
+    for P in (200, 37, 1, 150, 37):
+        o, lse = mk.decode(q.to(DEV), kc.to(DEV), vc.to(DEV), sl, scale=scale, n_parts=P,
+                           workspace=ws)
+        torch.cuda.synchronize()
+        assert_parity(f"reuse P={P}", o, lse, o_ref, lse_ref)
 
 
 def test_decode_equals_last_prefill_row():
