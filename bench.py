@@ -3,14 +3,15 @@
 One step = one pass over the whole path on resident synthetic inputs:
   * the fused causal attention forward on the prefill workload
     (causal MHA B=4 H=16 S=2048 D=128 bf16 by default), then
-  * the split-KV decode (equal-work part kernel + LSE merge kernel) on the ragged decode
-    batch (B=64 Hq=32 Hkv=8 D=128, lengths in [512, 4096]), alternating
-    between two copies of the cache so the 256 MB last-level cache cannot
-    hand the previous step's cache to the next one.
+  * the split-KV decode (equal-work part kernel + LSE merge kernel) on the
+    ragged decode batch (B=64 Hq=32 Hkv=8 D=128, lengths in [512, 4096]).
+Each workload alternates between two copies of its inputs so the 256 MB
+last-level cache cannot hand one launch the previous launch's data.
 
-Kernel durations are taken with HIP events recorded on the stream the
-kernels are launched on (torch's current stream), around every launch of
-the timed steps.  Prints ONE JSON line on stdout; progress goes to stderr.
+The K timed steps run as K prefill launches back to back, then K decode
+launches back to back, on torch's current stream; HIP events recorded on
+that stream before, between and after give each kernel's average launch
+duration.  Prints ONE JSON line on stdout; progress goes to stderr.
 """
 from __future__ import annotations
 
@@ -75,8 +76,10 @@ def _short(name: str) -> str:
     return name.split("(")[0].replace("void ", "")
 
 
-def summarize_trace(path: str, command: str) -> str:
-    """Markdown table of per-kernel durations from a --kernel-trace run."""
+def summarize_trace(path: str, command: str, kernels=None) -> str:
+    """Markdown table of per-kernel durations from a --kernel-trace run,
+    restricted to kernels whose names contain one of `kernels` if given
+    (the GPU-time share stays relative to all kernels of the run)."""
     import sqlite3
     db = sqlite3.connect(_find_db(path))
     rows = db.execute("select name, duration from kernels").fetchall()
@@ -84,6 +87,8 @@ def summarize_trace(path: str, command: str) -> str:
     for name, dur in rows:
         agg.setdefault(_short(name), []).append(dur / 1e3)  # ns -> us
     total = sum(sum(v) for v in agg.values())
+    if kernels:
+        agg = {k: v for k, v in agg.items() if any(f in k for f in kernels)}
     out = ["# rocprofv3 kernel trace", "", f"command: `{command}`", "",
            f"kernel_source_digest: {kernel_source_digest()}", "",
            "| kernel | calls | avg us | min us | max us | % of GPU time |",
@@ -164,14 +169,19 @@ def main():
                     help="print a summary of a rocprofv3 --kernel-trace output and exit")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print per-launch HBM bytes from FETCH_SIZE / WRITE_SIZE runs and exit")
-    ap.add_argument("--kernels", default="fwd_kernel",
-                    help="comma-separated kernel name fragments for --summarize-pmc")
+    ap.add_argument("--kernels", default=None,
+                    help="comma-separated kernel name fragments for --summarize-pmc "
+                         "(default fwd_kernel) or --summarize-trace (default all)")
     ap.add_argument("--command", action="append", default=[],
                     help="command line(s) recorded in a summary")
     args = ap.parse_args()
+    args.kernels_given = args.kernels is not None
+    if args.kernels is None:
+        args.kernels = "fwd_kernel"
 
     if args.summarize_trace:
-        print(summarize_trace(args.summarize_trace, "; ".join(args.command)), end="")
+        kern = args.kernels.split(",") if args.kernels_given else None
+        print(summarize_trace(args.summarize_trace, "; ".join(args.command), kern), end="")
         return
     if args.summarize_pmc:
         print(summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1],
@@ -181,7 +191,8 @@ def main():
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
-              "(the path shards by kv-head groups across GPUs, see DESIGN.md)", file=sys.stderr)
+              "(the path would shard by (batch, kv head) groups, one group set per GPU)",
+              file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -201,9 +212,15 @@ def main():
     dcfg = workloads.CONFIGS[args.decode]
     log(f"[bench] inputs: prefill {pcfg.name}, decode {dcfg.name}")
     q, k, v = workloads.config_inputs(pcfg)
-    q, k, v = q.to(dev), k.to(dev), v.to(dev)
-    o = torch.empty(q.shape, device=dev, dtype=torch.float32 if pcfg.out_fp32 else torch.bfloat16)
-    lse = torch.empty(q.shape[:3], device=dev, dtype=torch.float32)
+    # two copies of the prefill tensors, used alternately, so that the
+    # 256 MB last-level cache cannot hand one launch the previous one's data
+    pre = []
+    for _ in range(2):
+        o = torch.empty(q.shape, device=dev,
+                        dtype=torch.float32 if pcfg.out_fp32 else torch.bfloat16)
+        lse = torch.empty(q.shape[:3], device=dev, dtype=torch.float32)
+        pre.append((q.to(dev), k.to(dev), v.to(dev), o, lse))
+    del q, k, v
     qd, kc, vc, lens = workloads.config_inputs(dcfg)
     caches = [(kc.to(dev), vc.to(dev)), (kc.to(dev).clone(), vc.to(dev).clone())]
     del kc, vc
@@ -220,7 +237,8 @@ def main():
     fwd_entry = mk.mk_attn_fwd_o32 if pcfg.out_fp32 else mk.mk_attn_fwd
     stream = torch.cuda.current_stream()
 
-    def prefill():
+    def prefill(i):
+        q, k, v, o, lse = pre[i & 1]
         fwd_entry(q, k, v, o, lse, pcfg.B, pcfg.Hq, pcfg.Hkv, pcfg.S, pcfg.S, pcfg.D, 1,
                   pcfg.scale, None, stream)
 
@@ -241,31 +259,32 @@ def main():
 
     log(f"[bench] warmup {args.warmup}")
     for i in range(args.warmup):
-        prefill()
+        prefill(i)
         decode(i)
     torch.cuda.synchronize()
 
     K = args.steps
-    # One event at every kernel boundary: ev[2i] before prefill i, ev[2i+1]
-    # between prefill i and decode i, ev[2i+2] after decode i (and before
-    # prefill i+1), so each launch is bracketed by exactly two markers.
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * K + 1)]
+    # The K steps run as K prefill launches back to back, then K decode
+    # launches back to back (each alternating its two input copies), with
+    # one event before, between and after: a marker between two kernels
+    # costs the command processor several microseconds, which per-launch
+    # events would add to every launch's measured duration.
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
     log(f"[bench] timing {K} steps")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev[0].record(stream)
     for i in range(K):
-        prefill()
-        ev[2 * i + 1].record(stream)
+        prefill(i)
+    ev[1].record(stream)
+    for i in range(K):
         decode(i)
-        ev[2 * i + 2].record(stream)
+    ev[2].record(stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / K
-    t_pre = [ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(K)]  # ms
-    t_dec = [ev[2 * i + 1].elapsed_time(ev[2 * i + 2]) for i in range(K)]
-    pre_ms = sum(t_pre) / K
-    dec_ms = sum(t_dec) / K
+    pre_ms = ev[0].elapsed_time(ev[1]) / K  # average launch duration
+    dec_ms = ev[1].elapsed_time(ev[2]) / K
     flops = pcfg.flops
     tflops = flops / (pre_ms * 1e-3) / 1e12
     sum_l = int(lens.clamp(0, Smax).sum())
