@@ -3,7 +3,7 @@
 // One workgroup = 4 waves = BM query rows of one (batch, query head); wave w
 // owns QB blocks of 32 consecutive rows.  The workgroup streams the 64-key
 // K and V tiles of its KV head (hq / (Hq/Hkv)) from HBM straight into LDS
-// (global_load_lds_dwordx4, two tiles in flight), up to the causal
+// (global_load_lds_dwordx4, double-buffered), up to the causal
 // diagonal, and keeps the softmax state and the output accumulator in
 // registers: online softmax, an exact rewrite of softmax(Q K^T * scale) V
 // folded tile by tile.
@@ -99,6 +99,10 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   constexpr int TILE = BN * D;            // bf16 per tile per tensor
   constexpr int TILE_BYTES = TILE * 2;
   constexpr int ROW_BYTES = D * 2;
+  constexpr int NK = 2 * S::KSTEPS;     // K fragment reads per tile
+  constexpr int NV = 8 * S::DBLK;       // transposing V reads per tile
+  constexpr int RW = 8;                 // LDS reads in flight
+  static_assert(RW >= 2 && RW % 2 == 0 && RW <= NK && RW <= NV, "read window");
   __shared__ __attribute__((aligned(1024))) uint16_t k_lds[2][TILE];
   __shared__ __attribute__((aligned(1024))) uint16_t v_lds[2][TILE];
 
@@ -157,19 +161,19 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   const int dma_ch = ((lane % S::CHUNKS) ^ fwd_swz<D>(dma_row)) * 16;  // byte offset
   const uint32_t k_lds_w = __builtin_amdgcn_readfirstlane(lds_addr(&k_lds[0][0]) + wave * 1024);
   const uint32_t v_lds_w = __builtin_amdgcn_readfirstlane(lds_addr(&v_lds[0][0]) + wave * 1024);
-  auto issue_tile = [&](int kt, auto buf_tag) {
+  auto issue_block = [&](int kt, auto buf_tag, auto p_tag) {
     constexpr int BUF = decltype(buf_tag)::value;
+    constexpr int P = decltype(p_tag)::value;
     const int lim = L - 1 - kt * BN;  // last valid row of the tile
-    const char* kt_g = kg + (size_t)kt * BN * ROW_BYTES;
-    const char* vt_g = vg + (size_t)kt * BN * ROW_BYTES;
-#pragma unroll
-    for (int p = 0; p < S::BLOCKS_PER_WAVE; ++p) {
-      const uint32_t goff = (uint32_t)(min(dma_row, lim - p * ROW_STEP) * ROW_BYTES + dma_ch) +
-                            p * ROW_STEP * ROW_BYTES;
-      const uint32_t lds_off = BUF * TILE_BYTES + p * S::WAVES * 1024;
-      load_lds16_at(kt_g + goff, k_lds_w + lds_off);
-      load_lds16_at(vt_g + goff, v_lds_w + lds_off);
-    }
+    const uint32_t goff = (uint32_t)(min(dma_row, lim - P * ROW_STEP) * ROW_BYTES + dma_ch) +
+                          P * ROW_STEP * ROW_BYTES;
+    const size_t toff = (size_t)kt * BN * ROW_BYTES;
+    constexpr uint32_t lds_off = BUF * TILE_BYTES + P * S::WAVES * 1024;
+    load_lds16_at(kg + toff + goff, k_lds_w + lds_off);
+    load_lds16_at(vg + toff + goff, v_lds_w + lds_off);
+  };
+  auto issue_tile = [&](int kt, auto buf_tag) {
+    static_for<0, S::BLOCKS_PER_WAVE>([&](auto p_tag) { issue_block(kt, buf_tag, p_tag); });
   };
 
   float m_run[QB], l_run[QB];
@@ -187,7 +191,6 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   using B0 = std::integral_constant<int, 0>;
   using B1 = std::integral_constant<int, 1>;
   if (n_kt > 0) issue_tile(0, B0());
-  if (n_kt > 1) issue_tile(1, B1());
 
   // Lane parts of the LDS read addresses (bytes within a tile).  K row
   // 32 kb + n: the swizzle of n + 32 kb equals that of n.  Transposing V
@@ -215,11 +218,16 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
 
   // One 64-key tile for this wave from LDS buffer BUF.  MASK: apply the
   // length / causal mask.
-  auto tile = [&](auto mask_tag, auto buf_tag, int kt) {
+  auto tile = [&](auto mask_tag, auto buf_tag, int kt, auto&& qk_hook) {
     constexpr bool MASK = decltype(mask_tag)::value;
     constexpr int BUF = decltype(buf_tag)::value;
     const int key0 = kt * BN;
     // ---- S^T = K Q^T for the 64 keys of the tile ----
+    // The tile's LDS reads form one stream: the NK K fragments (step s,
+    // key block kb, alternating kb so that two accumulator chains are in
+    // flight), then the NV transposing V reads in the order the P V
+    // products consume them.  RW reads are kept in flight: consuming one
+    // issues the next, so V's first reads are under way during the softmax.
     f32x16 sacc[QB][2];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb)
@@ -227,17 +235,31 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) sacc[qb][kb][r] = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int s = 0; s < S::KSTEPS; ++s) {
-        const bf16x8 kf = as_bf16x8(*reinterpret_cast<const __attribute__((address_space(3)))
-                                                           u32x4*>(
-            (uintptr_t)(k_addr[s] + BUF * TILE_BYTES + kb * 32 * ROW_BYTES)));
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) sacc[qb][kb] = mfma32(kf, qf[qb][s], sacc[qb][kb]);
+    u32x4 kr[NK];
+    u32x2 vr[NV];
+    auto issue_read = [&](auto j_tag) {
+      constexpr int J = decltype(j_tag)::value;
+      if constexpr (J < NK) {
+        constexpr int OFF = BUF * TILE_BYTES + (J % 2) * 32 * ROW_BYTES;
+        kr[J] = lds_read_b128_async_off<OFF>(k_addr[J / 2]);
+      } else if constexpr (J < NK + NV) {
+        constexpr int V = J - NK;        // (kc, db, hh) = V / (2 DBLK), V / 2 % DBLK, V % 2
+        constexpr int OFF = BUF * TILE_BYTES + (V / (2 * S::DBLK)) * 16 * ROW_BYTES;
+        vr[V] = lds_read_tr16_async_off<OFF>(v_addr[(V / 2) % S::DBLK][V % 2]);
       }
-    }
+    };
+    static_for<0, RW>(issue_read);
+    static_for<0, NK>([&](auto i_tag) {
+      constexpr int I = decltype(i_tag)::value;
+      lds_wait_lgkm<RW - 1>();
+      lds_ready(kr[I]);
+      const bf16x8 kf = as_bf16x8(kr[I]);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+        sacc[qb][I % 2] = mfma32(kf, qf[qb][I / 2], sacc[qb][I % 2]);
+      issue_read(std::integral_constant<int, I + RW>());
+      qk_hook(i_tag);
+    });
     // ---- online softmax, one query column per lane ----
     bf16x8 pf[QB][4];
 #pragma unroll
@@ -298,29 +320,21 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
     // ---- O^T += V^T P^T over 16-key chunks ----
     // Chunk kc: k-group h holds P for keys 16 kc + {4h..4h+3, 8+4h..8+4h+3};
     // the two transposing reads fetch V for exactly those keys, column d.
-    auto pv_chunk = [&](auto kc_tag) {
-      constexpr int KC = decltype(kc_tag)::value;
-      constexpr int OFF = BUF * TILE_BYTES + KC * 16 * ROW_BYTES;
-      u32x2 vr[S::DBLK][2];
+    // Product m = (kc, db) takes V reads 2m and 2m + 1 of the stream.
+    static_for<0, NV / 2>([&](auto m_tag) {
+      constexpr int M = decltype(m_tag)::value;
+      constexpr int AHEAD = (RW < NV - 2 * M ? RW : NV - 2 * M) - 2;  // reads issued after 2M+1
+      lds_wait_lgkm<AHEAD>();
+      lds_ready(vr[2 * M]);
+      lds_ready(vr[2 * M + 1]);
+      const u32x4 w = {vr[2 * M][0], vr[2 * M][1], vr[2 * M + 1][0], vr[2 * M + 1][1]};
+      const bf16x8 vf = as_bf16x8(w);
 #pragma unroll
-      for (int db = 0; db < S::DBLK; ++db)
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) vr[db][hh] = lds_read_tr16_async_off<OFF>(v_addr[db][hh]);
-#pragma unroll
-      for (int db = 0; db < S::DBLK; db += 2)
-        lds_wait4(vr[db][0], vr[db][1], vr[db + 1][0], vr[db + 1][1]);
-#pragma unroll
-      for (int db = 0; db < S::DBLK; ++db) {
-        const u32x4 w = {vr[db][0][0], vr[db][0][1], vr[db][1][0], vr[db][1][1]};
-        const bf16x8 vf = as_bf16x8(w);
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) o_acc[qb][db] = mfma32(vf, pf[qb][KC], o_acc[qb][db]);
-      }
-    };
-    pv_chunk(std::integral_constant<int, 0>());
-    pv_chunk(std::integral_constant<int, 1>());
-    pv_chunk(std::integral_constant<int, 2>());
-    pv_chunk(std::integral_constant<int, 3>());
+      for (int qb = 0; qb < QB; ++qb)
+        o_acc[qb][M % S::DBLK] = mfma32(vf, pf[qb][M / S::DBLK], o_acc[qb][M % S::DBLK]);
+      issue_read(std::integral_constant<int, NK + RW + 2 * M>());
+      issue_read(std::integral_constant<int, NK + RW + 2 * M + 1>());
+    });
   };
 
   // Tiles [0, n_free) need no mask for any row of this wave; tiles up to
@@ -333,23 +347,35 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   n_free = max(0, min(n_free, n_live));
 
   // Tile kt lives in buffer kt % 2; the loop is unrolled by two so the
-  // buffer of every LDS access is a compile-time constant.
-  auto step = [&](int kt, auto buf_tag) {
-    if (kt + 1 < n_kt)
-      wait_vmcnt<S::LOADS_PER_TILE>();
-    else
-      wait_vmcnt<0>();
+  // buffer of every LDS access is a compile-time constant.  One barrier per
+  // tile: once every wave has waited for its own loads of tile kt, the
+  // barrier makes the whole tile visible and also proves that every wave
+  // has finished tile kt - 1, so the loads of tile kt + 1 can go into that
+  // buffer during tile kt, about a tile of compute ahead of their use.
+  // The loads of tile kt + 1 are spread over the score products of tile
+  // kt (one 1 KB block of K and of V per NK / BLOCKS_PER_WAVE products), so
+  // no wave stalls on a burst of memory instructions.
+  constexpr int QK_PER_BLOCK = NK / S::BLOCKS_PER_WAVE;
+  static_assert(NK % S::BLOCKS_PER_WAVE == 0, "load spreading");
+  auto step = [&](int kt, auto buf_tag, auto next_tag) {
+    wait_vmcnt<0>();
     __syncthreads();
+    const bool more = kt + 1 < n_kt;
+    auto hook = [&](auto i_tag) {
+      constexpr int I = decltype(i_tag)::value;
+      if constexpr (I % QK_PER_BLOCK == QK_PER_BLOCK - 1)
+        if (more) issue_block(kt + 1, next_tag, std::integral_constant<int, I / QK_PER_BLOCK>());
+    };
     if (kt < n_free)
-      tile(std::false_type(), buf_tag, kt);
+      tile(std::false_type(), buf_tag, kt, hook);
     else if (kt < n_live)
-      tile(std::true_type(), buf_tag, kt);
-    __syncthreads();
-    if (kt + 2 < n_kt) issue_tile(kt + 2, buf_tag);
+      tile(std::true_type(), buf_tag, kt, hook);
+    else if (more)
+      issue_tile(kt + 1, next_tag);
   };
   for (int kt = 0; kt < n_kt; kt += 2) {
-    step(kt, B0());
-    if (kt + 1 < n_kt) step(kt + 1, B1());
+    step(kt, B0(), B1());
+    if (kt + 1 < n_kt) step(kt + 1, B1(), B0());
   }
 
   // ---- epilogue: O = O_acc / l, LSE = ln 2 * (m + log2 l) ----

@@ -19,6 +19,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace mk {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -153,6 +155,22 @@ __device__ __forceinline__ void lds_wait_b128x2(u32x4& a, u32x4& b) {
   asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b) :: "memory");
 }
 
+// s_waitcnt lgkmcnt(N) for LDS reads issued as inline assembly: wait until
+// at most N of this wave's LDS operations are outstanding (LDS operations
+// complete in order).  Pass each destination register that must be ready
+// through lds_ready() after it: the empty statement redefines the register
+// after the wait, so no use of it can be scheduled before the wait
+// (volatile statements keep their order).
+template <int N>
+__device__ __forceinline__ void lds_wait_lgkm() {
+  static_assert(N >= 0 && N < 16, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+}
+template <class T>
+__device__ __forceinline__ void lds_ready(T& x) {
+  asm volatile("" : "+v"(x));
+}
+
 // s_waitcnt lgkmcnt(0) that the four given registers depend on, so no use
 // of them can be scheduled before the wait.
 __device__ __forceinline__ void lds_wait4(u32x2& a, u32x2& b, u32x2& c, u32x2& d) {
@@ -191,6 +209,15 @@ template <int D>
 __device__ __forceinline__ int fwd_swz(int r) {
   if (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
   return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+}
+
+// f(std::integral_constant<int, I>()) for I = A .. B-1, in order.
+template <int A, int B, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (A < B) {
+    f(std::integral_constant<int, A>());
+    static_for<A + 1, B>(f);
+  }
 }
 
 __device__ __forceinline__ int clamp_len(int len, int hi) {
