@@ -101,7 +101,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   constexpr int ROW_BYTES = D * 2;
   constexpr int NK = 2 * S::KSTEPS;     // K fragment reads per tile
   constexpr int NV = 8 * S::DBLK;       // transposing V reads per tile
-  constexpr int RW = 8;                 // LDS reads in flight
+  constexpr int RW = POS_SCALE ? 8 : 4;  // LDS reads in flight (fewer registers otherwise)
   static_assert(RW >= 2 && RW % 2 == 0 && RW <= NK && RW <= NV, "read window");
   __shared__ __attribute__((aligned(1024))) uint16_t k_lds[2][TILE];
   __shared__ __attribute__((aligned(1024))) uint16_t v_lds[2][TILE];
@@ -161,19 +161,15 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   const int dma_ch = ((lane % S::CHUNKS) ^ fwd_swz<D>(dma_row)) * 16;  // byte offset
   const uint32_t k_lds_w = __builtin_amdgcn_readfirstlane(lds_addr(&k_lds[0][0]) + wave * 1024);
   const uint32_t v_lds_w = __builtin_amdgcn_readfirstlane(lds_addr(&v_lds[0][0]) + wave * 1024);
-  auto issue_block = [&](int kt, auto buf_tag, auto p_tag) {
+  // Block p of tile kt of one tensor (K or V) into LDS buffer BUF.
+  auto issue_rows = [&](const char* g, uint32_t lds_w, int kt, auto buf_tag, auto p_tag) {
     constexpr int BUF = decltype(buf_tag)::value;
     constexpr int P = decltype(p_tag)::value;
     const int lim = L - 1 - kt * BN;  // last valid row of the tile
     const uint32_t goff = (uint32_t)(min(dma_row, lim - P * ROW_STEP) * ROW_BYTES + dma_ch) +
                           P * ROW_STEP * ROW_BYTES;
-    const size_t toff = (size_t)kt * BN * ROW_BYTES;
     constexpr uint32_t lds_off = BUF * TILE_BYTES + P * S::WAVES * 1024;
-    load_lds16_at(kg + toff + goff, k_lds_w + lds_off);
-    load_lds16_at(vg + toff + goff, v_lds_w + lds_off);
-  };
-  auto issue_tile = [&](int kt, auto buf_tag) {
-    static_for<0, S::BLOCKS_PER_WAVE>([&](auto p_tag) { issue_block(kt, buf_tag, p_tag); });
+    load_lds16_at(g + (size_t)kt * BN * ROW_BYTES + goff, lds_w + lds_off);
   };
 
   float m_run[QB], l_run[QB];
@@ -190,7 +186,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
 
   using B0 = std::integral_constant<int, 0>;
   using B1 = std::integral_constant<int, 1>;
-  if (n_kt > 0) issue_tile(0, B0());
+  if (n_kt > 0)
+    static_for<0, S::BLOCKS_PER_WAVE>([&](auto p_tag) { issue_rows(kg, k_lds_w, 0, B0(), p_tag); });
 
   // Lane parts of the LDS read addresses (bytes within a tile).  K row
   // 32 kb + n: the swizzle of n + 32 kb equals that of n.  Transposing V
@@ -216,127 +213,6 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
       }
   }
 
-  // One 64-key tile for this wave from LDS buffer BUF.  MASK: apply the
-  // length / causal mask.
-  auto tile = [&](auto mask_tag, auto buf_tag, int kt, auto&& qk_hook) {
-    constexpr bool MASK = decltype(mask_tag)::value;
-    constexpr int BUF = decltype(buf_tag)::value;
-    const int key0 = kt * BN;
-    // ---- S^T = K Q^T for the 64 keys of the tile ----
-    // The tile's LDS reads form one stream: the NK K fragments (step s,
-    // key block kb, alternating kb so that two accumulator chains are in
-    // flight), then the NV transposing V reads in the order the P V
-    // products consume them.  RW reads are kept in flight: consuming one
-    // issues the next, so V's first reads are under way during the softmax.
-    f32x16 sacc[QB][2];
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[qb][kb][r] = 0.f;
-    u32x4 kr[NK];
-    u32x2 vr[NV];
-    auto issue_read = [&](auto j_tag) {
-      constexpr int J = decltype(j_tag)::value;
-      if constexpr (J < NK) {
-        constexpr int OFF = BUF * TILE_BYTES + (J % 2) * 32 * ROW_BYTES;
-        kr[J] = lds_read_b128_async_off<OFF>(k_addr[J / 2]);
-      } else if constexpr (J < NK + NV) {
-        constexpr int V = J - NK;        // (kc, db, hh) = V / (2 DBLK), V / 2 % DBLK, V % 2
-        constexpr int OFF = BUF * TILE_BYTES + (V / (2 * S::DBLK)) * 16 * ROW_BYTES;
-        vr[V] = lds_read_tr16_async_off<OFF>(v_addr[(V / 2) % S::DBLK][V % 2]);
-      }
-    };
-    static_for<0, RW>(issue_read);
-    static_for<0, NK>([&](auto i_tag) {
-      constexpr int I = decltype(i_tag)::value;
-      lds_wait_lgkm<RW - 1>();
-      lds_ready(kr[I]);
-      const bf16x8 kf = as_bf16x8(kr[I]);
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
-        sacc[qb][I % 2] = mfma32(kf, qf[qb][I / 2], sacc[qb][I % 2]);
-      issue_read(std::integral_constant<int, I + RW>());
-      qk_hook(i_tag);
-    });
-    // ---- online softmax, one query column per lane ----
-    bf16x8 pf[QB][4];
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-      if (!POS_SCALE) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) sacc[qb][kb][r] *= c;
-      }
-      if (MASK) {
-        const int qrow = qw0 + qb * 32 + n;
-        const int lim = min(L - 1, CAUSAL ? qrow + off : L - 1);  // last admissible key
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = key0 + kb * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-            if (key > lim) sacc[qb][kb][r] = kNegInf;
-          }
-      }
-      float mx = kNegInf;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[qb][kb][r]);
-      mx = max_xor32(mx);
-      if (POS_SCALE) mx *= c;
-      if (__ballot(mx > m_run[qb] + kRescaleSlack)) {
-        const float m_new = fmaxf(m_run[qb], mx);
-        const float alpha = (m_new == kNegInf) ? 1.f : fast_exp2(m_run[qb] - m_new);
-        m_run[qb] = m_new;
-        l_run[qb] *= alpha;
-#pragma unroll
-        for (int db = 0; db < S::DBLK; ++db)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o_acc[qb][db][r] *= alpha;
-      }
-      const float m_use = (m_run[qb] == kNegInf) ? 0.f : m_run[qb];
-      const float cc = POS_SCALE ? c : 1.f;
-      float rs = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = fast_exp2(fmaf(sacc[qb][kb][r], cc, -m_use));
-          sacc[qb][kb][r] = p;
-          rs += p;
-        }
-      l_run[qb] += rs;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const f32x16 p = sacc[qb][kb];
-        pf[qb][2 * kb] = to_bf16x8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
-        pf[qb][2 * kb + 1] = to_bf16x8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
-      }
-    }
-    // ---- O^T += V^T P^T over 16-key chunks ----
-    // Chunk kc: k-group h holds P for keys 16 kc + {4h..4h+3, 8+4h..8+4h+3};
-    // the two transposing reads fetch V for exactly those keys, column d.
-    // Product m = (kc, db) takes V reads 2m and 2m + 1 of the stream.
-    static_for<0, NV / 2>([&](auto m_tag) {
-      constexpr int M = decltype(m_tag)::value;
-      constexpr int AHEAD = (RW < NV - 2 * M ? RW : NV - 2 * M) - 2;  // reads issued after 2M+1
-      lds_wait_lgkm<AHEAD>();
-      lds_ready(vr[2 * M]);
-      lds_ready(vr[2 * M + 1]);
-      const u32x4 w = {vr[2 * M][0], vr[2 * M][1], vr[2 * M + 1][0], vr[2 * M + 1][1]};
-      const bf16x8 vf = as_bf16x8(w);
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
-        o_acc[qb][M % S::DBLK] = mfma32(vf, pf[qb][M / S::DBLK], o_acc[qb][M % S::DBLK]);
-      issue_read(std::integral_constant<int, NK + RW + 2 * M>());
-      issue_read(std::integral_constant<int, NK + RW + 2 * M + 1>());
-    });
-  };
-
   // Tiles [0, n_free) need no mask for any row of this wave; tiles up to
   // n_live hold at least one admissible key for some row of the wave.
   const int w_first = qw0;                      // first query row of the wave
@@ -346,36 +222,253 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   n_live = (max(n_live, 0) + BN - 1) / BN;
   n_free = max(0, min(n_free, n_live));
 
-  // Tile kt lives in buffer kt % 2; the loop is unrolled by two so the
-  // buffer of every LDS access is a compile-time constant.  One barrier per
-  // tile: once every wave has waited for its own loads of tile kt, the
-  // barrier makes the whole tile visible and also proves that every wave
-  // has finished tile kt - 1, so the loads of tile kt + 1 can go into that
-  // buffer during tile kt, about a tile of compute ahead of their use.
-  // The loads of tile kt + 1 are spread over the score products of tile
-  // kt (one 1 KB block of K and of V per NK / BLOCKS_PER_WAVE products), so
-  // no wave stalls on a burst of memory instructions.
-  constexpr int QK_PER_BLOCK = NK / S::BLOCKS_PER_WAVE;
-  static_assert(NK % S::BLOCKS_PER_WAVE == 0, "load spreading");
-  auto step = [&](int kt, auto buf_tag, auto next_tag) {
+  // Scores of even and odd tiles: step t forms those of tile t while it
+  // turns those of tile t - 1 into weights.
+  f32x16 s_even[QB][2], s_odd[QB][2];
+  float m_use[QB];  // exponent offset for the weights of the last scored tile
+
+  // Step t (t = 0 .. n_kt) of the pipeline, for one wave:
+  //   QK (t < n_live):       S(t) = K(t) Q^T on the matrix cores, with the
+  //                          exponentials of tile t - 1 issued in between
+  //                          (PV), then the softmax head of tile t (MASK:
+  //                          tile t needs the length / causal mask): row
+  //                          max and lazy rescale;
+  //   PV (1 <= t <= n_live): O += P V(t-1), with the head of tile t issued
+  //                          in between (QK).
+  // K(t) sits in K buffer t % 2 and V(t - 1) in V buffer (t - 1) % 2; the
+  // step loads K(t + 1) and V(t) into the other two buffers, spread over
+  // its score products.  STEADY: both loads are due (t + 1 < n_kt), so they
+  // are issued without a branch that would split the products' schedule
+  // (used for unmasked tiles, the bulk of the work).
+  auto step = [&](int t, auto par_tag, auto qk_tag, auto pv_tag, auto mask_tag, auto steady_tag) {
+    constexpr int PAR = decltype(par_tag)::value;
+    constexpr bool QK = decltype(qk_tag)::value;
+    constexpr bool PV = decltype(pv_tag)::value;
+    constexpr bool MASK = decltype(mask_tag)::value;
+    constexpr bool STEADY = decltype(steady_tag)::value;
+    constexpr int KBUF = PAR, VBUF = 1 - PAR;
+    auto& s_new = pick<PAR>(s_even, s_odd);
+    auto& s_old = pick<1 - PAR>(s_even, s_odd);
+    const bool load_k = t + 1 < n_kt;
+    const bool load_v = t < n_kt;
+    auto load_block = [&](auto p_tag) {
+      if (STEADY || load_k)
+        issue_rows(kg, k_lds_w, t + 1, std::integral_constant<int, 1 - PAR>(), p_tag);
+      if (STEADY || load_v) issue_rows(vg, v_lds_w, t, std::integral_constant<int, PAR>(), p_tag);
+    };
+
+    // ---- LDS read stream: the NK K fragments of tile t (key block kb,
+    // then step s: the scores of key block 1 need registers only once the
+    // weights of key block 0 of tile t - 1 are formed), then the NV
+    // transposing V reads of tile t - 1 in the order the products consume
+    // them.  RS reads are kept in flight: consuming one issues the next.  The
+    // first ones go out before the softmax head, ahead of their products. ----
+    constexpr int NKS = QK ? NK : 0;
+    constexpr int NVS = PV ? NV : 0;
+    constexpr int TOT = NKS + NVS;
+    constexpr int RS = RW < TOT ? RW : TOT;
+    u32x4 kr[NK];
+    u32x2 vr[NV];
+    auto issue_read = [&](auto j_tag) {
+      constexpr int J = decltype(j_tag)::value;
+      if constexpr (J < NKS) {
+        constexpr int OFF = KBUF * TILE_BYTES + (J / S::KSTEPS) * 32 * ROW_BYTES;
+        kr[J] = lds_read_b128_async_off<OFF>(k_addr[J % S::KSTEPS]);
+      } else if constexpr (J < TOT) {
+        constexpr int V = J - NKS;  // (kc, db, hh) = V / (2 DBLK), V / 2 % DBLK, V % 2
+        constexpr int OFF = VBUF * TILE_BYTES + (V / (2 * S::DBLK)) * 16 * ROW_BYTES;
+        vr[V] = lds_read_tr16_async_off<OFF>(v_addr[(V / 2) % S::DBLK][V % 2]);
+      }
+    };
+    static_for<0, RS>(issue_read);
+
+    // Weights of 16-key chunk kc of tile t - 1 (accumulator rows
+    // 8 (kc % 2) .. +7 of key block kc / 2) as the bf16 P^T fragment, and
+    // their sum.
+    const float cc = POS_SCALE ? c : 1.f;
+    bf16x8 pf[QB][4];
+    // The exponentials of chunk kc come in PER_EXP parts (one per score
+    // product they are interleaved with); exp_finish then forms the chunk's
+    // fragment and sum.
+    constexpr int PER_EXP = NK / 4;   // score products per weight chunk
+    constexpr int EPP = 8 / PER_EXP;  // exponentials per part
+    static_assert(NK % 4 == 0 && 8 % PER_EXP == 0, "exponential spacing");
+    auto exp_part = [&](auto kc_tag, auto j_tag) {
+      constexpr int KC = decltype(kc_tag)::value;
+      constexpr int J = decltype(j_tag)::value;
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int e = 0; e < EPP; ++e) {
+          constexpr int R = 8 * (KC % 2) + J * EPP;
+          s_old[qb][KC / 2][R + e] = fast_exp2(fmaf(s_old[qb][KC / 2][R + e], cc, -m_use[qb]));
+        }
+    };
+    auto exp_finish = [&](auto kc_tag) {
+      constexpr int KC = decltype(kc_tag)::value;
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        const f32x16& x = s_old[qb][KC / 2];
+        constexpr int R = 8 * (KC % 2);
+        l_run[qb] += ((x[R] + x[R + 1]) + (x[R + 2] + x[R + 3])) +
+                     ((x[R + 4] + x[R + 5]) + (x[R + 6] + x[R + 7]));
+        pf[qb][KC] = to_bf16x8(x[R], x[R + 1], x[R + 2], x[R + 3], x[R + 4], x[R + 5], x[R + 6],
+                               x[R + 7]);
+      }
+    };
+    auto exp_chunk = [&](auto kc_tag) {
+      static_for<0, PER_EXP>([&](auto j_tag) { exp_part(kc_tag, j_tag); });
+      exp_finish(kc_tag);
+    };
+
+
+    if constexpr (QK) {
+      // ---- S^T(t) = K(t) Q^T, exponentials of tile t - 1 in between ----
+      constexpr int PER_LOAD = NK / S::BLOCKS_PER_WAVE;  // products per load block
+      static_assert(NK % S::BLOCKS_PER_WAVE == 0, "load spacing");
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) s_new[qb][kb][r] = 0.f;
+      static_for<0, NK>([&](auto i_tag) {
+        constexpr int I = decltype(i_tag)::value;
+        constexpr int KB = I / S::KSTEPS, ST = I % S::KSTEPS;
+        constexpr int AHEAD = (I + RS < TOT ? I + RS : TOT) - I - 1;  // reads issued after I
+        lds_wait_lgkm<AHEAD>();
+        lds_ready(kr[I]);
+        const bf16x8 kf = as_bf16x8(kr[I]);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) s_new[qb][KB] = mfma32(kf, qf[qb][ST], s_new[qb][KB]);
+        issue_read(std::integral_constant<int, I + RS>());
+        if constexpr (I % PER_LOAD == PER_LOAD - 1)
+          load_block(std::integral_constant<int, I / PER_LOAD>());
+        if constexpr (PV) {
+          exp_part(std::integral_constant<int, I / PER_EXP>(),
+                   std::integral_constant<int, I % PER_EXP>());
+          if constexpr (I % PER_EXP == PER_EXP - 1)
+            exp_finish(std::integral_constant<int, I / PER_EXP>());
+        }
+        // the source order is the schedule: it keeps each product's
+        // exponentials beside it and bounds the live registers
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    } else {
+      static_for<0, S::BLOCKS_PER_WAVE>(load_block);
+      if constexpr (PV) static_for<0, 4>(exp_chunk);
+    }
+
+    // ---- softmax head of tile t: scale (scale <= 0), mask, row max, in
+    // eight parts interleaved with the P V products of tile t - 1 (key block
+    // 0 first: its scores were formed first) ----
+    float mx0[QB], mx1[QB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) mx0[qb] = mx1[qb] = kNegInf;
+    auto head_part = [&](auto j_tag) {
+      constexpr int J = decltype(j_tag)::value;
+      constexpr int KB = J / 4, R0 = 4 * (J % 4);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+        for (int r = R0; r < R0 + 4; ++r) {
+          if (!POS_SCALE) s_new[qb][KB][r] *= c;
+          if (MASK) {
+            const int qrow = qw0 + qb * 32 + n;
+            const int lim = min(L - 1, CAUSAL ? qrow + off : L - 1);  // last admissible key
+            const int key = t * BN + KB * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+            if (key > lim) s_new[qb][KB][r] = kNegInf;
+          }
+        }
+        float& mx = KB == 0 ? mx0[qb] : mx1[qb];
+        mx = fmaxf(fmaxf(mx, s_new[qb][KB][R0]), s_new[qb][KB][R0 + 1]);
+        mx = fmaxf(fmaxf(mx, s_new[qb][KB][R0 + 2]), s_new[qb][KB][R0 + 3]);
+      }
+    };
+
+    if constexpr (PV) {
+      // ---- O^T += V^T(t-1) P^T(t-1) over 16-key chunks ----
+      // Chunk kc: k-group h holds P for keys 16 kc + {4h..4h+3, 8+4h..8+4h+3};
+      // the two transposing reads fetch V for exactly those keys, column d.
+      // Product m = (kc, db) takes V reads 2m and 2m + 1.
+      constexpr int PER_HEAD = (NV / 2) / 8;  // products per head part
+      static_assert((NV / 2) % 8 == 0, "head spacing");
+      static_for<0, NV / 2>([&](auto m_tag) {
+        constexpr int M = decltype(m_tag)::value;
+        constexpr int AHEAD = (RS < NV - 2 * M ? RS : NV - 2 * M) - 2;  // reads after 2M+1
+        lds_wait_lgkm<AHEAD>();
+        lds_ready(vr[2 * M]);
+        lds_ready(vr[2 * M + 1]);
+        const u32x4 w = {vr[2 * M][0], vr[2 * M][1], vr[2 * M + 1][0], vr[2 * M + 1][1]};
+        const bf16x8 vf = as_bf16x8(w);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+          o_acc[qb][M % S::DBLK] = mfma32(vf, pf[qb][M / S::DBLK], o_acc[qb][M % S::DBLK]);
+        issue_read(std::integral_constant<int, NKS + RS + 2 * M>());
+        issue_read(std::integral_constant<int, NKS + RS + 2 * M + 1>());
+        if constexpr (QK && M % PER_HEAD == PER_HEAD - 1)
+          head_part(std::integral_constant<int, M / PER_HEAD>());
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    } else if constexpr (QK) {
+      static_for<0, 8>(head_part);
+    }
+
+    // ---- softmax head of tile t, end: lazy rescale of the running state ----
+    if constexpr (QK) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        float mx = max_xor32(fmaxf(mx0[qb], mx1[qb]));
+        if (POS_SCALE) mx *= c;
+        if (__ballot(mx > m_run[qb] + kRescaleSlack)) {
+          const float m_new = fmaxf(m_run[qb], mx);
+          const float alpha = (m_new == kNegInf) ? 1.f : fast_exp2(m_run[qb] - m_new);
+          m_run[qb] = m_new;
+          l_run[qb] *= alpha;
+#pragma unroll
+          for (int db = 0; db < S::DBLK; ++db)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) o_acc[qb][db][r] *= alpha;
+        }
+        m_use[qb] = (m_run[qb] == kNegInf) ? 0.f : m_run[qb];
+      }
+    }
+  };
+
+  // One barrier per step: once every wave has waited for its own loads,
+  // the barrier makes K(t) and V(t - 1) visible and proves that every wave
+  // has finished step t - 1, whose buffers the step's loads overwrite.
+  using T1 = std::true_type;
+  using F0 = std::false_type;
+  auto run_step = [&](int t, auto par_tag) {
     wait_vmcnt<0>();
     __syncthreads();
-    const bool more = kt + 1 < n_kt;
-    auto hook = [&](auto i_tag) {
-      constexpr int I = decltype(i_tag)::value;
-      if constexpr (I % QK_PER_BLOCK == QK_PER_BLOCK - 1)
-        if (more) issue_block(kt + 1, next_tag, std::integral_constant<int, I / QK_PER_BLOCK>());
-    };
-    if (kt < n_free)
-      tile(std::false_type(), buf_tag, kt, hook);
-    else if (kt < n_live)
-      tile(std::true_type(), buf_tag, kt, hook);
-    else if (more)
-      issue_tile(kt + 1, next_tag);
+    const bool qk = t < n_live;
+    const bool pv = t >= 1 && t <= n_live;
+    const bool mask = t >= n_free;
+    if (qk && pv && t + 1 < n_kt && !mask) {
+      step(t, par_tag, T1(), T1(), F0(), T1());
+    } else if (qk && pv) {
+      if (mask)
+        step(t, par_tag, T1(), T1(), T1(), F0());
+      else
+        step(t, par_tag, T1(), T1(), F0(), F0());
+    } else if (qk) {
+      if (mask)
+        step(t, par_tag, T1(), F0(), T1(), F0());
+      else
+        step(t, par_tag, T1(), F0(), F0(), F0());
+    } else if (pv) {
+      step(t, par_tag, F0(), T1(), F0(), F0());
+    } else {
+      step(t, par_tag, F0(), F0(), F0(), F0());
+    }
   };
-  for (int kt = 0; kt < n_kt; kt += 2) {
-    step(kt, B0(), B1());
-    if (kt + 1 < n_kt) step(kt + 1, B1(), B0());
+  if (n_kt > 0) {
+    for (int t = 0; t <= n_kt; t += 2) {
+      run_step(t, B0());
+      if (t + 1 <= n_kt) run_step(t + 1, B1());
+    }
   }
 
   // ---- epilogue: O = O_acc / l, LSE = ln 2 * (m + log2 l) ----

@@ -220,6 +220,15 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
+// a for P == 0, b otherwise (compile-time choice between two objects).
+template <int P, class T>
+__device__ __forceinline__ T& pick(T& a, T& b) {
+  if constexpr (P == 0)
+    return a;
+  else
+    return b;
+}
+
 __device__ __forceinline__ int clamp_len(int len, int hi) {
   return len < 0 ? 0 : (len > hi ? hi : len);
 }
