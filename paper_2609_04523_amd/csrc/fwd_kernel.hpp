@@ -124,6 +124,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   if (CAUSAL) n_keys = min(L, q_end + off);
   if (n_keys < 0) n_keys = 0;
   const int n_kt = (n_keys + BN - 1) / BN;
+  const int n_full = L / BN;  // tiles that lie wholly inside the sequence
   const float c = a.scale_log2;
 
   const size_t q_row0 = ((size_t)b * a.Hq + hq) * (size_t)a.Sq;
@@ -161,13 +162,25 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   const int dma_ch = ((lane % S::CHUNKS) ^ fwd_swz<D>(dma_row)) * 16;  // byte offset
   const uint32_t k_lds_w = __builtin_amdgcn_readfirstlane(lds_addr(&k_lds[0][0]) + wave * 1024);
   const uint32_t v_lds_w = __builtin_amdgcn_readfirstlane(lds_addr(&v_lds[0][0]) + wave * 1024);
-  // Block p of tile kt of one tensor (K or V) into LDS buffer BUF.
-  auto issue_rows = [&](const char* g, uint32_t lds_w, int kt, auto buf_tag, auto p_tag) {
+  // Block p of tile kt of one tensor (K or V) into LDS buffer BUF.  FULL:
+  // the tile lies inside the sequence, so no row needs clamping and the
+  // lane offsets are the precomputed full_off[p].
+  uint32_t full_off[S::BLOCKS_PER_WAVE];
+#pragma unroll
+  for (int p = 0; p < S::BLOCKS_PER_WAVE; ++p)
+    full_off[p] = (uint32_t)((dma_row + p * ROW_STEP) * ROW_BYTES + dma_ch);
+  auto issue_rows = [&](const char* g, uint32_t lds_w, int kt, auto buf_tag, auto p_tag,
+                        auto full_tag) {
     constexpr int BUF = decltype(buf_tag)::value;
     constexpr int P = decltype(p_tag)::value;
-    const int lim = L - 1 - kt * BN;  // last valid row of the tile
-    const uint32_t goff = (uint32_t)(min(dma_row, lim - P * ROW_STEP) * ROW_BYTES + dma_ch) +
-                          P * ROW_STEP * ROW_BYTES;
+    uint32_t goff;
+    if constexpr (decltype(full_tag)::value) {
+      goff = full_off[P];
+    } else {
+      const int lim = L - 1 - kt * BN;  // last valid row of the tile
+      goff = (uint32_t)(min(dma_row, lim - P * ROW_STEP) * ROW_BYTES + dma_ch) +
+             P * ROW_STEP * ROW_BYTES;
+    }
     constexpr uint32_t lds_off = BUF * TILE_BYTES + P * S::WAVES * 1024;
     load_lds16_at(g + (size_t)kt * BN * ROW_BYTES + goff, lds_w + lds_off);
   };
@@ -187,7 +200,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   using B0 = std::integral_constant<int, 0>;
   using B1 = std::integral_constant<int, 1>;
   if (n_kt > 0)
-    static_for<0, S::BLOCKS_PER_WAVE>([&](auto p_tag) { issue_rows(kg, k_lds_w, 0, B0(), p_tag); });
+    static_for<0, S::BLOCKS_PER_WAVE>(
+        [&](auto p_tag) { issue_rows(kg, k_lds_w, 0, B0(), p_tag, std::false_type()); });
 
   // Lane parts of the LDS read addresses (bytes within a tile).  K row
   // 32 kb + n: the swizzle of n + 32 kb equals that of n.  Transposing V
@@ -237,9 +251,10 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   //                          in between (QK).
   // K(t) sits in K buffer t % 2 and V(t - 1) in V buffer (t - 1) % 2; the
   // step loads K(t + 1) and V(t) into the other two buffers, spread over
-  // its score products.  STEADY: both loads are due (t + 1 < n_kt), so they
-  // are issued without a branch that would split the products' schedule
-  // (used for unmasked tiles, the bulk of the work).
+  // its score products.  STEADY: both loads are due and both tiles are full
+  // (t + 1 < n_full), so they are issued without a branch that would split
+  // the products' schedule and without row clamping (used for unmasked
+  // tiles, the bulk of the work).
   auto step = [&](int t, auto par_tag, auto qk_tag, auto pv_tag, auto mask_tag, auto steady_tag) {
     constexpr int PAR = decltype(par_tag)::value;
     constexpr bool QK = decltype(qk_tag)::value;
@@ -252,9 +267,10 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
     const bool load_k = t + 1 < n_kt;
     const bool load_v = t < n_kt;
     auto load_block = [&](auto p_tag) {
-      if (STEADY || load_k)
-        issue_rows(kg, k_lds_w, t + 1, std::integral_constant<int, 1 - PAR>(), p_tag);
-      if (STEADY || load_v) issue_rows(vg, v_lds_w, t, std::integral_constant<int, PAR>(), p_tag);
+      using KB_ = std::integral_constant<int, 1 - PAR>;
+      using VB_ = std::integral_constant<int, PAR>;
+      if (STEADY || load_k) issue_rows(kg, k_lds_w, t + 1, KB_(), p_tag, steady_tag);
+      if (STEADY || load_v) issue_rows(vg, v_lds_w, t, VB_(), p_tag, steady_tag);
     };
 
     // ---- LDS read stream: the NK K fragments of tile t (key block kb,
@@ -446,7 +462,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
     const bool qk = t < n_live;
     const bool pv = t >= 1 && t <= n_live;
     const bool mask = t >= n_free;
-    if (qk && pv && t + 1 < n_kt && !mask) {
+    if (qk && pv && t + 1 < n_full && !mask) {
       step(t, par_tag, T1(), T1(), F0(), T1());
     } else if (qk && pv) {
       if (mask)
