@@ -63,6 +63,9 @@ def _declare(lib):
     lib.oracle_decode_split.argtypes = [_u16p, _u16p, _u16p, i, i, i, i, i, d,
                                         _i32p, i, _f64p, _f64p, _f64p, _f64p]
     lib.oracle_decode_split.restype = i
+    lib.oracle_decode_paged.argtypes = [_u16p, _u16p, _u16p, _i32p, i, i, i, i, i, i, i, d,
+                                        _i32p, _f64p, _f64p]
+    lib.oracle_decode_paged.restype = i
     lib.oracle_version.restype = i
     return lib
 
@@ -158,6 +161,28 @@ def decode(q, k_cache, v_cache, kv_seqlens, *, scale: float,
                            _ptr(o, _f64p), _ptr(lse, _f64p), threads or default_threads())
     if rc != 0:
         raise ValueError(f"oracle_decode failed ({rc})")
+    return o, lse
+
+
+def decode_paged(q, k_pages, v_pages, block_table, kv_seqlens, *, scale: float, lib=None):
+    """Paged decode step.  q [B,Hq,D], pages [n_pages,Hkv,page_size,D], block_table
+    [B,max_pages] int32 -> (o [B,Hq,D], lse [B,Hq])."""
+    lib = lib or load()
+    q, kp, vp = _u16(q), _u16(k_pages), _u16(v_pages)
+    B, Hq, D = q.shape
+    n_pages, Hkv, page_size, _ = kp.shape
+    bt = np.ascontiguousarray(block_table, dtype=np.int32)
+    if bt.ndim != 2 or bt.shape[0] != B:
+        raise ValueError("block_table must be [B, max_pages]")
+    sl = _seqlens(kv_seqlens, B)
+    o = np.empty((B, Hq, D), np.float64)
+    lse = np.empty((B, Hq), np.float64)
+    rc = lib.oracle_decode_paged(_ptr(q, _u16p), _ptr(kp, _u16p), _ptr(vp, _u16p),
+                                 _ptr(bt, _i32p), B, Hq, Hkv, page_size, bt.shape[1], n_pages,
+                                 D, float(scale), _ptr(sl, _i32p), _ptr(o, _f64p),
+                                 _ptr(lse, _f64p))
+    if rc != 0:
+        raise ValueError(f"oracle_decode_paged failed ({rc})")
     return o, lse
 
 

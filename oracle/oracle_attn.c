@@ -1,6 +1,7 @@
 /*
  * oracle_attn.c -- plain fp64 CPU oracle for causal grouped-query
- * scaled-dot-product attention (forward) and its split-KV decode form.
+ * scaled-dot-product attention (forward), its split-KV decode form, and
+ * decode over a paged cache (the "Paged Attention" workload of Table 2).
  *
  * TEST INFRASTRUCTURE ONLY.  This file is the checker the GPU path is
  * measured against; it is loaded by the test suite, by the smoke check and
@@ -37,7 +38,8 @@
  * force on tiny inputs, closed forms (scale 0, one key, equal V rows,
  * causal row 0), invariants (rows of P sum to 1, GQA equals MHA with
  * repeated K/V heads, decode equals the last prefill row, split-combine
- * equals unsplit) and hand-derived values stored under tests/golden/.
+ * equals unsplit, paged decode equals decode on the cache gathered through
+ * the block table) and hand-derived values stored under tests/golden/.
  *
  * Build: plain C11, no -ffast-math, libm only (gcc -O2 -shared -fPIC).
  */
@@ -61,6 +63,17 @@ static int clamp_len(int len, int hi)
     if (len < 0) return 0;
     if (len > hi) return hi;
     return len;
+}
+
+/* Row of key j of sequence b, kv head g, in a page pool
+   [n_pages, Hkv, page_size, D] (see oracle_decode_paged). */
+static size_t paged_row(const int32_t *block_table, int b, int max_pages,
+                        int n_pages, int page_size, int Hkv, int g, int j)
+{
+    int page = block_table[(size_t)b * max_pages + j / page_size];
+    if (page < 0) page = 0;
+    if (page > n_pages - 1) page = n_pages - 1;
+    return ((size_t)page * Hkv + g) * page_size + (size_t)(j % page_size);
 }
 
 /* ------------------------------------------------------------------ */
@@ -372,4 +385,77 @@ int oracle_decode_split(const uint16_t *q, const uint16_t *k_cache,
     return oracle_lse_combine(o_part, lse_part, B * Hq, nsplit, D, o, lse);
 }
 
-int oracle_version(void) { return 1; }
+/* ------------------------------------------------------------------ */
+/* Paged decode: the cache is a pool of fixed-size pages               */
+/* ------------------------------------------------------------------ */
+
+/*
+ * k_pages / v_pages [n_pages, Hkv, page_size, D]; block_table
+ * [B, max_pages] lists the pages of sequence b in key order, so key j of
+ * sequence b is row j % page_size of page block_table[b][j / page_size].
+ * The length clamps to [0, max_pages * page_size]; a table entry outside
+ * [0, n_pages) is read as the nearest valid page (the same clamp the
+ * lengths get: no lookup may leave the pool).  Then the plain decode
+ * definition, written out here with its own loops:
+ *   s_j = scale * q[b,hq,:] . k(j),  w_j = exp(s_j - max s),
+ *   O = sum_j (w_j / sum w) v(j),    LSE = max s + log(sum w).
+ * o [B,Hq,D], lse [B,Hq].
+ */
+int oracle_decode_paged(const uint16_t *q, const uint16_t *k_pages,
+                        const uint16_t *v_pages, const int32_t *block_table,
+                        int B, int Hq, int Hkv, int page_size, int max_pages,
+                        int n_pages, int D, double scale,
+                        const int32_t *kv_seqlens, double *o, double *lse)
+{
+    if (!q || !k_pages || !v_pages || !block_table || !kv_seqlens || !o || !lse)
+        return -1;
+    if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || page_size < 1 ||
+        max_pages < 1 || n_pages < 1 || D < 1)
+        return -2;
+    const int G = Hq / Hkv;
+    const int max_keys = max_pages * page_size;
+    double *s = malloc((size_t)max_keys * sizeof *s);
+    if (!s) return -3;
+    for (int b = 0; b < B; ++b) {
+        const int L = clamp_len(kv_seqlens[b], max_keys);
+        for (int hq = 0; hq < Hq; ++hq) {
+            const int g = hq / G;
+            const uint16_t *q_row = q + ((size_t)b * Hq + hq) * D;
+            double *o_row = o + ((size_t)b * Hq + hq) * D;
+            if (L == 0) {
+                for (int d = 0; d < D; ++d) o_row[d] = 0.0;
+                lse[(size_t)b * Hq + hq] = -INFINITY;
+                continue;
+            }
+            double m = -INFINITY;
+            for (int j = 0; j < L; ++j) {
+                const size_t krow = paged_row(block_table, b, max_pages, n_pages,
+                                              page_size, Hkv, g, j);
+                double dot = 0.0;
+                for (int d = 0; d < D; ++d)
+                    dot += bf16_bits_to_double(q_row[d]) *
+                           bf16_bits_to_double(k_pages[krow * D + d]);
+                s[j] = scale * dot;
+                if (s[j] > m) m = s[j];
+            }
+            double l = 0.0;
+            for (int j = 0; j < L; ++j) {
+                s[j] = exp(s[j] - m);
+                l += s[j];
+            }
+            for (int d = 0; d < D; ++d) o_row[d] = 0.0;
+            for (int j = 0; j < L; ++j) {
+                const size_t vrow = paged_row(block_table, b, max_pages, n_pages,
+                                              page_size, Hkv, g, j);
+                const double p = s[j] / l;
+                for (int d = 0; d < D; ++d)
+                    o_row[d] += p * bf16_bits_to_double(v_pages[vrow * D + d]);
+            }
+            lse[(size_t)b * Hq + hq] = m + log(l);
+        }
+    }
+    free(s);
+    return 0;
+}
+
+int oracle_version(void) { return 2; }

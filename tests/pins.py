@@ -20,7 +20,11 @@ The facts, none of which re-types the oracle's own formula:
   * a decode step equals the last row of the causal prefill over the same
     keys;
   * the split-KV form with its log-sum-exp merge equals the unsplit result
-    for any split length.
+    for any split length;
+  * a paged cache is a relayout: paged decode equals contiguous decode on
+    the cache gathered through the block table (numpy indexing), whatever
+    the page size, with out-of-range table entries read as the nearest
+    valid page and pages no sequence lists ignored.
 """
 from __future__ import annotations
 
@@ -278,6 +282,67 @@ def pin_row_subset(lib):
             assert np.array_equal(l_sub[b, h], l_all[b, h, rows[b, h]])
 
 
+def _gather_pages(pages: np.ndarray, block_table: np.ndarray) -> np.ndarray:
+    """Page pool [n_pages, Hkv, ps, D] + table [B, max_pages] -> contiguous
+    cache [B, Hkv, max_pages * ps, D], by numpy fancy indexing."""
+    n_pages, Hkv, ps, D = pages.shape
+    B, max_pages = block_table.shape
+    g = pages[np.clip(block_table, 0, n_pages - 1)]          # [B, max_pages, Hkv, ps, D]
+    return np.ascontiguousarray(g.transpose(0, 2, 1, 3, 4).reshape(B, Hkv, max_pages * ps, D))
+
+
+PAGED_CASES = [
+    # B, Hq, Hkv, page_size, max_pages, n_pages, D, lengths
+    (3, 4, 2, 16, 4, 15, 8, [64, 1, 37]),
+    (2, 2, 1, 3, 5, 12, 4, [15, 7]),        # odd page size
+    (2, 4, 4, 1, 9, 20, 4, [9, 0]),         # one key per page, an empty sequence
+    (1, 8, 2, 32, 3, 3, 16, [96]),
+    (2, 2, 2, 16, 2, 6, 8, [40, -3]),       # lengths clamp to [0, 32]
+]
+
+
+def pin_paged_equals_gathered(lib):
+    for n, (B, Hq, Hkv, ps, mp, npg, D, lens) in enumerate(PAGED_CASES):
+        q = _rand((B, Hq, D), 130 + n, -3, 3)
+        kp = _rand((npg, Hkv, ps, D), 140 + n, -3, 3)
+        vp = _rand((npg, Hkv, ps, D), 150 + n)
+        bt = np.random.default_rng(160 + n).integers(0, npg, size=(B, mp), dtype=np.int32)
+        o, lse = orc.decode_paged(q, kp, vp, bt, lens, scale=0.45, lib=lib)
+        og, lg = orc.decode(q, _gather_pages(kp, bt), _gather_pages(vp, bt), lens, scale=0.45,
+                            lib=lib)
+        _close(o, og, 1e-13, f"paged case {n} O")
+        _close(lse, lg, 1e-13, f"paged case {n} LSE")
+
+
+def pin_paged_table_clamp_and_unused_pages(lib):
+    B, Hq, Hkv, ps, mp, npg, D = 2, 4, 2, 4, 5, 9, 8
+    lens = [20, 11]
+    q = _rand((B, Hq, D), 171, -3, 3)
+    kp = _rand((npg, Hkv, ps, D), 172, -3, 3)
+    vp = _rand((npg, Hkv, ps, D), 173)
+    bt = np.array([[3, -7, 8, 14, 0], [5, 2, 2, 100, 1]], dtype=np.int32)
+    o, lse = orc.decode_paged(q, kp, vp, bt, lens, scale=0.3, lib=lib)
+    oc, lc = orc.decode_paged(q, kp, vp, np.clip(bt, 0, npg - 1), lens, scale=0.3, lib=lib)
+    assert np.array_equal(o, oc) and np.array_equal(lse, lc), "table entries not clamped"
+    og, lg = orc.decode(q, _gather_pages(kp, bt), _gather_pages(vp, bt), lens, scale=0.3, lib=lib)
+    _close(o, og, 1e-13, "clamped table vs gathered O")
+    _close(lse, lg, 1e-13, "clamped table vs gathered LSE")
+    # pages 4, 6 and 7 are listed by no sequence (and 1 only past sequence 1's
+    # length): changing them changes nothing; changing page 5 changes sequence 1
+    used = set(np.clip(bt[0, :5], 0, npg - 1).tolist()) | set(np.clip(bt[1, :3], 0, npg - 1).tolist())
+    kp2, vp2 = kp.copy(), vp.copy()
+    for pg in range(npg):
+        if pg not in used:
+            kp2[pg] = _rand((Hkv, ps, D), 180 + pg)
+            vp2[pg] = _rand((Hkv, ps, D), 190 + pg)
+    o2, l2 = orc.decode_paged(q, kp2, vp2, bt, lens, scale=0.3, lib=lib)
+    assert np.array_equal(o, o2) and np.array_equal(lse, l2), "an unused page changed the result"
+    vp2[5, :, 0] = _rand((Hkv, D), 199)
+    o3, _ = orc.decode_paged(q, kp2, vp2, bt, lens, scale=0.3, lib=lib)
+    assert np.array_equal(o3[0], o[0]) and not np.array_equal(o3[1], o[1]), "page 5 row 0 ignored"
+
+
 ALL_PINS = [pin_golden, pin_brute_force, pin_rows_sum_to_one, pin_equal_value_rows,
             pin_causal_row0, pin_single_key, pin_scale_zero, pin_gqa_equals_repeated_mha,
-            pin_decode_equals_last_prefill_row, pin_split_combine, pin_row_subset]
+            pin_decode_equals_last_prefill_row, pin_split_combine, pin_row_subset,
+            pin_paged_equals_gathered, pin_paged_table_clamp_and_unused_pages]

@@ -36,6 +36,11 @@ MUTANTS = {
     "row_subset_ignored": ("int i = job->rows ? job->rows[it] : (int)r;", "int i = (int)r;", 1),
     "combine_weight_by_max": ("double w = exp(ls[s] - L);", "double w = exp(ls[s] - M);", 1),
     "combine_lse_without_max": ("double L = M + log(sum);", "double L = log(sum);", 1),
+    "paged_table_row_stride": ("block_table[(size_t)b * max_pages + j / page_size]",
+                               "block_table[(size_t)b + j / page_size]", 1),
+    "paged_row_reversed": ("(size_t)(j % page_size);", "(size_t)(page_size - 1 - j % page_size);", 1),
+    "paged_head_ignored": ("return ((size_t)page * Hkv + g) * page_size",
+                           "return ((size_t)page * Hkv + 0) * page_size", 1),
 }
 
 
