@@ -114,6 +114,36 @@ int mk_attn_decode(const void *q, const void *k_cache, const void *v_cache, void
                    size_t workspace_bytes, void *stream);
 
 /*
+ * Decode step over a paged key/value cache (the paper's "Paged Attention"
+ * workload, Table 2): the same split-KV computation as mk_attn_decode, with
+ * the cache held in fixed-size pages that a block table lists per sequence.
+ *   q                 [B, Hq, D] bf16
+ *   k_pages, v_pages  [n_pages, Hkv, page_size, D] bf16 page pools; key j
+ *                     of sequence b, kv head g, is row j % page_size of
+ *                     page block_table[b][j / page_size], head g
+ *   block_table       device int32 [B, max_pages] (required); an entry
+ *                     outside [0, n_pages) is read as the nearest valid
+ *                     page (it cannot make the kernel leave the pool);
+ *                     entries at or past ceil(L_b / page_size) are not read
+ *   o, lse            as mk_attn_decode
+ *   page_size         keys per page, a positive multiple of 16
+ *   max_pages         table columns; lengths are clamped into
+ *                     [0, max_pages * page_size]
+ *   n_pages           pages in each pool (>= 1)
+ *   kv_seqlens, n_parts, workspace, workspace_bytes, stream: as
+ *                     mk_attn_decode (the same workspace size)
+ * B * max_pages and max_pages * page_size must fit in 31 bits, as must the
+ * stage count B * Hkv * ceil(max_pages * page_size / 32) (MK_ERR_SHAPE).
+ * The result is mk_attn_decode's on the contiguous cache that gathers each
+ * sequence's pages in table order (up to rounding: bitwise the same).
+ */
+int mk_attn_decode_paged(const void *q, const void *k_pages, const void *v_pages,
+                         const int *block_table, void *o, float *lse, int B, int Hq,
+                         int Hkv, int page_size, int max_pages, int n_pages, int D,
+                         float scale, const int *kv_seqlens, int n_parts,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * Bytes of decode workspace for these sizes: per part, two partial outputs
  * [2, G, D] fp32 (the part's first and last piece, G = Hq / Hkv) and their
  * LSEs [2, G] fp32, the two regions 256-byte aligned.  n_parts = 0 selects

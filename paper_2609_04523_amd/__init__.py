@@ -24,8 +24,8 @@ MK_STATUS = {0: "MK_OK", 1: "MK_ERR_NULL", 2: "MK_ERR_SHAPE", 3: "MK_ERR_UNSUPPO
 
 # every symbol include/mk_attn.h declares
 EXPORTS = ("mk_attn_fwd", "mk_attn_fwd_o32", "mk_attn_decode_workspace_bytes",
-           "mk_attn_decode", "mk_attn_decode_default_parts", "mk_status_str",
-           "mk_attn_version")
+           "mk_attn_decode", "mk_attn_decode_paged", "mk_attn_decode_default_parts",
+           "mk_status_str", "mk_attn_version")
 
 
 class MkAttnError(RuntimeError):
@@ -55,6 +55,9 @@ def lib():
         h.mk_attn_decode_workspace_bytes.restype = sz
         h.mk_attn_decode.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, f, vp, i, vp, sz, vp]
         h.mk_attn_decode.restype = i
+        h.mk_attn_decode_paged.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, vp, i,
+                                           vp, sz, vp]
+        h.mk_attn_decode_paged.restype = i
         h.mk_attn_decode_default_parts.argtypes = [i, i, i]
         h.mk_attn_decode_default_parts.restype = i
         h.mk_status_str.argtypes = [i]
@@ -125,6 +128,15 @@ def mk_attn_decode(q, k_cache, v_cache, o, lse, B, Hq, Hkv, Smax, D, scale, kv_s
                                 _ptr(workspace), int(workspace_bytes), _stream(stream)))
 
 
+def mk_attn_decode_paged(q, k_pages, v_pages, block_table, o, lse, B, Hq, Hkv, page_size,
+                         max_pages, n_pages, D, scale, kv_seqlens, n_parts, workspace,
+                         workspace_bytes, stream=None):
+    _check(lib().mk_attn_decode_paged(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(block_table),
+                                      _ptr(o), _ptr(lse), B, Hq, Hkv, page_size, max_pages,
+                                      n_pages, D, float(scale), _ptr(kv_seqlens), int(n_parts),
+                                      _ptr(workspace), int(workspace_bytes), _stream(stream)))
+
+
 # ---------------------------------------------------------------------------
 # conveniences: allocate outputs with torch, then call the entry points above
 # ---------------------------------------------------------------------------
@@ -176,6 +188,32 @@ def decode(q, k_cache, v_cache, kv_seqlens, *, scale: float | None = None, n_par
     lse = torch.empty((B, Hq), device=q.device, dtype=torch.float32) if with_lse else None
     mk_attn_decode(q, k_cache, v_cache, o, lse, B, Hq, Hkv, Smax, D, scale, kv_seqlens, n_parts,
                    workspace, workspace.numel() * workspace.element_size(), stream)
+    return o, lse
+
+
+def decode_paged(q, k_pages, v_pages, block_table, kv_seqlens, *, scale: float | None = None,
+                 n_parts: int = 0, workspace=None, with_lse: bool = True, stream=None):
+    """q [B,Hq,D], page pools [n_pages,Hkv,page_size,D] bf16, block_table int32
+    [B,max_pages], kv_seqlens int32 [B] -> (o, lse)."""
+    import torch
+    _require(q, "q", torch.bfloat16, 3)
+    _require(k_pages, "k_pages", torch.bfloat16, 4)
+    _require(v_pages, "v_pages", torch.bfloat16, 4)
+    _require(block_table, "block_table", torch.int32, 2)
+    _require(kv_seqlens, "kv_seqlens", torch.int32, 1)
+    B, Hq, D = q.shape
+    n_pages, Hkv, page_size, _ = k_pages.shape
+    max_pages = block_table.shape[1]
+    if scale is None:
+        scale = D ** -0.5
+    need = mk_attn_decode_workspace_bytes(Hq, Hkv, D, n_parts)
+    if workspace is None:
+        workspace = torch.empty(need, device=q.device, dtype=torch.uint8)
+    o = torch.empty((B, Hq, D), device=q.device, dtype=torch.bfloat16)
+    lse = torch.empty((B, Hq), device=q.device, dtype=torch.float32) if with_lse else None
+    mk_attn_decode_paged(q, k_pages, v_pages, block_table, o, lse, B, Hq, Hkv, page_size,
+                         max_pages, n_pages, D, scale, kv_seqlens, n_parts, workspace,
+                         workspace.numel() * workspace.element_size(), stream)
     return o, lse
 
 

@@ -24,6 +24,14 @@
 // and natural-log LSE go to the part's workspace slot 0 (first piece) or 1
 // (last piece).
 //
+// Paged cache (PAGED): K and V live in a pool of pages [n_pages, Hkv,
+// page_size, D]; block_table [B, max_pages] lists the pages of sequence b
+// in key order.  Pages hold a multiple of 16 keys, so each 16-key half of
+// a stage lies in one page: the stage's two page numbers come through the
+// scalar cache (consecutive entries of one table row share its lines) and
+// each lane's 16-byte row chunk is addressed in its half's page.  The
+// stream, the pieces and the merge are those of the contiguous cache.
+//
 // Kernel 2 (dec_merge_kernel), one wave per (batch, query head) row: rows
 // of pairs cut by part boundaries are merged from their pieces by
 // log-sum-exp, LSE = log sum_i exp(LSE_i), O = sum_i exp(LSE_i - LSE) O_i;
@@ -47,8 +55,11 @@ struct DecArgs {
   float* o_part;            // [P, 2, G, D]
   float* lse_part;          // [P, 2, G]
   const int* kv_seqlens;    // [B]
-  int B, Hq, Hkv, Smax, P;
+  int B, Hq, Hkv, Smax, P;  // paged: Smax = max_pages * page_size
   float scale_log2;
+  // paged cache only: kc / vc are page pools [n_pages, Hkv, page_size, D]
+  const int* block_table;   // [B, max_pages]
+  int page_size, max_pages, n_pages;
 };
 
 __device__ __forceinline__ int dec_stages_of_len(int L) {
@@ -174,7 +185,16 @@ struct DecShape {
   static_assert(2 * LOADS_PER_STAGE < 64, "vmcnt range");
 };
 
-template <int D, int QBLOCKS>
+// Page holding table position pi of sequence b (wave-uniform, through the
+// scalar cache), clamped into the pool.
+__device__ __forceinline__ int page_uniform(const DecArgs& a, int b, int pi) {
+  const __attribute__((address_space(4))) int* bt =
+      (const __attribute__((address_space(4))) int*)a.block_table;
+  const int p = bt[(size_t)b * a.max_pages + pi];
+  return p < 0 ? 0 : (p >= a.n_pages ? a.n_pages - 1 : p);
+}
+
+template <int D, int QBLOCKS, bool PAGED>
 __global__ __launch_bounds__(64) void dec_part_kernel(DecArgs a) {
   using S = DecShape<D, QBLOCKS>;
   constexpr int BN = S::BN;
@@ -204,16 +224,39 @@ __global__ __launch_bounds__(64) void dec_part_kernel(DecArgs a) {
   auto issue = [&](const DecCursor& c, uint32_t slot) {
     const int key0 = c.t * BN;
     const int lim = c.L - 1 - key0;  // last valid row of the stage
-    const size_t kv_off = (((size_t)c.b * a.Hkv + c.g) * (size_t)a.Smax + key0) * RB;
-    const char* kt_g = reinterpret_cast<const char*>(a.kc) + kv_off;
-    const char* vt_g = reinterpret_cast<const char*>(a.vc) + kv_off;
+    if constexpr (PAGED) {
+      // pages of rows [0, 16) and [16, 32) (the second is the first when the
+      // stage ends in its first half)
+      const int ps = a.page_size;
+      const int pi0 = key0 / ps;
+      const int pi1 = min(key0 + 16, c.L - 1) / ps;
+      const size_t head0 = ((size_t)page_uniform(a, c.b, pi0) * a.Hkv + c.g) * ps;
+      const size_t head1 = ((size_t)page_uniform(a, c.b, pi1) * a.Hkv + c.g) * ps;
+      const int first0 = pi0 * ps, first1 = pi1 * ps;  // first key of each page
 #pragma unroll
-    for (int blk = 0; blk < S::KV_BLOCKS; ++blk) {
-      const int r = dma_row + blk * S::ROWS_PER_KB;
-      const int ch = ((lane % S::CHUNKS) ^ chunk_swz<D>(r)) * 16;
-      const uint32_t goff = (uint32_t)(min(r, lim) * RB + ch);
-      load_lds16_at(kt_g + goff, slot + blk * 1024);
-      load_lds16_at(vt_g + goff, slot + S::TILE_BYTES + blk * 1024);
+      for (int blk = 0; blk < S::KV_BLOCKS; ++blk) {
+        const int r = dma_row + blk * S::ROWS_PER_KB;
+        const int ch = ((lane % S::CHUNKS) ^ chunk_swz<D>(r)) * 16;
+        const int rr = min(r, lim);
+        const bool hi = rr >= 16;
+        const size_t row = (hi ? head1 : head0) + (size_t)(key0 + rr - (hi ? first1 : first0));
+        const size_t goff = row * RB + ch;
+        load_lds16_at(reinterpret_cast<const char*>(a.kc) + goff, slot + blk * 1024);
+        load_lds16_at(reinterpret_cast<const char*>(a.vc) + goff,
+                      slot + S::TILE_BYTES + blk * 1024);
+      }
+    } else {
+      const size_t kv_off = (((size_t)c.b * a.Hkv + c.g) * (size_t)a.Smax + key0) * RB;
+      const char* kt_g = reinterpret_cast<const char*>(a.kc) + kv_off;
+      const char* vt_g = reinterpret_cast<const char*>(a.vc) + kv_off;
+#pragma unroll
+      for (int blk = 0; blk < S::KV_BLOCKS; ++blk) {
+        const int r = dma_row + blk * S::ROWS_PER_KB;
+        const int ch = ((lane % S::CHUNKS) ^ chunk_swz<D>(r)) * 16;
+        const uint32_t goff = (uint32_t)(min(r, lim) * RB + ch);
+        load_lds16_at(kt_g + goff, slot + blk * 1024);
+        load_lds16_at(vt_g + goff, slot + S::TILE_BYTES + blk * 1024);
+      }
     }
     const char* q_g = reinterpret_cast<const char*>(a.q) + ((size_t)c.b * a.Hq + c.g * G) * RB;
 #pragma unroll

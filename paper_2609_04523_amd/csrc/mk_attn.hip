@@ -12,7 +12,7 @@
 
 namespace {
 
-constexpr int kVersion = 2;
+constexpr int kVersion = 3;
 constexpr int kFwdQB = 1;             // 32-query blocks per wave in the forward kernel
 constexpr int kComputeUnits = 256;    // MI355X
 constexpr int kLdsPerCu = 160 * 1024; // gfx950
@@ -122,9 +122,82 @@ bool dec_layout(int Hq, int Hkv, int D, int n_parts, DecLayout* out) {
   return true;
 }
 
-template <int D, int QB>
+template <int D, int QB, bool PAGED>
 void launch_dec(const mk::DecArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((mk::dec_part_kernel<D, QB>), dim3(a.P), dim3(64), 0, st, a);
+  hipLaunchKernelGGL((mk::dec_part_kernel<D, QB, PAGED>), dim3(a.P), dim3(64), 0, st, a);
+}
+
+// Part kernel for the head dim and group size, then the merge kernel.
+template <bool PAGED>
+int launch_decode(const mk::DecArgs& a, int D, hipStream_t st) {
+  const int qb = dec_qblocks(D, a.Hq / a.Hkv);
+  if (D == 128) {
+    if (qb == 1) launch_dec<128, 1, PAGED>(a, st);
+    else if (qb == 2) launch_dec<128, 2, PAGED>(a, st);
+    else launch_dec<128, 4, PAGED>(a, st);
+  } else {
+    if (qb == 1) launch_dec<64, 1, PAGED>(a, st);
+    else launch_dec<64, 2, PAGED>(a, st);
+  }
+  if (hipGetLastError() != hipSuccess) return MK_ERR_HIP;
+  const unsigned mblocks = (unsigned)(((long long)a.B * a.Hq + 3) / 4);  // one wave per row
+  if (D == 128)
+    hipLaunchKernelGGL(mk::dec_merge_kernel<128>, dim3(mblocks), dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL(mk::dec_merge_kernel<64>, dim3(mblocks), dim3(256), 0, st, a);
+  return hipGetLastError() == hipSuccess ? MK_OK : MK_ERR_HIP;
+}
+
+// Checks shared by both decode entry points (max_keys: keys a sequence can
+// hold).
+int dec_check(const void* q, const void* kc, const void* vc, const void* o, const float* lse,
+              int B, int Hq, int Hkv, long long max_keys, int D, float scale,
+              const int* kv_seqlens, int n_parts, const void* workspace, size_t workspace_bytes,
+              DecLayout* l) {
+  if (!q || !kc || !vc || !o || !kv_seqlens) return MK_ERR_NULL;
+  if (B < 1 || Hq < 1 || Hkv < 1 || max_keys < 1 || D < 1) return MK_ERR_SHAPE;
+  if (Hq % Hkv != 0) return MK_ERR_SHAPE;
+  // stage indices, (batch, head) rows and key positions are 32-bit in the kernels
+  const long long max_stages =
+      (long long)B * Hkv * ((max_keys + mk::kDecStageKeys - 1) / mk::kDecStageKeys);
+  if ((long long)B * Hq > 0x7fffffffLL || max_stages > 0x7fffffffLL || max_keys > 0x7fffffffLL)
+    return MK_ERR_SHAPE;
+  if (D != 64 && D != 128) return MK_ERR_UNSUPPORTED;
+  if (Hq / Hkv > 16) return MK_ERR_UNSUPPORTED;
+  if (n_parts < 0 || n_parts > kMaxParts) return MK_ERR_ARG;
+  if (!isfinite(scale)) return MK_ERR_ARG;
+  if (!aligned(q, 16) || !aligned(kc, 16) || !aligned(vc, 16) || !aligned(o, 16) ||
+      !aligned(kv_seqlens, 4))
+    return MK_ERR_ALIGN;
+  if (lse && !aligned(lse, 4)) return MK_ERR_ALIGN;
+  if (!dec_layout(Hq, Hkv, D, n_parts, l)) return MK_ERR_SHAPE;
+  if (!workspace || workspace_bytes < l->total) return MK_ERR_WORKSPACE;
+  if (!aligned(workspace, 256)) return MK_ERR_ALIGN;
+  return MK_OK;
+}
+
+mk::DecArgs dec_args(const void* q, const void* kc, const void* vc, void* o, float* lse, int B,
+                     int Hq, int Hkv, int max_keys, float scale, const int* kv_seqlens,
+                     const DecLayout& l, void* workspace) {
+  char* ws = static_cast<char*>(workspace);
+  mk::DecArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.kc = static_cast<const uint16_t*>(kc);
+  a.vc = static_cast<const uint16_t*>(vc);
+  a.o = static_cast<uint16_t*>(o);
+  a.lse = lse;
+  a.o_part = reinterpret_cast<float*>(ws);
+  a.lse_part = reinterpret_cast<float*>(ws + l.lse_off);
+  a.kv_seqlens = kv_seqlens;
+  a.B = B;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.Smax = max_keys;
+  a.P = l.parts;
+  a.scale_log2 = scale * mk::kLog2e;
+  a.block_table = nullptr;
+  a.page_size = a.max_pages = a.n_pages = 0;
+  return a;
 }
 
 }  // namespace
@@ -160,59 +233,37 @@ int mk_attn_decode_default_parts(int Hq, int Hkv, int D) {
 int mk_attn_decode(const void* q, const void* k_cache, const void* v_cache, void* o, float* lse,
                    int B, int Hq, int Hkv, int Smax, int D, float scale, const int* kv_seqlens,
                    int n_parts, void* workspace, size_t workspace_bytes, void* stream) {
-  if (!q || !k_cache || !v_cache || !o || !kv_seqlens) return MK_ERR_NULL;
-  if (B < 1 || Hq < 1 || Hkv < 1 || Smax < 1 || D < 1) return MK_ERR_SHAPE;
-  if (Hq % Hkv != 0) return MK_ERR_SHAPE;
-  // stage indices and (batch, head) rows are 32-bit in the kernels
-  const long long max_stages = (long long)B * Hkv * ((Smax + mk::kDecStageKeys - 1) /
-                                                     mk::kDecStageKeys);
-  if ((long long)B * Hq > 0x7fffffffLL || max_stages > 0x7fffffffLL) return MK_ERR_SHAPE;
-  if (D != 64 && D != 128) return MK_ERR_UNSUPPORTED;
-  if (Hq / Hkv > 16) return MK_ERR_UNSUPPORTED;
-  if (n_parts < 0 || n_parts > kMaxParts) return MK_ERR_ARG;
-  if (!isfinite(scale)) return MK_ERR_ARG;
-  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(o, 16) ||
-      !aligned(kv_seqlens, 4))
-    return MK_ERR_ALIGN;
-  if (lse && !aligned(lse, 4)) return MK_ERR_ALIGN;
   DecLayout l;
-  if (!dec_layout(Hq, Hkv, D, n_parts, &l)) return MK_ERR_SHAPE;
-  if (!workspace || workspace_bytes < l.total) return MK_ERR_WORKSPACE;
-  if (!aligned(workspace, 256)) return MK_ERR_ALIGN;
+  const int rc = dec_check(q, k_cache, v_cache, o, lse, B, Hq, Hkv, Smax, D, scale, kv_seqlens,
+                           n_parts, workspace, workspace_bytes, &l);
+  if (rc != MK_OK) return rc;
+  const mk::DecArgs a =
+      dec_args(q, k_cache, v_cache, o, lse, B, Hq, Hkv, Smax, scale, kv_seqlens, l, workspace);
+  return launch_decode<false>(a, D, static_cast<hipStream_t>(stream));
+}
 
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  char* ws = static_cast<char*>(workspace);
-  mk::DecArgs a;
-  a.q = static_cast<const uint16_t*>(q);
-  a.kc = static_cast<const uint16_t*>(k_cache);
-  a.vc = static_cast<const uint16_t*>(v_cache);
-  a.o = static_cast<uint16_t*>(o);
-  a.lse = lse;
-  a.o_part = reinterpret_cast<float*>(ws);
-  a.lse_part = reinterpret_cast<float*>(ws + l.lse_off);
-  a.kv_seqlens = kv_seqlens;
-  a.B = B;
-  a.Hq = Hq;
-  a.Hkv = Hkv;
-  a.Smax = Smax;
-  a.P = l.parts;
-  a.scale_log2 = scale * mk::kLog2e;
-  const int qb = dec_qblocks(D, Hq / Hkv);
-  if (D == 128) {
-    if (qb == 1) launch_dec<128, 1>(a, st);
-    else if (qb == 2) launch_dec<128, 2>(a, st);
-    else launch_dec<128, 4>(a, st);
-  } else {
-    if (qb == 1) launch_dec<64, 1>(a, st);
-    else launch_dec<64, 2>(a, st);
-  }
-  if (hipGetLastError() != hipSuccess) return MK_ERR_HIP;
-  const unsigned mblocks = (unsigned)(((long long)B * Hq + 3) / 4);  // one wave per row
-  if (D == 128)
-    hipLaunchKernelGGL(mk::dec_merge_kernel<128>, dim3(mblocks), dim3(256), 0, st, a);
-  else
-    hipLaunchKernelGGL(mk::dec_merge_kernel<64>, dim3(mblocks), dim3(256), 0, st, a);
-  return hipGetLastError() == hipSuccess ? MK_OK : MK_ERR_HIP;
+int mk_attn_decode_paged(const void* q, const void* k_pages, const void* v_pages,
+                         const int* block_table, void* o, float* lse, int B, int Hq, int Hkv,
+                         int page_size, int max_pages, int n_pages, int D, float scale,
+                         const int* kv_seqlens, int n_parts, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  if (!block_table) return MK_ERR_NULL;
+  if (page_size < 16 || page_size % 16 != 0 || max_pages < 1 || n_pages < 1)
+    return MK_ERR_SHAPE;
+  if ((long long)B * max_pages > 0x7fffffffLL) return MK_ERR_SHAPE;
+  const long long max_keys = (long long)max_pages * page_size;
+  DecLayout l;
+  const int rc = dec_check(q, k_pages, v_pages, o, lse, B, Hq, Hkv, max_keys, D, scale,
+                           kv_seqlens, n_parts, workspace, workspace_bytes, &l);
+  if (rc != MK_OK) return rc;
+  if (!aligned(block_table, 4)) return MK_ERR_ALIGN;
+  mk::DecArgs a = dec_args(q, k_pages, v_pages, o, lse, B, Hq, Hkv, (int)max_keys, scale,
+                           kv_seqlens, l, workspace);
+  a.block_table = block_table;
+  a.page_size = page_size;
+  a.max_pages = max_pages;
+  a.n_pages = n_pages;
+  return launch_decode<true>(a, D, static_cast<hipStream_t>(stream));
 }
 
 const char* mk_status_str(int status) {

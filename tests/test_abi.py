@@ -43,7 +43,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert mk.mk_attn_version() == 2
+    assert mk.mk_attn_version() == 3
     names = ["MK_OK", "MK_ERR_NULL", "MK_ERR_SHAPE", "MK_ERR_UNSUPPORTED", "MK_ERR_ALIGN",
              "MK_ERR_WORKSPACE", "MK_ERR_HIP", "MK_ERR_ARG"]
     for code, name in enumerate(names):
@@ -114,6 +114,41 @@ def test_decode_validation(lib):
     assert dec_rc(lib, ws_bytes=need - 1) == 5
     assert dec_rc(lib, parts=100, ws_bytes=lib.mk_attn_decode_workspace_bytes(8, 2, 128, 99)) == 5
     assert dec_rc(lib, ws=P + 16) == 4  # workspace must be 256-byte aligned
+
+
+def paged_rc(lib, *, q=P, kp=P, vp=P, bt=P, o=P, lse=None, B=2, Hq=8, Hkv=2, ps=16,
+             max_pages=32, n_pages=64, D=128, scale=0.1, seqlens=P, parts=0, ws=P,
+             ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = lib.mk_attn_decode_workspace_bytes(max(Hq, 1), max(Hkv, 1), D, max(parts, 0))
+    return lib.mk_attn_decode_paged(q, kp, vp, bt, o, lse, B, Hq, Hkv, ps, max_pages, n_pages, D,
+                                    scale, seqlens, parts, ws, ws_bytes, None)
+
+
+def test_decode_paged_validation(lib):
+    for name in ("q", "kp", "vp", "bt", "o", "seqlens"):
+        assert paged_rc(lib, **{name: None}) == 1
+    for name in ("B", "Hq", "Hkv", "max_pages", "n_pages"):
+        assert paged_rc(lib, **{name: 0}) == 2
+    for ps in (0, 8, 24, -16):  # page size: a positive multiple of 16
+        assert paged_rc(lib, ps=ps) == 2
+    assert paged_rc(lib, Hq=6, Hkv=4) == 2
+    # 32-bit limits: table entries, keys per sequence, key stages
+    assert paged_rc(lib, B=1 << 16, max_pages=1 << 16) == 2
+    assert paged_rc(lib, B=1, ps=1 << 16, max_pages=1 << 16) == 2
+    assert paged_rc(lib, B=1 << 12, Hkv=64, Hq=64, ps=4096, max_pages=64) == 2
+    assert paged_rc(lib, D=96) == 3
+    assert paged_rc(lib, Hq=34, Hkv=2) == 3
+    assert paged_rc(lib, parts=-1, ws_bytes=1 << 30) == 7
+    assert paged_rc(lib, scale=math.inf) == 7
+    for name in ("q", "kp", "vp", "o"):
+        assert paged_rc(lib, **{name: P_ODD}) == 4
+    assert paged_rc(lib, bt=P + 2) == 4
+    assert paged_rc(lib, seqlens=P + 2) == 4
+    assert paged_rc(lib, ws=None) == 5
+    need = lib.mk_attn_decode_workspace_bytes(8, 2, 128, 0)
+    assert paged_rc(lib, ws_bytes=need - 1) == 5
+    assert paged_rc(lib, ws=P + 64) == 4
 
 
 def test_decode_default_parts(lib):

@@ -117,6 +117,49 @@ def decode_inputs(B: int, Hq: int, Hkv: int, Smax: int, D: int, seed: int,
     return q.to(torch.bfloat16), kc.to(torch.bfloat16), vc.to(torch.bfloat16), lens
 
 
+NAN_BF16_BITS = 0x7FC0
+
+
+def paged_layout(k_cache: torch.Tensor, v_cache: torch.Tensor, page_size: int, seed: int,
+                 extra_pages: int = 0, lens=None):
+    """Scatter contiguous caches [B,Hkv,Smax,D] into page pools
+    [n_pages,Hkv,page_size,D] under a seeded random page assignment.
+
+    Page i of sequence b (keys [i*page_size, (i+1)*page_size)) goes to
+    physical page block_table[b, i], a seeded permutation of all
+    B*max_pages + extra_pages pool pages.  Pool pages no table lists, and
+    rows at or past a sequence's length when ``lens`` is given, hold NaN,
+    so a read of them poisons the result.  Returns (k_pages, v_pages,
+    block_table int32 [B, max_pages])."""
+    B, Hkv, Smax, D = k_cache.shape
+    if Smax % page_size:
+        raise ValueError("Smax must be a multiple of page_size")
+    mp = Smax // page_size
+    n_pages = B * mp + extra_pages
+    perm = torch.randperm(n_pages, generator=_gen(seed))
+    bt = perm[: B * mp].reshape(B, mp).to(torch.int32)
+    kp = torch.full((n_pages, Hkv, page_size, D), float("nan"), dtype=torch.bfloat16)
+    vp = torch.full_like(kp, float("nan"))
+    # [B, Hkv, mp, ps, D] -> [B, mp, Hkv, ps, D] -> rows of the pool
+    src_k = k_cache.reshape(B, Hkv, mp, page_size, D).transpose(1, 2).reshape(B * mp, Hkv,
+                                                                                page_size, D)
+    src_v = v_cache.reshape(B, Hkv, mp, page_size, D).transpose(1, 2).reshape(B * mp, Hkv,
+                                                                                page_size, D)
+    if lens is not None:
+        src_k, src_v = src_k.clone(), src_v.clone()
+        key = torch.arange(Smax).reshape(mp, page_size)
+        for b in range(B):
+            L = max(0, min(int(lens[b]), Smax))
+            dead = key >= L                                   # [mp, ps]
+            src_k[b * mp:(b + 1) * mp].view(torch.int16).masked_fill_(
+                dead[:, None, :, None].expand(mp, Hkv, page_size, D), NAN_BF16_BITS)
+            src_v[b * mp:(b + 1) * mp].view(torch.int16).masked_fill_(
+                dead[:, None, :, None].expand(mp, Hkv, page_size, D), NAN_BF16_BITS)
+    kp[bt.reshape(-1).long()] = src_k
+    vp[bt.reshape(-1).long()] = src_v
+    return kp, vp, bt
+
+
 def sample_rows(B: int, Hq: int, S: int, nrows: int, seed: int) -> torch.Tensor:
     """int32 [B,Hq,nrows] of query rows: 0 and S-1 plus nrows-2 distinct
     rows drawn from a per-(b, hq) seeded permutation."""
