@@ -161,6 +161,8 @@ def main():
     ap.add_argument("--decode", default="c5_decode_b64")
     ap.add_argument("--parts", type=int, default=0, help="decode parts (0 = library default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--page-size", type=int, default=16,
+                    help="page size of the paged-decode leg (0 skips the leg)")
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="query rows per head timed for the CPU oracle baseline (0: all)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -223,6 +225,14 @@ def main():
     del q, k, v
     qd, kc, vc, lens = workloads.config_inputs(dcfg)
     caches = [(kc.to(dev), vc.to(dev)), (kc.to(dev).clone(), vc.to(dev).clone())]
+    paged = []
+    if args.page_size:
+        # the same keys scattered over pages in a seeded random order (two
+        # copies of the pools, used alternately like the caches above)
+        kp, vp, bt = workloads.paged_layout(kc, vc, args.page_size, seed=dcfg.seed + 7,
+                                            extra_pages=64)
+        paged = [(kp.to(dev), vp.to(dev), bt.to(dev)) for _ in range(2)]
+        del kp, vp, bt
     del kc, vc
     qd = qd.to(dev)
     lens_d = lens.to(dev)
@@ -246,6 +256,12 @@ def main():
         kcc, vcc = caches[i & 1]
         mk.mk_attn_decode(qd, kcc, vcc, od, lsed, B, Hq, Hkv, Smax, D, dcfg.scale, lens_d,
                           args.parts, ws, ws_bytes, stream)
+
+    def decode_paged(i):
+        kp_, vp_, bt_ = paged[i & 1]
+        mk.mk_attn_decode_paged(qd, kp_, vp_, bt_, od, lsed, B, Hq, Hkv, args.page_size,
+                                bt_.shape[1], kp_.shape[0], D, dcfg.scale, lens_d, args.parts,
+                                ws, ws_bytes, stream)
 
     if args.calib_copy_mib:
         n = args.calib_copy_mib << 20
@@ -282,6 +298,19 @@ def main():
     ev[2].record(stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    paged_ms = None
+    if paged:
+        # the paged-decode leg, timed after the step the same way
+        for i in range(args.warmup):
+            decode_paged(i)
+        evp = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        evp[0].record(stream)
+        for i in range(K):
+            decode_paged(i)
+        evp[1].record(stream)
+        torch.cuda.synchronize()
+        paged_ms = evp[0].elapsed_time(evp[1]) / K
     ms_step = (t1 - t0) * 1e3 / K
     pre_ms = ev[0].elapsed_time(ev[1]) / K  # average launch duration
     dec_ms = ev[1].elapsed_time(ev[2]) / K
@@ -291,7 +320,8 @@ def main():
     dec_bytes = 4 * D * Hkv * sum_l + (B * Hq * D * 2) * 2 + B * Hq * 4  # K+V, q, o, lse
     dec_gbs = dec_bytes / (dec_ms * 1e-3) / 1e9
     log(f"[bench] prefill {pre_ms * 1e3:.1f} us ({tflops:.1f} TFLOP/s), "
-        f"decode {dec_ms * 1e3:.1f} us ({dec_gbs:.1f} GB/s), step {ms_step:.3f} ms")
+        f"decode {dec_ms * 1e3:.1f} us ({dec_gbs:.1f} GB/s), step {ms_step:.3f} ms"
+        + (f", paged decode {paged_ms * 1e3:.1f} us" if paged_ms is not None else ""))
 
     digest = kernel_source_digest()
     traffic_pre = read_traffic(f"fwd_kernel_{pcfg.name}_counters.md", digest)
@@ -345,6 +375,18 @@ def main():
         },
         "cpu_baseline": None,
     }
+    if paged_ms is not None:
+        p_gbs = dec_bytes / (paged_ms * 1e-3) / 1e9
+        result["paged_decode"] = {
+            "workload": (f"{dcfg.name} with its cache in {args.page_size}-key pages "
+                         "in a seeded random order (block table)"),
+            "value": round(p_gbs, 1),
+            "unit": "GB/s",
+            "us": round(paged_ms * 1e3, 2),
+            "roofline": {"bound": "hbm", "achieved": round(p_gbs, 1), "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": round(p_gbs / PEAK_HBM_GBS, 4),
+                         "traffic": None},
+        }
 
     if not args.no_cpu_baseline:
         from oracle import oracle as orc  # timed CPU baseline only
