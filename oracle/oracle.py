@@ -66,6 +66,9 @@ def _declare(lib):
     lib.oracle_decode_paged.argtypes = [_u16p, _u16p, _u16p, _i32p, i, i, i, i, i, i, i, d,
                                         _i32p, _f64p, _f64p]
     lib.oracle_decode_paged.restype = i
+    lib.oracle_attn_fwd_varlen.argtypes = [_u16p, _u16p, _u16p, _i32p, _i32p, i, i, i, i, i, i,
+                                           i, d, _f64p, _f64p]
+    lib.oracle_attn_fwd_varlen.restype = i
     lib.oracle_version.restype = i
     return lib
 
@@ -161,6 +164,30 @@ def decode(q, k_cache, v_cache, kv_seqlens, *, scale: float,
                            _ptr(o, _f64p), _ptr(lse, _f64p), threads or default_threads())
     if rc != 0:
         raise ValueError(f"oracle_decode failed ({rc})")
+    return o, lse
+
+
+def attn_fwd_varlen(q, k, v, cu_seqlens_q, cu_seqlens_k, *, causal: bool, scale: float,
+                    lib=None):
+    """Packed ragged forward.  q [total_q,Hq,D], k/v [total_k,Hkv,D], cu_seqlens int32
+    [B+1] -> (o [total_q,Hq,D], lse [Hq,total_q]); rows no sequence owns stay NaN."""
+    lib = lib or load()
+    q, k, v = _u16(q), _u16(k), _u16(v)
+    total_q, Hq, D = q.shape
+    total_k, Hkv, _ = k.shape
+    cq = np.ascontiguousarray(cu_seqlens_q, dtype=np.int32)
+    ck = np.ascontiguousarray(cu_seqlens_k, dtype=np.int32)
+    if cq.shape != ck.shape or cq.ndim != 1 or cq.shape[0] < 2:
+        raise ValueError("cu_seqlens_q / cu_seqlens_k must both be [B+1]")
+    B = cq.shape[0] - 1
+    o = np.full((total_q, Hq, D), np.nan, np.float64)
+    lse = np.full((Hq, total_q), np.nan, np.float64)
+    rc = lib.oracle_attn_fwd_varlen(_ptr(q, _u16p), _ptr(k, _u16p), _ptr(v, _u16p),
+                                    _ptr(cq, _i32p), _ptr(ck, _i32p), B, Hq, Hkv, total_q,
+                                    total_k, D, int(bool(causal)), float(scale), _ptr(o, _f64p),
+                                    _ptr(lse, _f64p))
+    if rc != 0:
+        raise ValueError(f"oracle_attn_fwd_varlen failed ({rc})")
     return o, lse
 
 

@@ -1,7 +1,9 @@
 /*
  * oracle_attn.c -- plain fp64 CPU oracle for causal grouped-query
- * scaled-dot-product attention (forward), its split-KV decode form, and
- * decode over a paged cache (the "Paged Attention" workload of Table 2).
+ * scaled-dot-product attention (forward), its split-KV decode form,
+ * decode over a paged cache (the "Paged Attention" workload of Table 2),
+ * and the forward over packed variable-length sequences (the ragged
+ * batches of the "Ragged Paged Attention" workload of Table 2).
  *
  * TEST INFRASTRUCTURE ONLY.  This file is the checker the GPU path is
  * measured against; it is loaded by the test suite, by the smoke check and
@@ -39,7 +41,8 @@
  * causal row 0), invariants (rows of P sum to 1, GQA equals MHA with
  * repeated K/V heads, decode equals the last prefill row, split-combine
  * equals unsplit, paged decode equals decode on the cache gathered through
- * the block table) and hand-derived values stored under tests/golden/.
+ * the block table, a packed ragged batch equals each of its sequences run
+ * alone) and hand-derived values stored under tests/golden/.
  *
  * Build: plain C11, no -ffast-math, libm only (gcc -O2 -shared -fPIC).
  */
@@ -458,4 +461,91 @@ int oracle_decode_paged(const uint16_t *q, const uint16_t *k_pages,
     return 0;
 }
 
-int oracle_version(void) { return 2; }
+/* ------------------------------------------------------------------ */
+/* Variable-length (ragged) forward over packed sequences              */
+/* ------------------------------------------------------------------ */
+
+/* Clamped [start, end) of sequence b from cumulative offsets cu[0..B]. */
+static void seq_range(const int32_t *cu, int b, int total, int *start, int *end)
+{
+    int s0 = cu[b], s1 = cu[b + 1];
+    if (s0 < 0) s0 = 0;
+    if (s0 > total) s0 = total;
+    if (s1 < s0) s1 = s0;
+    if (s1 > total) s1 = total;
+    *start = s0;
+    *end = s1;
+}
+
+/*
+ * Packed layout, token-major with the heads inside a token: q and o
+ * [total_q, Hq, D], k and v [total_k, Hkv, D].  Sequence b owns query
+ * tokens [cu_q[b], cu_q[b+1]) and key tokens [cu_k[b], cu_k[b+1]) (offsets
+ * clamped into [0, total] and made non-decreasing).  Query row i of
+ * sequence b, head hq, attends to its sequence's keys j < Skv_b, and when
+ * causal only to j <= i + Skv_b - Sq_b (bottom-right alignment, so a
+ * sequence whose queries are its last tokens -- a chunk of a longer prompt
+ * or a single decode token -- sees every earlier key).  The plain
+ * definition per row, written out here with strided rows:
+ *   s_j = scale * q . k_j,  O = sum_j softmax(s)_j v_j,  LSE = log sum exp s.
+ * lse [Hq, total_q].  Rows no sequence owns are not written.
+ */
+int oracle_attn_fwd_varlen(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                           const int32_t *cu_q, const int32_t *cu_k, int B, int Hq,
+                           int Hkv, int total_q, int total_k, int D, int causal,
+                           double scale, double *o, double *lse)
+{
+    if (!q || !k || !v || !cu_q || !cu_k || !o || !lse) return -1;
+    if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || D < 1 || total_q < 0 ||
+        total_k < 0 || (causal != 0 && causal != 1))
+        return -2;
+    const int G = Hq / Hkv;
+    double *s = malloc(sizeof(double) * (size_t)(total_k > 0 ? total_k : 1));
+    if (!s) return -3;
+    for (int b = 0; b < B; ++b) {
+        int q0, q1, k0, k1;
+        seq_range(cu_q, b, total_q, &q0, &q1);
+        seq_range(cu_k, b, total_k, &k0, &k1);
+        const int Sq = q1 - q0, Skv = k1 - k0;
+        for (int hq = 0; hq < Hq; ++hq) {
+            const int g = hq / G;
+            for (int i = 0; i < Sq; ++i) {
+                const uint16_t *q_row = q + ((size_t)(q0 + i) * Hq + hq) * D;
+                double *o_row = o + ((size_t)(q0 + i) * Hq + hq) * D;
+                double *lse_row = lse + (size_t)hq * total_q + (q0 + i);
+                int n_valid = Skv;
+                if (causal && i + Skv - Sq + 1 < n_valid) n_valid = i + Skv - Sq + 1;
+                if (n_valid <= 0) {
+                    for (int d = 0; d < D; ++d) o_row[d] = 0.0;
+                    *lse_row = -INFINITY;
+                    continue;
+                }
+                double m = -INFINITY;
+                for (int j = 0; j < n_valid; ++j) {
+                    const uint16_t *k_row = k + ((size_t)(k0 + j) * Hkv + g) * D;
+                    double dot = 0.0;
+                    for (int d = 0; d < D; ++d)
+                        dot += bf16_bits_to_double(q_row[d]) * bf16_bits_to_double(k_row[d]);
+                    s[j] = scale * dot;
+                    if (s[j] > m) m = s[j];
+                }
+                double l = 0.0;
+                for (int j = 0; j < n_valid; ++j) {
+                    s[j] = exp(s[j] - m);
+                    l += s[j];
+                }
+                for (int d = 0; d < D; ++d) o_row[d] = 0.0;
+                for (int j = 0; j < n_valid; ++j) {
+                    const uint16_t *v_row = v + ((size_t)(k0 + j) * Hkv + g) * D;
+                    const double p = s[j] / l;
+                    for (int d = 0; d < D; ++d) o_row[d] += p * bf16_bits_to_double(v_row[d]);
+                }
+                *lse_row = m + log(l);
+            }
+        }
+    }
+    free(s);
+    return 0;
+}
+
+int oracle_version(void) { return 3; }

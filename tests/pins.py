@@ -24,7 +24,10 @@ The facts, none of which re-types the oracle's own formula:
   * a paged cache is a relayout: paged decode equals contiguous decode on
     the cache gathered through the block table (numpy indexing), whatever
     the page size, with out-of-range table entries read as the nearest
-    valid page and pages no sequence lists ignored.
+    valid page and pages no sequence lists ignored;
+  * a packed ragged batch equals each of its sequences run alone through
+    the batched forward (bottom-right causal per sequence), rows no
+    sequence owns are not written, and out-of-range offsets clamp.
 """
 from __future__ import annotations
 
@@ -342,7 +345,68 @@ def pin_paged_table_clamp_and_unused_pages(lib):
     assert np.array_equal(o3[0], o[0]) and not np.array_equal(o3[1], o[1]), "page 5 row 0 ignored"
 
 
+VARLEN_CASES = [
+    # Hq, Hkv, D, [(Sq_b, Skv_b), ...]
+    (4, 2, 8, [(5, 5), (1, 9), (0, 4), (7, 3), (6, 6)]),  # decode-like, empty, Sq > Skv
+    (2, 1, 16, [(12, 20), (3, 3)]),                        # a chunk of a longer prompt
+    (3, 3, 4, [(4, 0), (2, 2)]),                           # a sequence without keys
+]
+
+
+def _varlen_inputs(n, Hq, Hkv, D, seqs):
+    cq = np.concatenate([[0], np.cumsum([a for a, _ in seqs])]).astype(np.int32)
+    ck = np.concatenate([[0], np.cumsum([b for _, b in seqs])]).astype(np.int32)
+    q = _rand((int(cq[-1]), Hq, D), 200 + n, -2.5, 2.5)
+    k = _rand((max(int(ck[-1]), 1), Hkv, D), 210 + n, -2.5, 2.5)
+    v = _rand((max(int(ck[-1]), 1), Hkv, D), 220 + n)
+    return q, k, v, cq, ck
+
+
+def pin_varlen_equals_each_sequence(lib):
+    for causal in (True, False):
+        for n, (Hq, Hkv, D, seqs) in enumerate(VARLEN_CASES):
+            q, k, v, cq, ck = _varlen_inputs(n, Hq, Hkv, D, seqs)
+            o, lse = orc.attn_fwd_varlen(q, k, v, cq, ck, causal=causal, scale=0.4, lib=lib)
+            for b, (Sq, Skv) in enumerate(seqs):
+                if Sq == 0:
+                    continue
+                ob = o[cq[b]:cq[b + 1]].transpose(1, 0, 2)
+                lb = lse[:, cq[b]:cq[b + 1]]
+                if Skv == 0:
+                    assert np.all(ob == 0) and np.all(np.isneginf(lb)), "keyless sequence"
+                    continue
+                qb = np.ascontiguousarray(q[cq[b]:cq[b + 1]].transpose(1, 0, 2)[None])
+                kb = np.ascontiguousarray(k[ck[b]:ck[b + 1]].transpose(1, 0, 2)[None])
+                vb = np.ascontiguousarray(v[ck[b]:ck[b + 1]].transpose(1, 0, 2)[None])
+                o1, l1 = orc.attn_fwd(qb, kb, vb, causal=causal, scale=0.4, lib=lib)
+                _close(ob, o1[0], 1e-14, f"varlen case {n} seq {b} causal={causal} O")
+                _close(lb, l1[0], 1e-14, f"varlen case {n} seq {b} causal={causal} LSE")
+
+
+def pin_varlen_gaps_and_clamped_offsets(lib):
+    Hq, Hkv, D = 2, 1, 8
+    q = _rand((12, Hq, D), 231)
+    k = _rand((10, Hkv, D), 232)
+    v = _rand((10, Hkv, D), 233)
+    # query rows 3..4 and 9..11 belong to no sequence; offsets past the
+    # totals clamp
+    cq = np.array([0, 3, 5, 9], np.int32)
+    ck = np.array([0, 4, 4, 99], np.int32)
+    cq_gap = np.array([0, 3, 3, 3], np.int32)  # same first sequence, nothing else
+    o, lse = orc.attn_fwd_varlen(q, k, v, np.array([0, 3, 5, 9], np.int32), ck, causal=True,
+                                 scale=0.5, lib=lib)
+    og, lg = orc.attn_fwd_varlen(q, k, v, cq_gap, ck, causal=True, scale=0.5, lib=lib)
+    assert np.array_equal(o[:3], og[:3]) and np.array_equal(lse[:, :3], lg[:, :3])
+    assert np.all(np.isnan(og[3:])) and np.all(np.isnan(lg[:, 3:])), "unowned rows written"
+    # sequence 2: queries 5..8, keys clamp to [4, 10)
+    oc, lc = orc.attn_fwd_varlen(q, k, v, cq, np.array([0, 4, 4, 10], np.int32), causal=True,
+                                 scale=0.5, lib=lib)
+    assert np.array_equal(o[:9], oc[:9]) and np.array_equal(lse[:, :9], lc[:, :9]), \
+        "offsets not clamped"
+
+
 ALL_PINS = [pin_golden, pin_brute_force, pin_rows_sum_to_one, pin_equal_value_rows,
             pin_causal_row0, pin_single_key, pin_scale_zero, pin_gqa_equals_repeated_mha,
             pin_decode_equals_last_prefill_row, pin_split_combine, pin_row_subset,
-            pin_paged_equals_gathered, pin_paged_table_clamp_and_unused_pages]
+            pin_paged_equals_gathered, pin_paged_table_clamp_and_unused_pages,
+            pin_varlen_equals_each_sequence, pin_varlen_gaps_and_clamped_offsets]

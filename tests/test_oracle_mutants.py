@@ -41,6 +41,12 @@ MUTANTS = {
     "paged_row_reversed": ("(size_t)(j % page_size);", "(size_t)(page_size - 1 - j % page_size);", 1),
     "paged_head_ignored": ("return ((size_t)page * Hkv + g) * page_size",
                            "return ((size_t)page * Hkv + 0) * page_size", 1),
+    "varlen_causal_top_left": ("if (causal && i + Skv - Sq + 1 < n_valid) n_valid = i + Skv - Sq + 1;",
+                               "if (causal && i + 1 < n_valid) n_valid = i + 1;", 1),
+    "varlen_lse_token_major": ("lse_row = lse + (size_t)hq * total_q + (q0 + i);",
+                               "lse_row = lse + (size_t)(q0 + i) * Hq + hq;", 1),
+    "varlen_key_start_ignored": ("const uint16_t *k_row = k + ((size_t)(k0 + j) * Hkv + g) * D;",
+                                 "const uint16_t *k_row = k + ((size_t)(j) * Hkv + g) * D;", 1),
 }
 
 
