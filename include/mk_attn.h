@@ -80,6 +80,37 @@ int mk_attn_fwd_o32(const void *q, const void *k, const void *v, float *o, float
                     int causal, float scale, const int *kv_seqlens, void *stream);
 
 /*
+ * Forward over a packed batch of variable-length sequences (the ragged
+ * batches of the paper's "Ragged Paged Attention" workload, Table 2): each
+ * sequence is attended on its own, with the same computation as
+ * mk_attn_fwd.  Sequences with one query token are decode steps, so prefill
+ * chunks and decode tokens can share one call.
+ *   q, o   [total_q, Hq, D] bf16, token-major (a token's Hq heads adjacent);
+ *          o is written only at rows some sequence owns
+ *   k, v   [total_k, Hkv, D] bf16
+ *   lse    [Hq, total_q] fp32 natural-log LSE (written at owned rows), or
+ *          NULL to skip
+ *   cu_seqlens_q, cu_seqlens_k  device int32 [B + 1]: sequence b owns query
+ *          tokens [cu_seqlens_q[b], cu_seqlens_q[b + 1]) and key tokens
+ *          [cu_seqlens_k[b], cu_seqlens_k[b + 1]); each offset is clamped
+ *          into [0, total] on the device and a decreasing pair gives an empty
+ *          range, so no offset makes the kernel leave the tensors.
+ *          Sequences must not share query rows (their writes would race).
+ *   max_seqlen_q  at least every sequence's query count: the grid covers
+ *          that many rows per sequence, and rows past it are not computed
+ *   causal 0 or 1; causal is bottom-right per sequence: query i of a
+ *          sequence with Sq queries and Skv keys sees keys j <= i + Skv - Sq
+ *          (its queries are its last Sq tokens)
+ *   B, Hq, Hkv, max_seqlen_q, total_q, total_k >= 1, Hq % Hkv == 0,
+ *   D in {64, 128}; scale, stream as mk_attn_fwd
+ * Returns MK_OK or an mk_status; asynchronous on `stream`.
+ */
+int mk_attn_fwd_varlen(const void *q, const void *k, const void *v, void *o, float *lse,
+                       const int *cu_seqlens_q, const int *cu_seqlens_k, int B, int Hq,
+                       int Hkv, int max_seqlen_q, int total_q, int total_k, int D,
+                       int causal, float scale, void *stream);
+
+/*
  * Decode step: one query token per sequence against a key/value cache
  * (the decode step of the paper's paged-attention workloads, Table 2),
  * computed as split-KV attention whose per-split results are merged by

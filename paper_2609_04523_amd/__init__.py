@@ -23,8 +23,8 @@ MK_STATUS = {0: "MK_OK", 1: "MK_ERR_NULL", 2: "MK_ERR_SHAPE", 3: "MK_ERR_UNSUPPO
              4: "MK_ERR_ALIGN", 5: "MK_ERR_WORKSPACE", 6: "MK_ERR_HIP", 7: "MK_ERR_ARG"}
 
 # every symbol include/mk_attn.h declares
-EXPORTS = ("mk_attn_fwd", "mk_attn_fwd_o32", "mk_attn_decode_workspace_bytes",
-           "mk_attn_decode", "mk_attn_decode_paged", "mk_attn_decode_default_parts",
+EXPORTS = ("mk_attn_fwd", "mk_attn_fwd_o32", "mk_attn_fwd_varlen",
+           "mk_attn_decode_workspace_bytes", "mk_attn_decode", "mk_attn_decode_paged", "mk_attn_decode_default_parts",
            "mk_status_str", "mk_attn_version")
 
 
@@ -51,6 +51,8 @@ def lib():
         h.mk_attn_fwd.restype = i
         h.mk_attn_fwd_o32.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, vp, vp]
         h.mk_attn_fwd_o32.restype = i
+        h.mk_attn_fwd_varlen.argtypes = [vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, i, f, vp]
+        h.mk_attn_fwd_varlen.restype = i
         h.mk_attn_decode_workspace_bytes.argtypes = [i, i, i, i]
         h.mk_attn_decode_workspace_bytes.restype = sz
         h.mk_attn_decode.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, f, vp, i, vp, sz, vp]
@@ -121,6 +123,14 @@ def mk_attn_fwd_o32(q, k, v, o, lse, B, Hq, Hkv, Sq, Skv, D, causal, scale, kv_s
                                  _stream(stream)))
 
 
+def mk_attn_fwd_varlen(q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, B, Hq, Hkv, max_seqlen_q,
+                       total_q, total_k, D, causal, scale, stream=None):
+    _check(lib().mk_attn_fwd_varlen(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse),
+                                    _ptr(cu_seqlens_q), _ptr(cu_seqlens_k), B, Hq, Hkv,
+                                    max_seqlen_q, total_q, total_k, D, int(causal), float(scale),
+                                    _stream(stream)))
+
+
 def mk_attn_decode(q, k_cache, v_cache, o, lse, B, Hq, Hkv, Smax, D, scale, kv_seqlens,
                    n_parts, workspace, workspace_bytes, stream=None):
     _check(lib().mk_attn_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(o), _ptr(lse), B,
@@ -166,6 +176,31 @@ def fwd(q, k, v, *, causal: bool = True, scale: float | None = None, kv_seqlens=
     lse = torch.empty((B, Hq, Sq), device=q.device, dtype=torch.float32) if with_lse else None
     entry = mk_attn_fwd_o32 if out_fp32 else mk_attn_fwd
     entry(q, k, v, o, lse, B, Hq, Hkv, Sq, Skv, D, causal, scale, kv_seqlens, stream)
+    return o, lse
+
+
+def fwd_varlen(q, k, v, cu_seqlens_q, cu_seqlens_k, max_seqlen_q: int, *, causal: bool = True,
+               scale: float | None = None, with_lse: bool = True, stream=None):
+    """Packed ragged forward.  q [total_q,Hq,D], k/v [total_k,Hkv,D] bf16,
+    cu_seqlens int32 [B+1] (device) -> (o [total_q,Hq,D], lse [Hq,total_q] or None).
+    Rows no sequence owns are left as allocated (uninitialised)."""
+    import torch
+    _require(q, "q", torch.bfloat16, 3)
+    _require(k, "k", torch.bfloat16, 3)
+    _require(v, "v", torch.bfloat16, 3)
+    _require(cu_seqlens_q, "cu_seqlens_q", torch.int32, 1)
+    _require(cu_seqlens_k, "cu_seqlens_k", torch.int32, 1)
+    total_q, Hq, D = q.shape
+    total_k, Hkv, _ = k.shape
+    B = cu_seqlens_q.shape[0] - 1
+    if cu_seqlens_k.shape[0] != B + 1:
+        raise ValueError("cu_seqlens_q and cu_seqlens_k must have the same length")
+    if scale is None:
+        scale = D ** -0.5
+    o = torch.empty((total_q, Hq, D), device=q.device, dtype=torch.bfloat16)
+    lse = torch.empty((Hq, total_q), device=q.device, dtype=torch.float32) if with_lse else None
+    mk_attn_fwd_varlen(q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, B, Hq, Hkv, max_seqlen_q,
+                       total_q, total_k, D, causal, scale, stream)
     return o, lse
 
 

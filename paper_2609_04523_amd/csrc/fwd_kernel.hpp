@@ -43,7 +43,23 @@ struct FwdArgs {
   int n_qtiles;
   int xcd_groups;     // 1: (batch, kv head) groups spread over the 8 XCDs
   float scale_log2;   // scale * log2(e)
+  // packed ragged batches only: q, o [total_q, Hq, D], k, v [total_k, Hkv, D],
+  // sequence b = query tokens [cu_q[b], cu_q[b+1]), keys [cu_k[b], cu_k[b+1]),
+  // lse [Hq, total_q]; Sq is then the largest query length
+  const int* cu_q;
+  const int* cu_k;
+  int total_q, total_k;
 };
+
+// Tokens [start, end) of sequence b from cumulative offsets, clamped into
+// [0, total] and non-decreasing, so no offset can lead outside the tensor.
+__device__ __forceinline__ void fwd_seq_range(const int* cu, int b, int total, int& start,
+                                              int& len) {
+  const int s0 = clamp_len(cu[b], total);
+  const int s1 = clamp_len(cu[b + 1], total);
+  start = s0;
+  len = s1 > s0 ? s1 - s0 : 0;
+}
 
 template <int D, int QB>
 struct FwdShape {
@@ -91,8 +107,9 @@ __device__ __forceinline__ void fwd_map_block(int bid, const FwdArgs& a, int& qt
 
 // POS_SCALE: scale > 0, so the row maximum can be taken on raw scores and
 // the scale folded into the exponent's FMA.  Otherwise scores are scaled
-// first (scale 0 and negative scales).
-template <int D, bool CAUSAL, bool OUT_F32, int QB, bool POS_SCALE>
+// first (scale 0 and negative scales).  VARLEN: a packed ragged batch (see
+// FwdArgs); only where rows live changes, the tile pipeline is the same.
+template <int D, bool CAUSAL, bool OUT_F32, int QB, bool POS_SCALE, bool VARLEN>
 __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   using S = FwdShape<D, QB>;
   constexpr int BN = S::BN;
@@ -116,21 +133,49 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   fwd_map_block(blockIdx.x, a, qt, hq, b);
   const int G = a.Hq / a.Hkv;
   const int g = hq / G;
-  const int L = a.kv_seqlens ? clamp_len(a.kv_seqlens[b], a.Skv) : a.Skv;
-  const int off = L - a.Sq;  // bottom-right causal alignment
+  // Where the rows of (b, hq) and (b, g) live: query / output row i at
+  // q_base + i * q_stride (elements), key / value row j at byte
+  // j * kv_stride from kg / vg, LSE of row i at lse_base[i].
+  int Sq, L;
+  const uint16_t* q_base;
+  size_t o_base, q_stride, kv_stride;
+  float* lse_base = a.lse;
+  const char* kg;
+  const char* vg;
+  if constexpr (VARLEN) {
+    int qs, ks;
+    fwd_seq_range(a.cu_q, b, a.total_q, qs, Sq);
+    fwd_seq_range(a.cu_k, b, a.total_k, ks, L);
+    if (qt * S::BM >= Sq) return;  // past this sequence's queries (whole workgroup)
+    o_base = ((size_t)qs * a.Hq + hq) * D;
+    q_stride = (size_t)a.Hq * D;
+    kv_stride = (size_t)a.Hkv * ROW_BYTES;
+    if (lse_base) lse_base += (size_t)hq * a.total_q + qs;
+    const size_t kv_off = ((size_t)ks * a.Hkv + g) * D;
+    kg = reinterpret_cast<const char*>(a.k + kv_off);
+    vg = reinterpret_cast<const char*>(a.v + kv_off);
+  } else {
+    Sq = a.Sq;
+    L = a.kv_seqlens ? clamp_len(a.kv_seqlens[b], a.Skv) : a.Skv;
+    const size_t q_row0 = ((size_t)b * a.Hq + hq) * (size_t)a.Sq;
+    o_base = q_row0 * D;
+    q_stride = D;
+    kv_stride = ROW_BYTES;
+    if (lse_base) lse_base += q_row0;
+    const size_t kv_off = ((size_t)b * a.Hkv + g) * (size_t)a.Skv * D;
+    kg = reinterpret_cast<const char*>(a.k + kv_off);
+    vg = reinterpret_cast<const char*>(a.v + kv_off);
+  }
+  q_base = a.q + o_base;
+  const int off = L - Sq;  // bottom-right causal alignment
   const int q0 = qt * S::BM;
-  const int q_end = min(q0 + S::BM, a.Sq);
+  const int q_end = min(q0 + S::BM, Sq);
   int n_keys = L;
   if (CAUSAL) n_keys = min(L, q_end + off);
   if (n_keys < 0) n_keys = 0;
   const int n_kt = (n_keys + BN - 1) / BN;
   const int n_full = L / BN;  // tiles that lie wholly inside the sequence
   const float c = a.scale_log2;
-
-  const size_t q_row0 = ((size_t)b * a.Hq + hq) * (size_t)a.Sq;
-  const size_t kv_off = ((size_t)b * a.Hkv + g) * (size_t)a.Skv * D;
-  const char* __restrict__ kg = reinterpret_cast<const char*>(a.k + kv_off);
-  const char* __restrict__ vg = reinterpret_cast<const char*>(a.v + kv_off);
 
   // Q^T fragments: lane (column n, k-group h) holds q[row][16 s + 8 h .. +7].
   // Loaded before any K/V traffic so waiting for them waits for nothing else.
@@ -142,8 +187,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
 #pragma unroll
     for (int s = 0; s < S::KSTEPS; ++s) {
       u32x4 u = {0u, 0u, 0u, 0u};
-      if (row < a.Sq)
-        u = *reinterpret_cast<const u32x4*>(a.q + (q_row0 + row) * D + s * 16 + h * 8);
+      if (row < Sq)
+        u = *reinterpret_cast<const u32x4*>(q_base + row * q_stride + s * 16 + h * 8);
       qf[qb][s] = as_bf16x8(u);
     }
   }
@@ -168,7 +213,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   uint32_t full_off[S::BLOCKS_PER_WAVE];
 #pragma unroll
   for (int p = 0; p < S::BLOCKS_PER_WAVE; ++p)
-    full_off[p] = (uint32_t)((dma_row + p * ROW_STEP) * ROW_BYTES + dma_ch);
+    full_off[p] = (uint32_t)((dma_row + p * ROW_STEP) * kv_stride + dma_ch);
   auto issue_rows = [&](const char* g, uint32_t lds_w, int kt, auto buf_tag, auto p_tag,
                         auto full_tag) {
     constexpr int BUF = decltype(buf_tag)::value;
@@ -178,11 +223,11 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
       goff = full_off[P];
     } else {
       const int lim = L - 1 - kt * BN;  // last valid row of the tile
-      goff = (uint32_t)(min(dma_row, lim - P * ROW_STEP) * ROW_BYTES + dma_ch) +
-             P * ROW_STEP * ROW_BYTES;
+      goff = (uint32_t)(min(dma_row, lim - P * ROW_STEP) * kv_stride + dma_ch) +
+             (uint32_t)(P * ROW_STEP * kv_stride);
     }
     constexpr uint32_t lds_off = BUF * TILE_BYTES + P * S::WAVES * 1024;
-    load_lds16_at(g + (size_t)kt * BN * ROW_BYTES + goff, lds_w + lds_off);
+    load_lds16_at(g + (size_t)kt * BN * kv_stride + goff, lds_w + lds_off);
   };
 
   float m_run[QB], l_run[QB];
@@ -230,9 +275,9 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   // Tiles [0, n_free) need no mask for any row of this wave; tiles up to
   // n_live hold at least one admissible key for some row of the wave.
   const int w_first = qw0;                      // first query row of the wave
-  const int w_last = min(qw0 + 32 * QB, a.Sq) - 1;
+  const int w_last = min(qw0 + 32 * QB, Sq) - 1;
   int n_free = (CAUSAL ? min(L, w_first + off + 1) : L) / BN;
-  int n_live = qw0 < a.Sq ? (CAUSAL ? min(L, w_last + off + 1) : L) : 0;
+  int n_live = qw0 < Sq ? (CAUSAL ? min(L, w_last + off + 1) : L) : 0;
   n_live = (max(n_live, 0) + BN - 1) / BN;
   n_free = max(0, min(n_free, n_live));
 
@@ -492,9 +537,9 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   for (int qb = 0; qb < QB; ++qb) {
     const int qrow = qw0 + qb * 32 + n;
     const float lsum = sum_xor32(l_run[qb]);
-    if (qrow >= a.Sq) continue;
+    if (qrow >= Sq) continue;
     const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
-    const size_t obase = (q_row0 + qrow) * D;
+    const size_t obase = o_base + qrow * q_stride;
 #pragma unroll
     for (int db = 0; db < S::DBLK; ++db)
 #pragma unroll
@@ -513,8 +558,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
           *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(a.o) + obase + d) = w;
         }
       }
-    if (h == 0 && a.lse)
-      a.lse[q_row0 + qrow] = lsum > 0.f ? (m_run[qb] + log2f(lsum)) * kLn2 : kNegInf;
+    if (h == 0 && lse_base)
+      lse_base[qrow] = lsum > 0.f ? (m_run[qb] + log2f(lsum)) * kLn2 : kNegInf;
   }
 }
 

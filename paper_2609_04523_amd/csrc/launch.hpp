@@ -1,0 +1,28 @@
+// launch.hpp -- host launchers of the kernel families, each in translation
+// units of its own (fwd_launch_d128.hip, fwd_launch_d64.hip,
+// fwd_varlen_launch.hip, dec_launch.hip) so that the library compiles in
+// parallel.  Arguments are validated by the callers in mk_attn.hip; these
+// only pick the instantiation and enqueue.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "decode_kernel.hpp"
+#include "fwd_kernel.hpp"
+
+namespace mk {
+
+constexpr int kFwdQB = 1;  // 32-query blocks per wave in the forward kernel
+
+// Dense [B, H, S, D] forward: nblocks workgroups of the forward kernel.
+hipError_t launch_fwd(const FwdArgs& a, unsigned nblocks, int D, bool causal, bool out_f32,
+                      bool pos_scale, hipStream_t st);
+
+// Packed ragged forward (bf16 O).
+hipError_t launch_fwd_varlen(const FwdArgs& a, unsigned nblocks, int D, bool causal,
+                             bool pos_scale, hipStream_t st);
+
+// Decode: the part kernel (contiguous or paged cache) then the merge kernel.
+hipError_t launch_decode(const DecArgs& a, int D, int qblocks, bool paged, hipStream_t st);
+
+}  // namespace mk

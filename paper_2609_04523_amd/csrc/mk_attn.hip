@@ -7,13 +7,11 @@
 #include <stdint.h>
 
 #include "../../include/mk_attn.h"
-#include "decode_kernel.hpp"
-#include "fwd_kernel.hpp"
+#include "launch.hpp"
 
 namespace {
 
-constexpr int kVersion = 3;
-constexpr int kFwdQB = 1;             // 32-query blocks per wave in the forward kernel
+constexpr int kVersion = 4;
 constexpr int kComputeUnits = 256;    // MI355X
 constexpr int kLdsPerCu = 160 * 1024; // gfx950
 constexpr int kMaxParts = 1 << 20;    // decode parts per call
@@ -21,29 +19,6 @@ constexpr int kMaxParts = 1 << 20;    // decode parts per call
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
-
-template <int D, bool CAUSAL, bool OUT_F32, bool POS>
-hipError_t launch_fwd(const mk::FwdArgs& a, unsigned nblocks, hipStream_t st) {
-  hipLaunchKernelGGL((mk::fwd_kernel<D, CAUSAL, OUT_F32, kFwdQB, POS>), dim3(nblocks),
-                     dim3(mk::FwdShape<D, kFwdQB>::THREADS), 0, st, a);
-  return hipGetLastError();
-}
-
-template <int D, bool CAUSAL, bool OUT_F32>
-hipError_t launch_fwd_s(const mk::FwdArgs& a, unsigned nblocks, bool pos, hipStream_t st) {
-  return pos ? launch_fwd<D, CAUSAL, OUT_F32, true>(a, nblocks, st)
-             : launch_fwd<D, CAUSAL, OUT_F32, false>(a, nblocks, st);
-}
-
-template <int D>
-hipError_t launch_fwd_d(const mk::FwdArgs& a, unsigned nblocks, bool causal, bool out_f32,
-                        bool pos, hipStream_t st) {
-  if (causal)
-    return out_f32 ? launch_fwd_s<D, true, true>(a, nblocks, pos, st)
-                   : launch_fwd_s<D, true, false>(a, nblocks, pos, st);
-  return out_f32 ? launch_fwd_s<D, false, true>(a, nblocks, pos, st)
-                 : launch_fwd_s<D, false, false>(a, nblocks, pos, st);
-}
 
 int fwd_impl(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq,
              int Hkv, int Sq, int Skv, int D, int causal, float scale, const int* kv_seqlens,
@@ -58,7 +33,7 @@ int fwd_impl(const void* q, const void* k, const void* v, void* o, float* lse, i
     return MK_ERR_ALIGN;
   if (lse && !aligned(lse, 4)) return MK_ERR_ALIGN;
   if (kv_seqlens && !aligned(kv_seqlens, 4)) return MK_ERR_ALIGN;
-  const int BM = mk::FwdShape<128, kFwdQB>::BM;  // same for both head dims
+  const int BM = mk::FwdShape<128, mk::kFwdQB>::BM;  // same for both head dims
   const long long n_qtiles = (Sq + BM - 1) / BM;
   const long long nblocks = n_qtiles * B * Hq;
   if (nblocks > 0x7fffffffLL) return MK_ERR_SHAPE;
@@ -78,10 +53,11 @@ int fwd_impl(const void* q, const void* k, const void* v, void* o, float* lse, i
   a.n_qtiles = (int)n_qtiles;
   a.xcd_groups = ((B * Hkv) % 8 == 0) ? 1 : 0;
   a.scale_log2 = scale * mk::kLog2e;
+  a.cu_q = a.cu_k = nullptr;
+  a.total_q = a.total_k = 0;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool pos = scale > 0.f;
-  hipError_t e = (D == 128) ? launch_fwd_d<128>(a, (unsigned)nblocks, causal, out_f32, pos, st)
-                            : launch_fwd_d<64>(a, (unsigned)nblocks, causal, out_f32, pos, st);
+  const hipError_t e = mk::launch_fwd(a, (unsigned)nblocks, D, causal, out_f32, pos, st);
   return e == hipSuccess ? MK_OK : MK_ERR_HIP;
 }
 
@@ -120,32 +96,6 @@ bool dec_layout(int Hq, int Hkv, int D, int n_parts, DecLayout* out) {
   l.total = l.lse_off + round_up((size_t)l.parts * 2 * G * sizeof(float), 256);
   *out = l;
   return true;
-}
-
-template <int D, int QB, bool PAGED>
-void launch_dec(const mk::DecArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((mk::dec_part_kernel<D, QB, PAGED>), dim3(a.P), dim3(64), 0, st, a);
-}
-
-// Part kernel for the head dim and group size, then the merge kernel.
-template <bool PAGED>
-int launch_decode(const mk::DecArgs& a, int D, hipStream_t st) {
-  const int qb = dec_qblocks(D, a.Hq / a.Hkv);
-  if (D == 128) {
-    if (qb == 1) launch_dec<128, 1, PAGED>(a, st);
-    else if (qb == 2) launch_dec<128, 2, PAGED>(a, st);
-    else launch_dec<128, 4, PAGED>(a, st);
-  } else {
-    if (qb == 1) launch_dec<64, 1, PAGED>(a, st);
-    else launch_dec<64, 2, PAGED>(a, st);
-  }
-  if (hipGetLastError() != hipSuccess) return MK_ERR_HIP;
-  const unsigned mblocks = (unsigned)(((long long)a.B * a.Hq + 3) / 4);  // one wave per row
-  if (D == 128)
-    hipLaunchKernelGGL(mk::dec_merge_kernel<128>, dim3(mblocks), dim3(256), 0, st, a);
-  else
-    hipLaunchKernelGGL(mk::dec_merge_kernel<64>, dim3(mblocks), dim3(256), 0, st, a);
-  return hipGetLastError() == hipSuccess ? MK_OK : MK_ERR_HIP;
 }
 
 // Checks shared by both decode entry points (max_keys: keys a sequence can
@@ -218,6 +168,54 @@ int mk_attn_fwd_o32(const void* q, const void* k, const void* v, float* o, float
                   true);
 }
 
+int mk_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o, float* lse,
+                       const int* cu_seqlens_q, const int* cu_seqlens_k, int B, int Hq,
+                       int Hkv, int max_seqlen_q, int total_q, int total_k, int D, int causal,
+                       float scale, void* stream) {
+  if (!q || !k || !v || !o || !cu_seqlens_q || !cu_seqlens_k) return MK_ERR_NULL;
+  if (B < 1 || Hq < 1 || Hkv < 1 || max_seqlen_q < 1 || total_q < 1 || total_k < 1 || D < 1)
+    return MK_ERR_SHAPE;
+  if (Hq % Hkv != 0) return MK_ERR_SHAPE;
+  if (D != 64 && D != 128) return MK_ERR_UNSUPPORTED;
+  if (causal != 0 && causal != 1) return MK_ERR_ARG;
+  if (!isfinite(scale)) return MK_ERR_ARG;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16) ||
+      !aligned(cu_seqlens_q, 4) || !aligned(cu_seqlens_k, 4))
+    return MK_ERR_ALIGN;
+  if (lse && !aligned(lse, 4)) return MK_ERR_ALIGN;
+  const int BM = mk::FwdShape<128, mk::kFwdQB>::BM;
+  const long long n_qtiles = (max_seqlen_q + BM - 1) / BM;
+  const long long nblocks = n_qtiles * B * Hq;
+  // workgroups of one launch; a key tile's rows (64 tokens of Hkv heads)
+  // addressed with 32-bit offsets; B + 1 offsets per table
+  if (nblocks > 0x7fffffffLL || (long long)Hkv * D * 2 * 64 > 0xffffffffLL || B > 0x7ffffffe)
+    return MK_ERR_SHAPE;
+
+  mk::FwdArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.o = o;
+  a.lse = lse;
+  a.kv_seqlens = nullptr;
+  a.B = B;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.Sq = max_seqlen_q;
+  a.Skv = 0;
+  a.n_qtiles = (int)n_qtiles;
+  a.xcd_groups = 0;
+  a.scale_log2 = scale * mk::kLog2e;
+  a.cu_q = cu_seqlens_q;
+  a.cu_k = cu_seqlens_k;
+  a.total_q = total_q;
+  a.total_k = total_k;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const bool pos = scale > 0.f;
+  const hipError_t e = mk::launch_fwd_varlen(a, (unsigned)nblocks, D, causal, pos, st);
+  return e == hipSuccess ? MK_OK : MK_ERR_HIP;
+}
+
 size_t mk_attn_decode_workspace_bytes(int Hq, int Hkv, int D, int n_parts) {
   DecLayout l;
   if (!dec_layout(Hq, Hkv, D, n_parts, &l)) return 0;
@@ -239,7 +237,9 @@ int mk_attn_decode(const void* q, const void* k_cache, const void* v_cache, void
   if (rc != MK_OK) return rc;
   const mk::DecArgs a =
       dec_args(q, k_cache, v_cache, o, lse, B, Hq, Hkv, Smax, scale, kv_seqlens, l, workspace);
-  return launch_decode<false>(a, D, static_cast<hipStream_t>(stream));
+  const hipError_t e = mk::launch_decode(a, D, dec_qblocks(D, Hq / Hkv), false,
+                                         static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MK_OK : MK_ERR_HIP;
 }
 
 int mk_attn_decode_paged(const void* q, const void* k_pages, const void* v_pages,
@@ -263,7 +263,9 @@ int mk_attn_decode_paged(const void* q, const void* k_pages, const void* v_pages
   a.page_size = page_size;
   a.max_pages = max_pages;
   a.n_pages = n_pages;
-  return launch_decode<true>(a, D, static_cast<hipStream_t>(stream));
+  const hipError_t e = mk::launch_decode(a, D, dec_qblocks(D, Hq / Hkv), true,
+                                         static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MK_OK : MK_ERR_HIP;
 }
 
 const char* mk_status_str(int status) {

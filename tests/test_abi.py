@@ -43,7 +43,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert mk.mk_attn_version() == 3
+    assert mk.mk_attn_version() == 4
     names = ["MK_OK", "MK_ERR_NULL", "MK_ERR_SHAPE", "MK_ERR_UNSUPPORTED", "MK_ERR_ALIGN",
              "MK_ERR_WORKSPACE", "MK_ERR_HIP", "MK_ERR_ARG"]
     for code, name in enumerate(names):
@@ -81,6 +81,29 @@ def test_fwd_validation(lib, o32):
         assert r(scale=s) == 7
     # too many workgroups for one launch
     assert r(B=65536, Hq=65536, Hkv=1, Sq=1) == 2
+
+
+def varlen_rc(lib, *, q=P, k=P, v=P, o=P, lse=None, cq=P, ck=P, B=3, Hq=8, Hkv=2, max_sq=100,
+              total_q=300, total_k=400, D=128, causal=1, scale=0.125):
+    return lib.mk_attn_fwd_varlen(q, k, v, o, lse, cq, ck, B, Hq, Hkv, max_sq, total_q, total_k,
+                                  D, causal, scale, None)
+
+
+def test_fwd_varlen_validation(lib):
+    for name in ("q", "k", "v", "o", "cq", "ck"):
+        assert varlen_rc(lib, **{name: None}) == 1
+    for name in ("B", "Hq", "Hkv", "max_sq", "total_q", "total_k"):
+        assert varlen_rc(lib, **{name: 0}) == 2
+    assert varlen_rc(lib, Hq=6, Hkv=4) == 2
+    assert varlen_rc(lib, B=1 << 16, Hq=64, Hkv=64, max_sq=1 << 20) == 2  # too many workgroups
+    assert varlen_rc(lib, D=96) == 3
+    assert varlen_rc(lib, causal=3) == 7
+    assert varlen_rc(lib, scale=math.nan) == 7
+    for name in ("q", "k", "v", "o"):
+        assert varlen_rc(lib, **{name: P_ODD}) == 4
+    assert varlen_rc(lib, cq=P + 2) == 4
+    assert varlen_rc(lib, ck=P + 1) == 4
+    assert varlen_rc(lib, lse=P + 2) == 4
 
 
 def dec_rc(lib, *, q=P, kc=P, vc=P, o=P, lse=None, B=2, Hq=8, Hkv=2, Smax=512, D=128,

@@ -1,0 +1,113 @@
+"""Forward over packed variable-length sequences on the GPU
+(paper_2609_04523_amd.mk_attn_fwd_varlen, through the C ABI) against the
+fp64 oracle's packed forward, and against the dense kernel run on each
+sequence alone."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_04523_amd as mk
+import workloads
+from oracle import oracle as orc
+from parity import assert_parity
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+NAN_BITS = 0x7FC0
+
+
+def packed(seqs, Hq, Hkv, D, seed, k_mult=1.0):
+    """Seeded packed inputs for sequences [(Sq_b, Skv_b), ...]."""
+    cq = np.concatenate([[0], np.cumsum([a for a, _ in seqs])]).astype(np.int32)
+    ck = np.concatenate([[0], np.cumsum([b for _, b in seqs])]).astype(np.int32)
+    g = torch.Generator().manual_seed(seed)
+    q = torch.randn((int(cq[-1]), Hq, D), generator=g).to(torch.bfloat16)
+    k = (torch.randn((max(int(ck[-1]), 1), Hkv, D), generator=g) * k_mult).to(torch.bfloat16)
+    v = torch.randn((max(int(ck[-1]), 1), Hkv, D), generator=g).to(torch.bfloat16)
+    return q, k, v, cq, ck
+
+
+def run_varlen(q, k, v, cq, ck, *, causal, scale, max_sq=None):
+    max_sq = max_sq or int(np.max(np.diff(cq)))
+    o, lse = mk.fwd_varlen(q.to(DEV), k.to(DEV), v.to(DEV), torch.from_numpy(cq).to(DEV),
+                           torch.from_numpy(ck).to(DEV), max(max_sq, 1), causal=causal,
+                           scale=scale)
+    torch.cuda.synchronize()
+    return o, lse
+
+
+def check_against_oracle(name, seqs, Hq, Hkv, D, causal, seed, k_mult=1.0):
+    q, k, v, cq, ck = packed(seqs, Hq, Hkv, D, seed, k_mult)
+    scale = D ** -0.5
+    o, lse = run_varlen(q, k, v, cq, ck, causal=causal, scale=scale)
+    o_ref, lse_ref = orc.attn_fwd_varlen(workloads.bits(q), workloads.bits(k), workloads.bits(v),
+                                         cq, ck, causal=causal, scale=scale)
+    # compare in the [1, Hq, total_q] / [1, Hq, total_q, D] shape the checker takes
+    assert_parity(name, o.permute(1, 0, 2)[None], lse[None],
+                  o_ref.transpose(1, 0, 2)[None], lse_ref[None])
+
+
+# name, Hq, Hkv, D, sequences [(Sq, Skv)]
+CASES = [
+    ("mixed_prefill_decode", 8, 2, 128, [(1, 700), (300, 300), (1, 65), (129, 900), (1, 1)]),
+    ("chunks_and_short", 4, 4, 128, [(64, 64), (200, 450), (3, 3), (130, 130)]),
+    ("more_queries_than_keys", 8, 2, 128, [(150, 40), (70, 200)]),
+    ("empty_sequences", 4, 1, 64, [(0, 10), (90, 90), (20, 0), (0, 0), (33, 100)]),
+    ("gqa16_d64", 16, 1, 64, [(257, 257), (1, 513)]),
+]
+
+
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_varlen_against_oracle(case, causal):
+    name, Hq, Hkv, D, seqs = case
+    check_against_oracle(f"{name} causal={causal}", seqs, Hq, Hkv, D, causal, seed=len(name))
+
+
+def test_varlen_sharp_softmax():
+    check_against_oracle("k x2", [(256, 512), (500, 500)], 8, 2, 128, True, seed=3, k_mult=2.0)
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_varlen_equals_dense_per_sequence_bitwise(causal):
+    # the same tiles in the same order: each sequence of the packed batch
+    # must give the dense kernel's bits for that sequence alone
+    seqs = [(2048, 2048), (1, 3000), (700, 1800), (1500, 1500), (64, 64), (5, 4000)]
+    Hq, Hkv, D = 32, 8, 128
+    q, k, v, cq, ck = packed(seqs, Hq, Hkv, D, seed=11)
+    o, lse = run_varlen(q, k, v, cq, ck, causal=causal, scale=D ** -0.5)
+    for b, (Sq, Skv) in enumerate(seqs):
+        qb = q[cq[b]:cq[b + 1]].permute(1, 0, 2)[None].contiguous().to(DEV)
+        kb = k[ck[b]:ck[b + 1]].permute(1, 0, 2)[None].contiguous().to(DEV)
+        vb = v[ck[b]:ck[b + 1]].permute(1, 0, 2)[None].contiguous().to(DEV)
+        od, ld = mk.fwd(qb, kb, vb, causal=causal, scale=D ** -0.5)
+        torch.cuda.synchronize()
+        assert torch.equal(o[cq[b]:cq[b + 1]].permute(1, 0, 2), od[0]), f"sequence {b} O"
+        assert torch.equal(lse[:, cq[b]:cq[b + 1]], ld[0]), f"sequence {b} LSE"
+
+
+def test_varlen_unowned_rows_untouched_and_offsets_clamped():
+    Hq, Hkv, D = 8, 2, 128
+    q, k, v, cq, ck = packed([(100, 100), (50, 80)], Hq, Hkv, D, seed=21)
+    total_q = q.shape[0] + 40  # 40 trailing rows no sequence owns
+    qx = torch.cat([q, torch.randn((40, Hq, D)).to(torch.bfloat16)])
+    cq_dev = torch.tensor([0, 100, 150], dtype=torch.int32, device=DEV)
+    ck_bad = torch.tensor([0, 100, 10 ** 6], dtype=torch.int32, device=DEV)  # clamps to total_k
+    o = torch.empty((total_q, Hq, D), device=DEV, dtype=torch.bfloat16)
+    o.view(torch.int16).fill_(NAN_BITS)
+    lse = torch.full((Hq, total_q), float("nan"), device=DEV)
+    mk.mk_attn_fwd_varlen(qx.to(DEV), k.to(DEV), v.to(DEV), o, lse, cq_dev, ck_bad, 2, Hq, Hkv,
+                          100, total_q, k.shape[0], D, 1, D ** -0.5)
+    torch.cuda.synchronize()
+    assert torch.all(o[150:].view(torch.int16) == NAN_BITS), "unowned rows written"
+    assert torch.all(torch.isnan(lse[:, 150:]))
+    o_ref, lse_ref = run_varlen(q, k, v, cq, ck, causal=True, scale=D ** -0.5)
+    assert torch.equal(o[:150], o_ref[:150]) and torch.equal(lse[:, :150], lse_ref[:, :150])
+
+
+def test_varlen_deterministic_bitwise():
+    q, k, v, cq, ck = packed([(1000, 3000), (1, 2000), (777, 777)], 32, 8, 128, seed=31)
+    a = run_varlen(q, k, v, cq, ck, causal=True, scale=128 ** -0.5)
+    b = run_varlen(q, k, v, cq, ck, causal=True, scale=128 ** -0.5)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
