@@ -163,6 +163,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--page-size", type=int, default=16,
                     help="page size of the paged-decode leg (0 skips the leg)")
+    ap.add_argument("--no-varlen", action="store_true",
+                    help="skip the packed ragged prefill leg")
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="query rows per head timed for the CPU oracle baseline (0: all)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -225,6 +227,17 @@ def main():
     del q, k, v
     qd, kc, vc, lens = workloads.config_inputs(dcfg)
     caches = [(kc.to(dev), vc.to(dev)), (kc.to(dev).clone(), vc.to(dev).clone())]
+    # packed ragged prefill batch: 16 causal sequences, lengths U{256..8192}
+    VL = dict(B=16, Hq=32, Hkv=8, D=128, lmin=256, lmax=8192, seed=1006)
+    varlen = []
+    if not args.no_varlen:
+        vq, vk, vv, vcu = workloads.varlen_inputs(**VL)
+        vlens = (vcu[1:] - vcu[:-1]).tolist()
+        varlen = [(vq.to(dev), vk.to(dev), vv.to(dev), vcu.to(dev),
+                   torch.empty(vq.shape, device=dev, dtype=torch.bfloat16),
+                   torch.empty((VL["Hq"], vq.shape[0]), device=dev, dtype=torch.float32))
+                  for _ in range(2)]
+        del vq, vk, vv
     paged = []
     if args.page_size:
         # the same keys scattered over pages in a seeded random order (two
@@ -256,6 +269,12 @@ def main():
         kcc, vcc = caches[i & 1]
         mk.mk_attn_decode(qd, kcc, vcc, od, lsed, B, Hq, Hkv, Smax, D, dcfg.scale, lens_d,
                           args.parts, ws, ws_bytes, stream)
+
+    def prefill_varlen(i):
+        vq_, vk_, vv_, vcu_, vo_, vl_ = varlen[i & 1]
+        mk.mk_attn_fwd_varlen(vq_, vk_, vv_, vo_, vl_, vcu_, vcu_, VL["B"], VL["Hq"], VL["Hkv"],
+                              max(vlens), vq_.shape[0], vk_.shape[0], VL["D"], 1,
+                              VL["D"] ** -0.5, stream)
 
     def decode_paged(i):
         kp_, vp_, bt_ = paged[i & 1]
@@ -298,6 +317,19 @@ def main():
     ev[2].record(stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    varlen_ms = None
+    if varlen:
+        # the packed ragged prefill leg, timed after the step the same way
+        for i in range(args.warmup):
+            prefill_varlen(i)
+        evv = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        evv[0].record(stream)
+        for i in range(K):
+            prefill_varlen(i)
+        evv[1].record(stream)
+        torch.cuda.synchronize()
+        varlen_ms = evv[0].elapsed_time(evv[1]) / K
     paged_ms = None
     if paged:
         # the paged-decode leg, timed after the step the same way
@@ -321,6 +353,7 @@ def main():
     dec_gbs = dec_bytes / (dec_ms * 1e-3) / 1e9
     log(f"[bench] prefill {pre_ms * 1e3:.1f} us ({tflops:.1f} TFLOP/s), "
         f"decode {dec_ms * 1e3:.1f} us ({dec_gbs:.1f} GB/s), step {ms_step:.3f} ms"
+        + (f", varlen prefill {varlen_ms * 1e3:.1f} us" if varlen_ms is not None else "")
         + (f", paged decode {paged_ms * 1e3:.1f} us" if paged_ms is not None else ""))
 
     digest = kernel_source_digest()
@@ -375,6 +408,22 @@ def main():
         },
         "cpu_baseline": None,
     }
+    if varlen_ms is not None:
+        # causal pairs counted exactly: S (S + 1) / 2 per sequence and head
+        v_flops = 4 * VL["D"] * VL["Hq"] * sum(L * (L + 1) // 2 for L in vlens)
+        v_tf = v_flops / (varlen_ms * 1e-3) / 1e12
+        result["varlen_prefill"] = {
+            "workload": (f"packed ragged causal prefill: B={VL['B']} sequences, lengths "
+                         f"U[{VL['lmin']},{VL['lmax']}] (total {sum(vlens)} tokens), "
+                         f"Hq={VL['Hq']} Hkv={VL['Hkv']} D={VL['D']}"),
+            "value": round(v_tf, 2),
+            "unit": "TFLOP/s",
+            "us": round(varlen_ms * 1e3, 2),
+            "flops": v_flops,
+            "roofline": {"bound": "mfma", "achieved": round(v_tf, 2), "peak": PEAK_BF16_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(v_tf / PEAK_BF16_TFLOPS, 4),
+                         "traffic": None},
+        }
     if paged_ms is not None:
         p_gbs = dec_bytes / (paged_ms * 1e-3) / 1e9
         result["paged_decode"] = {

@@ -117,6 +117,21 @@ def decode_inputs(B: int, Hq: int, Hkv: int, Smax: int, D: int, seed: int,
     return q.to(torch.bfloat16), kc.to(torch.bfloat16), vc.to(torch.bfloat16), lens
 
 
+def varlen_inputs(B: int, Hq: int, Hkv: int, D: int, lmin: int, lmax: int, seed: int):
+    """Packed ragged prefill batch: lengths U{lmin..lmax} (queries = keys per
+    sequence), then q [total,Hq,D], k/v [total,Hkv,D] bf16 N(0,1), and
+    cu_seqlens int32 [B+1]."""
+    g = _gen(seed)
+    lens = torch.randint(lmin, lmax + 1, (B,), generator=g, dtype=torch.int64)
+    cu = torch.zeros(B + 1, dtype=torch.int32)
+    cu[1:] = torch.cumsum(lens, 0).to(torch.int32)
+    T = int(cu[-1])
+    q = torch.randn((T, Hq, D), generator=g, dtype=torch.float32).to(torch.bfloat16)
+    k = torch.randn((T, Hkv, D), generator=g, dtype=torch.float32).to(torch.bfloat16)
+    v = torch.randn((T, Hkv, D), generator=g, dtype=torch.float32).to(torch.bfloat16)
+    return q, k, v, cu
+
+
 NAN_BF16_BITS = 0x7FC0
 
 
