@@ -40,6 +40,13 @@ def attention(q, k, v, *, causal: bool, scale: float, kv_seqlens=None):
 
     Returns (o [B][Hq][Sq][D], lse [B][Hq][Sq]) as Python floats.
     """
+    dec = lambda t: [[[[bf16_bits_to_float(x) for x in row] for row in h] for h in bb] for bb in t]
+    return attention_f(dec(q), dec(k), dec(v), causal=causal, scale=scale,
+                       kv_seqlens=kv_seqlens)
+
+
+def attention_f(q, k, v, *, causal: bool, scale: float, kv_seqlens=None):
+    """The same on nested lists of Python floats (for finite differences)."""
     B, Hq, Sq, D = len(q), len(q[0]), len(q[0][0]), len(q[0][0][0])
     Hkv, Skv = len(k[0]), len(k[0][0])
     G = Hq // Hkv
@@ -50,10 +57,10 @@ def attention(q, k, v, *, causal: bool, scale: float, kv_seqlens=None):
         allowed = _mask(Sq, Skv, L, causal)
         for hq in range(Hq):
             kh = hq // G
-            Kf = [[bf16_bits_to_float(x) for x in row] for row in k[b][kh]]
-            Vf = [[bf16_bits_to_float(x) for x in row] for row in v[b][kh]]
+            Kf = k[b][kh]
+            Vf = v[b][kh]
             for i in range(Sq):
-                qi = [bf16_bits_to_float(x) for x in q[b][hq][i]]
+                qi = q[b][hq][i]
                 scores = []
                 for j in range(Skv):
                     if allowed[i][j]:

@@ -69,6 +69,9 @@ def _declare(lib):
     lib.oracle_attn_fwd_varlen.argtypes = [_u16p, _u16p, _u16p, _i32p, _i32p, i, i, i, i, i, i,
                                            i, d, _f64p, _f64p]
     lib.oracle_attn_fwd_varlen.restype = i
+    lib.oracle_attn_bwd.argtypes = [_u16p, _u16p, _u16p, _u16p, i, i, i, i, i, i, i, d, _i32p,
+                                    _f64p, _f64p, _f64p]
+    lib.oracle_attn_bwd.restype = i
     lib.oracle_version.restype = i
     return lib
 
@@ -165,6 +168,28 @@ def decode(q, k_cache, v_cache, kv_seqlens, *, scale: float,
     if rc != 0:
         raise ValueError(f"oracle_decode failed ({rc})")
     return o, lse
+
+
+def attn_bwd(q, k, v, dout, *, causal: bool, scale: float, kv_seqlens=None, lib=None):
+    """Gradients of L = <dout, O> for q [B,Hq,Sq,D], k/v [B,Hkv,Skv,D] (bf16 bits)
+    -> (dq, dk, dv) float64, same shapes."""
+    lib = lib or load()
+    q, k, v, do = _u16(q), _u16(k), _u16(v), _u16(dout)
+    B, Hq, Sq, D = q.shape
+    _, Hkv, Skv, _ = k.shape
+    if do.shape != q.shape:
+        raise ValueError("dout must have q's shape")
+    sl = None if kv_seqlens is None else _seqlens(kv_seqlens, B)
+    dq = np.empty(q.shape, np.float64)
+    dk = np.empty(k.shape, np.float64)
+    dv = np.empty(v.shape, np.float64)
+    rc = lib.oracle_attn_bwd(_ptr(q, _u16p), _ptr(k, _u16p), _ptr(v, _u16p), _ptr(do, _u16p),
+                             B, Hq, Hkv, Sq, Skv, D, int(bool(causal)), float(scale),
+                             None if sl is None else _ptr(sl, _i32p), _ptr(dq, _f64p),
+                             _ptr(dk, _f64p), _ptr(dv, _f64p))
+    if rc != 0:
+        raise ValueError(f"oracle_attn_bwd failed ({rc})")
+    return dq, dk, dv
 
 
 def attn_fwd_varlen(q, k, v, cu_seqlens_q, cu_seqlens_k, *, causal: bool, scale: float,

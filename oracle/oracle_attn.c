@@ -2,8 +2,9 @@
  * oracle_attn.c -- plain fp64 CPU oracle for causal grouped-query
  * scaled-dot-product attention (forward), its split-KV decode form,
  * decode over a paged cache (the "Paged Attention" workload of Table 2),
- * and the forward over packed variable-length sequences (the ragged
- * batches of the "Ragged Paged Attention" workload of Table 2).
+ * the forward over packed variable-length sequences (the ragged batches of
+ * the "Ragged Paged Attention" workload of Table 2), and the backward
+ * (gradients of the output with respect to q, k and v).
  *
  * TEST INFRASTRUCTURE ONLY.  This file is the checker the GPU path is
  * measured against; it is loaded by the test suite, by the smoke check and
@@ -42,7 +43,8 @@
  * repeated K/V heads, decode equals the last prefill row, split-combine
  * equals unsplit, paged decode equals decode on the cache gathered through
  * the block table, a packed ragged batch equals each of its sequences run
- * alone) and hand-derived values stored under tests/golden/.
+ * alone, the backward equals central finite differences of an independent
+ * forward) and hand-derived values stored under tests/golden/.
  *
  * Build: plain C11, no -ffast-math, libm only (gcc -O2 -shared -fPIC).
  */
@@ -548,4 +550,90 @@ int oracle_attn_fwd_varlen(const uint16_t *q, const uint16_t *k, const uint16_t 
     return 0;
 }
 
-int oracle_version(void) { return 3; }
+/* ------------------------------------------------------------------ */
+/* Backward: gradients of the output with respect to q, k, v            */
+/* ------------------------------------------------------------------ */
+
+/*
+ * Given do = dL/dO for the forward of oracle_attn_fwd (same layouts and
+ * masks; the LSE output is taken as not differentiated), the gradients of
+ * L with respect to q, k and v, from the derivative of softmax: with
+ * P_ij = softmax_j(s_i) over the valid keys,
+ *   dV_j  = sum_i P_ij dO_i               (summed over the query heads of
+ *   dP_ij = dO_i . v_j                      the kv head for dK and dV)
+ *   D_i   = sum_j P_ij dP_ij
+ *   dS_ij = P_ij (dP_ij - D_i)
+ *   dQ_i  = scale * sum_j dS_ij k_j
+ *   dK_j  = scale * sum_i dS_ij q_i
+ * Rows without valid keys contribute nothing; keys no row sees get zero.
+ * dq [B,Hq,Sq,D], dk, dv [B,Hkv,Skv,D], all double.
+ */
+int oracle_attn_bwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                    const uint16_t *dout, int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                    int causal, double scale, const int32_t *kv_seqlens, double *dq,
+                    double *dk, double *dv)
+{
+    if (!q || !k || !v || !dout || !dq || !dk || !dv) return -1;
+    if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || Sq < 1 || Skv < 1 || D < 1 ||
+        (causal != 0 && causal != 1))
+        return -2;
+    const int G = Hq / Hkv;
+    double *p = malloc(sizeof(double) * (size_t)Skv);
+    double *dp = malloc(sizeof(double) * (size_t)Skv);
+    if (!p || !dp) { free(p); free(dp); return -3; }
+    memset(dq, 0, sizeof(double) * (size_t)B * Hq * Sq * D);
+    memset(dk, 0, sizeof(double) * (size_t)B * Hkv * Skv * D);
+    memset(dv, 0, sizeof(double) * (size_t)B * Hkv * Skv * D);
+    for (int b = 0; b < B; ++b) {
+        const int L = clamp_len(kv_seqlens ? kv_seqlens[b] : Skv, Skv);
+        for (int hq = 0; hq < Hq; ++hq) {
+            const int g = hq / G;
+            const size_t kv0 = ((size_t)b * Hkv + g) * (size_t)Skv * D;
+            for (int i = 0; i < Sq; ++i) {
+                int n = L;
+                if (causal && i + L - Sq + 1 < n) n = i + L - Sq + 1;
+                if (n <= 0) continue;
+                const size_t qi = (((size_t)b * Hq + hq) * Sq + i) * D;
+                /* probabilities of row i */
+                double m = -INFINITY;
+                for (int j = 0; j < n; ++j) {
+                    double dot = 0.0;
+                    for (int d = 0; d < D; ++d)
+                        dot += bf16_bits_to_double(q[qi + d]) *
+                               bf16_bits_to_double(k[kv0 + (size_t)j * D + d]);
+                    p[j] = scale * dot;
+                    if (p[j] > m) m = p[j];
+                }
+                double z = 0.0;
+                for (int j = 0; j < n; ++j) {
+                    p[j] = exp(p[j] - m);
+                    z += p[j];
+                }
+                for (int j = 0; j < n; ++j) p[j] /= z;
+                /* dP_ij, D_i */
+                double delta = 0.0;
+                for (int j = 0; j < n; ++j) {
+                    double dot = 0.0;
+                    for (int d = 0; d < D; ++d)
+                        dot += bf16_bits_to_double(dout[qi + d]) *
+                               bf16_bits_to_double(v[kv0 + (size_t)j * D + d]);
+                    dp[j] = dot;
+                    delta += p[j] * dot;
+                }
+                for (int j = 0; j < n; ++j) {
+                    const double ds = p[j] * (dp[j] - delta);
+                    for (int d = 0; d < D; ++d) {
+                        dv[kv0 + (size_t)j * D + d] += p[j] * bf16_bits_to_double(dout[qi + d]);
+                        dq[qi + d] += scale * ds * bf16_bits_to_double(k[kv0 + (size_t)j * D + d]);
+                        dk[kv0 + (size_t)j * D + d] += scale * ds * bf16_bits_to_double(q[qi + d]);
+                    }
+                }
+            }
+        }
+    }
+    free(p);
+    free(dp);
+    return 0;
+}
+
+int oracle_version(void) { return 4; }

@@ -27,7 +27,11 @@ The facts, none of which re-types the oracle's own formula:
     valid page and pages no sequence lists ignored;
   * a packed ragged batch equals each of its sequences run alone through
     the batched forward (bottom-right causal per sequence), rows no
-    sequence owns are not written, and out-of-range offsets clamp.
+    sequence owns are not written, and out-of-range offsets clamp;
+  * the backward equals central finite differences of <dO, O> computed
+    with the pure-Python forward in float64 (independent of the gradient
+    formulas), and grouped heads' dK/dV are the sums over the group of the
+    repeated-head gradients.
 """
 from __future__ import annotations
 
@@ -405,8 +409,61 @@ def pin_varlen_gaps_and_clamped_offsets(lib):
         "offsets not clamped"
 
 
+BWD_FD_CASES = [
+    # B, Hq, Hkv, Sq, Skv, D, causal, seqlens
+    (1, 2, 1, 4, 4, 3, True, None),
+    (1, 2, 2, 3, 5, 2, False, [4]),
+    (2, 2, 1, 3, 3, 2, True, [3, 1]),   # a short sequence: rows without keys
+    (1, 1, 1, 2, 4, 2, True, None),     # bottom-right causal, Sq < Skv
+]
+
+
+def pin_bwd_finite_differences(lib):
+    h = 1e-4
+    for n, (B, Hq, Hkv, Sq, Skv, D, causal, sl) in enumerate(BWD_FD_CASES):
+        q = _rand((B, Hq, Sq, D), 240 + n, -1.5, 1.5)
+        k = _rand((B, Hkv, Skv, D), 250 + n, -1.5, 1.5)
+        v = _rand((B, Hkv, Skv, D), 260 + n)
+        do = _rand((B, Hq, Sq, D), 270 + n)
+        scale = 0.8
+        dq, dk, dv = orc.attn_bwd(q, k, v, do, causal=causal, scale=scale, kv_seqlens=sl, lib=lib)
+        qf, kf, vf, dof = _f(q), _f(k), _f(v), _f(do)
+
+        def loss(qx, kx, vx):
+            o, _ = brute.attention_f(qx.tolist(), kx.tolist(), vx.tolist(), causal=causal,
+                                     scale=scale, kv_seqlens=sl)
+            return float(np.sum(np.array(o) * dof))
+
+        for name, x, got in (("dq", qf, dq), ("dk", kf, dk), ("dv", vf, dv)):
+            fd = np.zeros_like(x)
+            for idx in np.ndindex(x.shape):
+                xp, xm = x.copy(), x.copy()
+                xp[idx] += h
+                xm[idx] -= h
+                args_p = [xp if t is x else t for t in (qf, kf, vf)]
+                args_m = [xm if t is x else t for t in (qf, kf, vf)]
+                fd[idx] = (loss(*args_p) - loss(*args_m)) / (2 * h)
+            _close(got, fd, 1e-6, f"bwd case {n} {name} vs finite differences")
+
+
+def pin_bwd_gqa_sums_repeated_heads(lib):
+    B, Hq, Hkv, S, D = 1, 6, 2, 7, 4
+    G = Hq // Hkv
+    q = _rand((B, Hq, S, D), 281)
+    k = _rand((B, Hkv, S, D), 282)
+    v = _rand((B, Hkv, S, D), 283)
+    do = _rand((B, Hq, S, D), 284)
+    dq, dk, dv = orc.attn_bwd(q, k, v, do, causal=True, scale=0.5, lib=lib)
+    dq2, dk2, dv2 = orc.attn_bwd(q, np.repeat(k, G, axis=1), np.repeat(v, G, axis=1), do,
+                                 causal=True, scale=0.5, lib=lib)
+    _close(dq, dq2, 1e-14, "GQA dq")
+    _close(dk, dk2.reshape(B, Hkv, G, S, D).sum(axis=2), 1e-13, "GQA dk = group sum")
+    _close(dv, dv2.reshape(B, Hkv, G, S, D).sum(axis=2), 1e-13, "GQA dv = group sum")
+
+
 ALL_PINS = [pin_golden, pin_brute_force, pin_rows_sum_to_one, pin_equal_value_rows,
             pin_causal_row0, pin_single_key, pin_scale_zero, pin_gqa_equals_repeated_mha,
             pin_decode_equals_last_prefill_row, pin_split_combine, pin_row_subset,
             pin_paged_equals_gathered, pin_paged_table_clamp_and_unused_pages,
-            pin_varlen_equals_each_sequence, pin_varlen_gaps_and_clamped_offsets]
+            pin_varlen_equals_each_sequence, pin_varlen_gaps_and_clamped_offsets,
+            pin_bwd_finite_differences, pin_bwd_gqa_sums_repeated_heads]

@@ -45,6 +45,14 @@ MUTANTS = {
                                "if (causal && i + 1 < n_valid) n_valid = i + 1;", 1),
     "varlen_lse_token_major": ("lse_row = lse + (size_t)hq * total_q + (q0 + i);",
                                "lse_row = lse + (size_t)(q0 + i) * Hq + hq;", 1),
+    "bwd_delta_dropped": ("const double ds = p[j] * (dp[j] - delta);",
+                          "const double ds = p[j] * (dp[j]);", 1),
+    "bwd_dk_without_scale": ("dk[kv0 + (size_t)j * D + d] += scale * ds *",
+                             "dk[kv0 + (size_t)j * D + d] += ds *", 1),
+    "bwd_dv_from_ds": ("dv[kv0 + (size_t)j * D + d] += p[j] *",
+                       "dv[kv0 + (size_t)j * D + d] += ds *", 1),
+    "bwd_dq_from_values": ("dq[qi + d] += scale * ds * bf16_bits_to_double(k[kv0",
+                           "dq[qi + d] += scale * ds * bf16_bits_to_double(v[kv0", 1),
     "varlen_key_start_ignored": ("const uint16_t *k_row = k + ((size_t)(k0 + j) * Hkv + g) * D;",
                                  "const uint16_t *k_row = k + ((size_t)(j) * Hkv + g) * D;", 1),
 }
