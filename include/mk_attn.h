@@ -48,7 +48,7 @@ typedef enum {
     MK_ERR_SHAPE = 2,       /* a size is < 1, Hq % Hkv != 0, or too large */
     MK_ERR_UNSUPPORTED = 3, /* head dim / group size this library does not build */
     MK_ERR_ALIGN = 4,       /* a pointer is not aligned as required */
-    MK_ERR_WORKSPACE = 5,   /* decode workspace missing or too small */
+    MK_ERR_WORKSPACE = 5,   /* workspace missing or too small */
     MK_ERR_HIP = 6,         /* the HIP runtime refused a launch */
     MK_ERR_ARG = 7          /* non-finite scale, bad causal flag or part count */
 } mk_status;
@@ -188,6 +188,40 @@ size_t mk_attn_decode_workspace_bytes(int Hq, int Hkv, int D, int n_parts);
  * invalid sizes.
  */
 int mk_attn_decode_default_parts(int Hq, int Hkv, int D);
+
+/*
+ * Attention backward: gradients of a scalar loss L with respect to q, k
+ * and v, given dout = dL/dO of the forward above (same q, k, v, masks,
+ * scale and kv_seqlens).  The LSE output is taken as not differentiated.
+ * From the derivative of softmax (the standard identity the paper's
+ * "Flash Attention" workload family relies on, Table 2), with
+ * P_ij = exp(scale s_ij - LSE_i) over the valid keys:
+ *   dV_j = sum_i P_ij dO_i,   dP_ij = dO_i . v_j,   D_i = dO_i . O_i,
+ *   dS_ij = P_ij (dP_ij - D_i),
+ *   dQ_i = scale sum_j dS_ij k_j,   dK_j = scale sum_i dS_ij q_i,
+ * dK and dV summed over the Hq / Hkv query heads of each kv head.
+ *   q, o, dout   [B, Hq,  Sq,  D] bf16; o is the forward's output
+ *   k, v         [B, Hkv, Skv, D] bf16
+ *   lse          [B, Hq,  Sq] fp32, the forward's LSE (required)
+ *   dq           [B, Hq,  Sq,  D] bf16 (written)
+ *   dk, dv       [B, Hkv, Skv, D] bf16 (written; keys no row sees get 0)
+ *   workspace    device memory of at least mk_attn_bwd_workspace_bytes()
+ *                bytes, 256-byte aligned, owned by the caller; holds D_i
+ *                during the call and may be reused after it returns.
+ * Rows without a valid key give dq = 0.  Products run in bf16 with fp32
+ * accumulation; P and dS enter them rounded to bf16.  The result is
+ * deterministic (no atomics).  Outputs may not alias inputs.
+ * Errors as mk_attn_fwd; MK_ERR_WORKSPACE when the workspace is missing or
+ * too small.
+ */
+int mk_attn_bwd(const void *q, const void *k, const void *v, const void *o, const void *dout,
+                const float *lse, void *dq, void *dk, void *dv, int B, int Hq, int Hkv,
+                int Sq, int Skv, int D, int causal, float scale, const int *kv_seqlens,
+                void *workspace, size_t workspace_bytes, void *stream);
+
+/* Bytes of backward workspace: B * Hq * Sq fp32, rounded up to 256; 0 for
+ * invalid sizes. */
+size_t mk_attn_bwd_workspace_bytes(int B, int Hq, int Sq);
 
 /* Static string naming a status code ("MK_OK", ...); never NULL. */
 const char *mk_status_str(int status);

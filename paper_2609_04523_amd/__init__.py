@@ -24,7 +24,8 @@ MK_STATUS = {0: "MK_OK", 1: "MK_ERR_NULL", 2: "MK_ERR_SHAPE", 3: "MK_ERR_UNSUPPO
 
 # every symbol include/mk_attn.h declares
 EXPORTS = ("mk_attn_fwd", "mk_attn_fwd_o32", "mk_attn_fwd_varlen",
-           "mk_attn_decode_workspace_bytes", "mk_attn_decode", "mk_attn_decode_paged", "mk_attn_decode_default_parts",
+           "mk_attn_decode_workspace_bytes", "mk_attn_decode", "mk_attn_decode_paged",
+           "mk_attn_decode_default_parts", "mk_attn_bwd", "mk_attn_bwd_workspace_bytes",
            "mk_status_str", "mk_attn_version")
 
 
@@ -62,6 +63,11 @@ def lib():
         h.mk_attn_decode_paged.restype = i
         h.mk_attn_decode_default_parts.argtypes = [i, i, i]
         h.mk_attn_decode_default_parts.restype = i
+        h.mk_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f,
+                                  vp, vp, sz, vp]
+        h.mk_attn_bwd.restype = i
+        h.mk_attn_bwd_workspace_bytes.argtypes = [i, i, i]
+        h.mk_attn_bwd_workspace_bytes.restype = sz
         h.mk_status_str.argtypes = [i]
         h.mk_status_str.restype = ctypes.c_char_p
         h.mk_attn_version.argtypes = []
@@ -84,6 +90,10 @@ def mk_attn_decode_default_parts(Hq: int, Hkv: int, D: int) -> int:
 
 def mk_attn_decode_workspace_bytes(Hq: int, Hkv: int, D: int, n_parts: int = 0) -> int:
     return lib().mk_attn_decode_workspace_bytes(Hq, Hkv, D, n_parts)
+
+
+def mk_attn_bwd_workspace_bytes(B: int, Hq: int, Sq: int) -> int:
+    return int(lib().mk_attn_bwd_workspace_bytes(B, Hq, Sq))
 
 
 def _check(rc: int):
@@ -147,6 +157,14 @@ def mk_attn_decode_paged(q, k_pages, v_pages, block_table, o, lse, B, Hq, Hkv, p
                                       _ptr(workspace), int(workspace_bytes), _stream(stream)))
 
 
+def mk_attn_bwd(q, k, v, o, dout, lse, dq, dk, dv, B, Hq, Hkv, Sq, Skv, D, causal, scale,
+                kv_seqlens, workspace, workspace_bytes, stream=None):
+    _check(lib().mk_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dout), _ptr(lse),
+                             _ptr(dq), _ptr(dk), _ptr(dv), B, Hq, Hkv, Sq, Skv, D, int(causal),
+                             float(scale), _ptr(kv_seqlens), _ptr(workspace),
+                             int(workspace_bytes), _stream(stream)))
+
+
 # ---------------------------------------------------------------------------
 # conveniences: allocate outputs with torch, then call the entry points above
 # ---------------------------------------------------------------------------
@@ -177,6 +195,34 @@ def fwd(q, k, v, *, causal: bool = True, scale: float | None = None, kv_seqlens=
     entry = mk_attn_fwd_o32 if out_fp32 else mk_attn_fwd
     entry(q, k, v, o, lse, B, Hq, Hkv, Sq, Skv, D, causal, scale, kv_seqlens, stream)
     return o, lse
+
+
+def bwd(q, k, v, o, lse, dout, *, causal: bool = True, scale: float | None = None,
+        kv_seqlens=None, workspace=None, stream=None):
+    """Gradients of the forward fwd(q, k, v) -> (o, lse) given dout = dL/dO:
+    -> (dq [B,Hq,Sq,D], dk, dv [B,Hkv,Skv,D]) bf16.  The LSE is not
+    differentiated."""
+    import torch
+    for t, nm in ((q, "q"), (k, "k"), (v, "v"), (o, "o"), (dout, "dout")):
+        _require(t, nm, torch.bfloat16, 4)
+    _require(lse, "lse", torch.float32, 3)
+    B, Hq, Sq, D = q.shape
+    _, Hkv, Skv, _ = k.shape
+    if o.shape != q.shape or dout.shape != q.shape or tuple(lse.shape) != (B, Hq, Sq):
+        raise ValueError("o and dout must have q's shape, lse [B, Hq, Sq]")
+    if scale is None:
+        scale = D ** -0.5
+    if kv_seqlens is not None:
+        _require(kv_seqlens, "kv_seqlens", torch.int32, 1)
+    need = mk_attn_bwd_workspace_bytes(B, Hq, Sq)
+    if workspace is None:
+        workspace = torch.empty(need, device=q.device, dtype=torch.uint8)
+    dq = torch.empty_like(q)
+    dk = torch.empty_like(k)
+    dv = torch.empty_like(v)
+    mk_attn_bwd(q, k, v, o, dout, lse, dq, dk, dv, B, Hq, Hkv, Sq, Skv, D, causal, scale,
+                kv_seqlens, workspace, workspace.numel() * workspace.element_size(), stream)
+    return dq, dk, dv
 
 
 def fwd_varlen(q, k, v, cu_seqlens_q, cu_seqlens_k, max_seqlen_q: int, *, causal: bool = True,

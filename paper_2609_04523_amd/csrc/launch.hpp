@@ -1,12 +1,13 @@
 // launch.hpp -- host launchers of the kernel families, each in translation
 // units of its own (fwd_launch_d128.hip, fwd_launch_d64.hip,
-// fwd_varlen_launch.hip, dec_launch.hip) so that the library compiles in
+// fwd_varlen_launch.hip, dec_launch.hip, bwd_launch.hip) so that the library compiles in
 // parallel.  Arguments are validated by the callers in mk_attn.hip; these
 // only pick the instantiation and enqueue.
 #pragma once
 
 #include <hip/hip_runtime.h>
 
+#include "bwd_kernel.hpp"
 #include "decode_kernel.hpp"
 #include "fwd_kernel.hpp"
 
@@ -24,5 +25,10 @@ hipError_t launch_fwd_varlen(const FwdArgs& a, unsigned nblocks, int D, bool cau
 
 // Decode: the part kernel (contiguous or paged cache) then the merge kernel.
 hipError_t launch_decode(const DecArgs& a, int D, int qblocks, bool paged, hipStream_t st);
+
+// Backward: the row-delta kernel, the dK/dV kernel (skipped when
+// dkdv_blocks is 0), then the dQ kernel.
+hipError_t launch_bwd(const BwdArgs& a, unsigned delta_blocks, unsigned dq_blocks,
+                      unsigned dkdv_blocks, int D, bool causal, hipStream_t st);
 
 }  // namespace mk

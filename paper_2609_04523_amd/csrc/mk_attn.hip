@@ -11,7 +11,7 @@
 
 namespace {
 
-constexpr int kVersion = 4;
+constexpr int kVersion = 5;
 constexpr int kComputeUnits = 256;    // MI355X
 constexpr int kLdsPerCu = 160 * 1024; // gfx950
 constexpr int kMaxParts = 1 << 20;    // decode parts per call
@@ -268,6 +268,64 @@ int mk_attn_decode_paged(const void* q, const void* k_pages, const void* v_pages
   return e == hipSuccess ? MK_OK : MK_ERR_HIP;
 }
 
+size_t mk_attn_bwd_workspace_bytes(int B, int Hq, int Sq) {
+  if (B < 1 || Hq < 1 || Sq < 1) return 0;
+  return round_up((size_t)B * Hq * Sq * sizeof(float), 256);
+}
+
+int mk_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                const float* lse, void* dq, void* dk, void* dv, int B, int Hq, int Hkv, int Sq,
+                int Skv, int D, int causal, float scale, const int* kv_seqlens, void* workspace,
+                size_t workspace_bytes, void* stream) {
+  if (!q || !k || !v || !o || !dout || !lse || !dq || !dk || !dv) return MK_ERR_NULL;
+  if (B < 1 || Hq < 1 || Hkv < 1 || Sq < 1 || Skv < 1 || D < 1) return MK_ERR_SHAPE;
+  if (Hq % Hkv != 0) return MK_ERR_SHAPE;
+  if (D != 64 && D != 128) return MK_ERR_UNSUPPORTED;
+  if (causal != 0 && causal != 1) return MK_ERR_ARG;
+  if (!isfinite(scale)) return MK_ERR_ARG;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16) ||
+      !aligned(dout, 16) || !aligned(dq, 16) || !aligned(dk, 16) || !aligned(dv, 16) ||
+      !aligned(lse, 4))
+    return MK_ERR_ALIGN;
+  if (kv_seqlens && !aligned(kv_seqlens, 4)) return MK_ERR_ALIGN;
+  // workgroups of each launch
+  const long long rows = (long long)B * Hq * Sq;
+  const long long delta_blocks = (rows + 15) / 16;
+  const long long dq_blocks = (long long)((Sq + 127) / 128) * B * Hq;
+  const long long dkdv_blocks = (long long)((Skv + 127) / 128) * B * Hkv;
+  if (delta_blocks > 0x7fffffffLL || dq_blocks > 0x7fffffffLL || dkdv_blocks > 0x7fffffffLL)
+    return MK_ERR_SHAPE;
+  const size_t need = mk_attn_bwd_workspace_bytes(B, Hq, Sq);
+  if (!workspace || workspace_bytes < need) return MK_ERR_WORKSPACE;
+  if (!aligned(workspace, 256)) return MK_ERR_ALIGN;
+
+  mk::BwdArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.o = static_cast<const uint16_t*>(o);
+  a.dout = static_cast<const uint16_t*>(dout);
+  a.lse = lse;
+  a.dq = static_cast<uint16_t*>(dq);
+  a.dk = static_cast<uint16_t*>(dk);
+  a.dv = static_cast<uint16_t*>(dv);
+  a.delta = static_cast<float*>(workspace);
+  a.kv_seqlens = kv_seqlens;
+  a.B = B;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.Sq = Sq;
+  a.Skv = Skv;
+  a.n_qtiles = (Sq + 127) / 128;
+  a.n_kblocks = (Skv + 127) / 128;
+  a.scale = scale;
+  a.scale_log2 = scale * mk::kLog2e;
+  const hipError_t e =
+      mk::launch_bwd(a, (unsigned)delta_blocks, (unsigned)dq_blocks, (unsigned)dkdv_blocks, D,
+                     causal != 0, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MK_OK : MK_ERR_HIP;
+}
+
 const char* mk_status_str(int status) {
   switch (status) {
     case MK_OK: return "MK_OK";
@@ -275,7 +333,7 @@ const char* mk_status_str(int status) {
     case MK_ERR_SHAPE: return "MK_ERR_SHAPE: invalid or too large sizes, or Hq % Hkv != 0";
     case MK_ERR_UNSUPPORTED: return "MK_ERR_UNSUPPORTED: head dim or group size not built";
     case MK_ERR_ALIGN: return "MK_ERR_ALIGN: a pointer is not aligned as required";
-    case MK_ERR_WORKSPACE: return "MK_ERR_WORKSPACE: decode workspace missing or too small";
+    case MK_ERR_WORKSPACE: return "MK_ERR_WORKSPACE: workspace missing or too small";
     case MK_ERR_HIP: return "MK_ERR_HIP: the HIP runtime refused a launch";
     case MK_ERR_ARG: return "MK_ERR_ARG: non-finite scale, bad causal flag or part count";
     default: return "MK_ERR_UNKNOWN: not an mk_status value";

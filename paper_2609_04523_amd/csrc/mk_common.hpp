@@ -119,6 +119,17 @@ __device__ __forceinline__ bf16x4 lds_read_tr16(const void* lds) {
       (__attribute__((address_space(3))) bf16x4*)(lds));
 }
 
+// Same, with the address given as a 32-bit LDS address (turned into an LDS
+// pointer directly, see load_lds16_at).
+__device__ __forceinline__ bf16x4 lds_read_tr16_at(uint32_t lds_addr) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      (__attribute__((address_space(3))) bf16x4*)(uintptr_t)lds_addr);
+}
+// 16-byte LDS read at a 32-bit LDS address.
+__device__ __forceinline__ u32x4 lds_read_b128_at(uint32_t lds_addr) {
+  return *(const __attribute__((address_space(3))) u32x4*)(uintptr_t)lds_addr;
+}
+
 // The same read issued as inline assembly, so that the compiler's wait
 // insertion does not tie it to in-flight LDS-DMA loads of other buffers.
 // The result is NOT ready on return: pass it through lds_wait4() before

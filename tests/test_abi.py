@@ -43,7 +43,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert mk.mk_attn_version() == 4
+    assert mk.mk_attn_version() == 5
     names = ["MK_OK", "MK_ERR_NULL", "MK_ERR_SHAPE", "MK_ERR_UNSUPPORTED", "MK_ERR_ALIGN",
              "MK_ERR_WORKSPACE", "MK_ERR_HIP", "MK_ERR_ARG"]
     for code, name in enumerate(names):
@@ -210,3 +210,37 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(mk, "LIB_PATH", str(tmp_path / "libmk_attn.so"))
     with pytest.raises(RuntimeError, match="has not been built"):
         mk.lib()
+
+
+def bwd_rc(lib, *, q=P, k=P, v=P, o=P, do=P, lse=P, dq=P, dk=P, dv=P, B=2, Hq=8, Hkv=2, Sq=100,
+           Skv=200, D=128, causal=1, scale=0.125, seqlens=None, ws=P, ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = lib.mk_attn_bwd_workspace_bytes(max(B, 1), max(Hq, 1), max(Sq, 1))
+    return lib.mk_attn_bwd(q, k, v, o, do, lse, dq, dk, dv, B, Hq, Hkv, Sq, Skv, D, causal, scale,
+                           seqlens, ws, ws_bytes, None)
+
+
+def test_bwd_workspace_bytes(lib):
+    assert lib.mk_attn_bwd_workspace_bytes(2, 8, 100) == 6400  # 1600 fp32, 256-aligned
+    assert lib.mk_attn_bwd_workspace_bytes(1, 1, 1) == 256
+    assert lib.mk_attn_bwd_workspace_bytes(0, 8, 100) == 0
+    assert lib.mk_attn_bwd_workspace_bytes(2, 8, -1) == 0
+
+
+def test_bwd_validation(lib):
+    for name in ("q", "k", "v", "o", "do", "lse", "dq", "dk", "dv"):
+        assert bwd_rc(lib, **{name: None}) == 1
+    for name in ("B", "Hq", "Hkv", "Sq", "Skv"):
+        assert bwd_rc(lib, **{name: 0}) == 2
+    assert bwd_rc(lib, Hq=6, Hkv=4) == 2
+    assert bwd_rc(lib, B=1 << 16, Hq=1 << 12, Hkv=1 << 12, Sq=1 << 10, ws_bytes=1 << 62) == 2
+    assert bwd_rc(lib, D=96) == 3
+    assert bwd_rc(lib, causal=2) == 7
+    assert bwd_rc(lib, scale=math.inf) == 7
+    for name in ("q", "k", "v", "o", "do", "dq", "dk", "dv"):
+        assert bwd_rc(lib, **{name: P_ODD}) == 4
+    assert bwd_rc(lib, lse=P + 2) == 4
+    assert bwd_rc(lib, seqlens=P + 1) == 4
+    assert bwd_rc(lib, ws=None) == 5
+    assert bwd_rc(lib, ws_bytes=lib.mk_attn_bwd_workspace_bytes(2, 8, 100) - 1) == 5
+    assert bwd_rc(lib, ws=P + 16) == 4
