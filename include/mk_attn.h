@@ -207,7 +207,8 @@ int mk_attn_decode_default_parts(int Hq, int Hkv, int D);
  *   dk, dv       [B, Hkv, Skv, D] bf16 (written; keys no row sees get 0)
  *   workspace    device memory of at least mk_attn_bwd_workspace_bytes()
  *                bytes, 256-byte aligned, owned by the caller; holds D_i
- *                during the call and may be reused after it returns.
+ *                and LSE_i log2 e during the call (written by it, so no
+ *                clearing is needed) and may be reused after it returns.
  * Rows without a valid key give dq = 0.  Products run in bf16 with fp32
  * accumulation; P and dS enter them rounded to bf16.  The result is
  * deterministic (no atomics).  Outputs may not alias inputs.
@@ -219,8 +220,9 @@ int mk_attn_bwd(const void *q, const void *k, const void *v, const void *o, cons
                 int Sq, int Skv, int D, int causal, float scale, const int *kv_seqlens,
                 void *workspace, size_t workspace_bytes, void *stream);
 
-/* Bytes of backward workspace: B * Hq * Sq fp32, rounded up to 256; 0 for
- * invalid sizes. */
+/* Bytes of backward workspace: two arrays of B * Hq * round_up(Sq, 128)
+ * fp32 (D_i and LSE_i log2 e), each rounded up to 256 bytes; 0 for invalid
+ * sizes. */
 size_t mk_attn_bwd_workspace_bytes(int B, int Hq, int Sq);
 
 /* Static string naming a status code ("MK_OK", ...); never NULL. */

@@ -41,9 +41,12 @@ struct BwdArgs {
   uint16_t* dq;          // [B, Hq, Sq, D] bf16 (written)
   uint16_t* dk;          // [B, Hkv, Skv, D] bf16 (written)
   uint16_t* dv;
-  float* delta;          // workspace [B, Hq, Sq]: D_i
+  float* delta;          // workspace [B, Hq, sq_pad]: D_i (0 on padding rows)
+  float* lse2;           // workspace [B, Hq, sq_pad]: LSE_i log2(e); +inf on rows
+                         // without keys and on padding rows, so that P = 0 there
   const int* kv_seqlens;
   int B, Hq, Hkv, Sq, Skv;
+  int sq_pad;            // Sq rounded up to a multiple of 128
   int n_qtiles;          // dQ kernel: ceil(Sq / 128)
   int n_kblocks;         // dK/dV kernel: ceil(Skv / 128)
   float scale;
@@ -53,18 +56,25 @@ struct BwdArgs {
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// D_i = dO_i . O_i, 16 lanes per row of D bf16 values.
+// D_i = dO_i . O_i (16 lanes per row of D bf16 values) and LSE_i log2(e),
+// over sq_pad rows per (b, hq): rows past Sq get D = 0 and +inf.  The dQ
+// and dK/dV kernels read both arrays without row bounds (their 128- and
+// 64-row tiles end at or before sq_pad).
 template <int D>
 __global__ __launch_bounds__(256) void bwd_delta_kernel(BwdArgs a) {
   constexpr int LPR = 16;
   constexpr int WORDS = D / LPR / 2;  // 32-bit words (bf16 pairs) per lane
-  const long long rows = (long long)a.B * a.Hq * a.Sq;
+  const long long rows = (long long)a.B * a.Hq * a.sq_pad;
   const long long row = (long long)blockIdx.x * (256 / LPR) + threadIdx.x / LPR;
   const int part = threadIdx.x % LPR;
+  const long long bh = row / a.sq_pad;
+  const int i = (int)(row - bh * a.sq_pad);
+  const bool real = row < rows && i < a.Sq;
+  const long long src = bh * a.Sq + i;  // row of O, dO and LSE
   float acc = 0.f;
-  if (row < rows) {
-    const uint32_t* o = reinterpret_cast<const uint32_t*>(a.o + row * D) + part * WORDS;
-    const uint32_t* d = reinterpret_cast<const uint32_t*>(a.dout + row * D) + part * WORDS;
+  if (real) {
+    const uint32_t* o = reinterpret_cast<const uint32_t*>(a.o + src * D) + part * WORDS;
+    const uint32_t* d = reinterpret_cast<const uint32_t*>(a.dout + src * D) + part * WORDS;
 #pragma unroll
     for (int w = 0; w < WORDS; ++w) {
       const uint32_t x = o[w], y = d[w];
@@ -74,13 +84,18 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(BwdArgs a) {
   }
 #pragma unroll
   for (int off = LPR / 2; off >= 1; off >>= 1) acc += __shfl_xor(acc, off, 64);
-  if (row < rows && part == 0) a.delta[row] = acc;
+  if (row < rows && part == 0) {
+    const float lse = real ? a.lse[src] : kNegInf;
+    a.delta[row] = acc;
+    a.lse2[row] = lse == kNegInf ? __builtin_inff() : lse * kLog2e;
+  }
 }
 
-// P and the validity of one element; lse2 = LSE * log2 e of the row.
-__device__ __forceinline__ float bwd_prob(float s, float c, float lse, bool valid) {
-  const float p = fast_exp2(fmaf(s, c, -lse * kLog2e));
-  return (valid && lse != kNegInf) ? p : 0.f;
+// P of one element: 2^(s c - LSE log2 e), 0 where masked (lse2 = +inf on
+// rows without keys gives 0 by itself).
+__device__ __forceinline__ float bwd_prob(float s, float c, float lse2, bool valid) {
+  const float p = fast_exp2(fmaf(s, c, -lse2));
+  return valid ? p : 0.f;
 }
 
 // ---------------------------------------------------------------------------
@@ -133,8 +148,9 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
     qf[s] = as_bf16x8(u);
     df[s] = as_bf16x8(w);
   }
-  const float lse = row_ok ? a.lse[row0 + qrow] : kNegInf;
-  const float dl = row_ok ? a.delta[row0 + qrow] : 0.f;
+  const size_t prow = ((size_t)b * a.Hq + hq) * (size_t)a.sq_pad + qrow;  // qrow < sq_pad
+  const float lse2 = a.lse2[prow];
+  const float dl = a.delta[prow];
   const int lim = CAUSAL ? min(L - 1, qrow + off) : L - 1;  // last key this row sees
 
   // tile loads, as in the forward kernel
@@ -219,7 +235,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
       for (int j = 0; j < 8; ++j) {
         const int r = 8 * (kc % 2) + j;
         const int key = key0 + (kc / 2) * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-        const float p = bwd_prob(st[kc / 2][r], c, lse, key <= lim);
+        const float p = bwd_prob(st[kc / 2][r], c, lse2, key <= lim);
         e[j] = p * (dpt[kc / 2][r] - dl);
       }
       dsf[kc] = to_bf16x8(e[0], e[1], e[2], e[3], e[4], e[5], e[6], e[7]);
@@ -258,22 +274,42 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// dK, dV: workgroup = 4 waves x 32 keys of one (b, kv head); 64-row tiles of
-// Q, dO (and their LSE, D) of every query head of the group.
+// dK, dV: workgroup = 4 waves x 32 keys of one (b, kv head).  The tiles of
+// 64 query rows of every query head of the group that see a key of the
+// block stream through LDS (NBUF-deep ring of Q, dO and their LSE log2 e
+// and D rows); each wave keeps its keys' K and V in registers and its
+// dK^T, dV^T accumulators in accumulation registers.
+//
+// Per 32-row chunk c of a tile, with S = Q K^T and dP = dO V^T:
+//   A(c):  S(c), dP(c) on the matrix cores (Q, dO fragments from LDS);
+//   B(c):  P = 2^(S c - lse2), dS = P (dP - D) on the vector ALU, as bf16;
+//   C(c):  dV^T += dO^T P, dK^T += Q^T dS (transposing LDS reads).
+// The steps are software-pipelined one chunk deep: A(c + 1) runs on the
+// matrix cores while the vector ALU forms B(c), then C(c) follows, so the
+// exponentials cost no matrix-core time.  LDS reads are issued as inline
+// assembly a few ahead of their use, and waited for by count.
 // ---------------------------------------------------------------------------
+template <int D>
+struct DkdvShape {
+  static constexpr int WAVES = 4, BK = 128, BQ = 64, NBUF = 4;
+  static constexpr int KSTEPS = D / 16, DBLK = D / 32, CHUNKS = D / 8;
+  static constexpr int ROW_BYTES = D * 2, TILE_BYTES = BQ * ROW_BYTES;
+  static constexpr int BUF_BYTES = 2 * TILE_BYTES;  // Q tile, then dO tile
+  static constexpr int ROWS_PER_KB = 512 / D;
+  static constexpr int BLOCKS_PER_WAVE = TILE_BYTES / 1024 / WAVES;  // per tensor
+  static constexpr int ROW_STEP = WAVES * ROWS_PER_KB;
+  static constexpr int RL_BYTES = 2 * BQ * 4;  // lse2 row, then D row, per buffer
+  static constexpr int RW = 4;                 // LDS reads kept in flight
+};
+
 template <int D, bool CAUSAL>
 __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
-  constexpr int WAVES = 4, BK = 128, BQ = 64;
-  constexpr int KSTEPS = D / 16, DBLK = D / 32, CHUNKS = D / 8;
-  constexpr int ROW_BYTES = D * 2, TILE = BQ * D, TILE_BYTES = TILE * 2;
-  constexpr int ROWS_PER_KB = 512 / D;
-  constexpr int BLOCKS_PER_WAVE = BQ * D * 2 / 1024 / WAVES;
-  // per thread per tile: Q and dO blocks, plus one dword of LSE or D on
-  // waves 0 and 1
-  __shared__ __attribute__((aligned(1024))) uint16_t q_lds[2][TILE];
-  __shared__ __attribute__((aligned(1024))) uint16_t do_lds[2][TILE];
-  __shared__ __attribute__((aligned(256))) float lse_lds[2][BQ];
-  __shared__ __attribute__((aligned(256))) float dl_lds[2][BQ];
+  using S = DkdvShape<D>;
+  constexpr int KSTEPS = S::KSTEPS, DBLK = S::DBLK, ROW_BYTES = S::ROW_BYTES;
+  constexpr int TILE_BYTES = S::TILE_BYTES, NBUF = S::NBUF, BQ = S::BQ;
+  static_assert(S::ROW_STEP % 16 == 0, "row step must preserve the swizzle");
+  __shared__ __attribute__((aligned(1024))) uint8_t qd_lds[NBUF * S::BUF_BYTES];
+  __shared__ __attribute__((aligned(512))) uint8_t rl_lds[NBUF * S::RL_BYTES];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 31, h = lane >> 5;
@@ -286,7 +322,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   const int G = a.Hq / a.Hkv;
   const int L = a.kv_seqlens ? clamp_len(a.kv_seqlens[b], a.Skv) : a.Skv;
   const int off = L - a.Sq;
-  const int k0 = kblk * BK;
+  const int k0 = kblk * S::BK;
   const int kw0 = k0 + wave * 32;  // this wave's first key
   const int key = kw0 + n;         // this lane's key (MFMA column)
   const float c = a.scale_log2;
@@ -298,9 +334,9 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   const int n_qt = q_first < a.Sq ? (a.Sq + BQ - 1) / BQ - qt_first : 0;
   const int n_it = G * n_qt;
 
-  // K^T and V^T fragments of this wave's keys (B operand: lane = key
-  // column, k-group h = head dims 16 s + 8 h .. +7); rows past the
-  // sequence read its last row (their gradients are masked to zero)
+  // K and V of this wave's keys as B operands (lane = key column, k-group
+  // h = head dims 16 s + 8 h .. +7); keys past the sequence read its last
+  // row (their gradients are replaced by zeros at the end)
   const size_t kvh = ((size_t)b * a.Hkv + g) * (size_t)a.Skv;
   const int krow = min(key, L > 0 ? L - 1 : 0);
   bf16x8 kf[KSTEPS], vf[KSTEPS];
@@ -315,15 +351,14 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
     vf[s] = as_bf16x8(w);
   }
 
-  // tile loads: Q and dO rows like the forward's K/V tiles; LSE by wave 0
-  // and D by wave 1, one dword per lane
-  constexpr int ROW_STEP = WAVES * ROWS_PER_KB;
-  const int dma_row = wave * ROWS_PER_KB + lane / CHUNKS;
-  const int dma_ch = ((lane % CHUNKS) ^ fwd_swz<D>(dma_row)) * 16;
-  const uint32_t q_lds_w = __builtin_amdgcn_readfirstlane(lds_addr(&q_lds[0][0]) + wave * 1024);
-  const uint32_t do_lds_w = __builtin_amdgcn_readfirstlane(lds_addr(&do_lds[0][0]) + wave * 1024);
-  const uint32_t lse_lds0 = __builtin_amdgcn_readfirstlane(lds_addr(&lse_lds[0][0]));
-  const uint32_t dl_lds0 = __builtin_amdgcn_readfirstlane(lds_addr(&dl_lds[0][0]));
+  // ---- tile loads: Q and dO rows of tile `it` into ring buffer `buf`
+  // (rows past Sq repeat row Sq - 1; their lse2 = +inf zeroes them), the
+  // lse2 row by wave 0 and the D row by wave 1 (one dword per lane) ----
+  const int dma_row = wave * S::ROWS_PER_KB + lane / S::CHUNKS;
+  const int dma_ch = ((lane % S::CHUNKS) ^ fwd_swz<D>(dma_row)) * 16;
+  const uint32_t qd_base = lds_addr(&qd_lds[0]);
+  const uint32_t rl_base = lds_addr(&rl_lds[0]);
+  const uint32_t qd_w = __builtin_amdgcn_readfirstlane(qd_base + wave * 1024);
   auto issue_tile = [&](int it, int buf) {
     const int hq = g * G + it / n_qt;
     const int q0 = (qt_first + it % n_qt) * BQ;
@@ -331,29 +366,49 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
     const int tlim = a.Sq - 1 - q0;  // last valid row of the tile
     const char* qg = reinterpret_cast<const char*>(a.q + (row0 + q0) * D);
     const char* dg = reinterpret_cast<const char*>(a.dout + (row0 + q0) * D);
+    const uint32_t lbuf = qd_w + buf * S::BUF_BYTES;
 #pragma unroll
-    for (int p = 0; p < BLOCKS_PER_WAVE; ++p) {
-      const uint32_t goff = (uint32_t)(min(dma_row + p * ROW_STEP, tlim) * ROW_BYTES + dma_ch);
-      const uint32_t lds_off = buf * TILE_BYTES + p * WAVES * 1024;
-      load_lds16_at(qg + goff, q_lds_w + lds_off);
-      load_lds16_at(dg + goff, do_lds_w + lds_off);
+    for (int p = 0; p < S::BLOCKS_PER_WAVE; ++p) {
+      const uint32_t goff = (uint32_t)(min(dma_row + p * S::ROW_STEP, tlim) * ROW_BYTES + dma_ch);
+      load_lds16_at(qg + goff, lbuf + p * S::WAVES * 1024);
+      load_lds16_at(dg + goff, lbuf + TILE_BYTES + p * S::WAVES * 1024);
     }
     if (wave < 2) {
-      const float* src = (wave == 0 ? a.lse : a.delta) + row0 + q0 + min(lane, tlim);
-      const uint32_t dst = (wave == 0 ? lse_lds0 : dl_lds0) + buf * BQ * 4;
+      const size_t prow = ((size_t)b * a.Hq + hq) * (size_t)a.sq_pad + q0 + lane;
+      const float* src = (wave == 0 ? a.lse2 : a.delta) + prow;
+      const uint32_t dst =
+          __builtin_amdgcn_readfirstlane(rl_base + buf * S::RL_BYTES + wave * BQ * 4);
       __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
                                        (void __attribute__((address_space(3)))*)(uintptr_t)dst,
                                        4, 0, 0);
     }
   };
+  // s_waitcnt vmcnt: at most k tiles' loads issued after the one waited for
+  // remain outstanding (waves 0 and 1 issue one more load per tile)
+  constexpr int LPT = 2 * S::BLOCKS_PER_WAVE;
+  auto wait_tiles = [&](int k) {
+    if (wave < 2) {
+      if (k >= 2) wait_vmcnt<2 * (LPT + 1)>();
+      else if (k == 1) wait_vmcnt<LPT + 1>();
+      else wait_vmcnt<0>();
+    } else {
+      if (k >= 2) wait_vmcnt<2 * LPT>();
+      else if (k == 1) wait_vmcnt<LPT>();
+      else wait_vmcnt<0>();
+    }
+  };
 
-  // LDS read addresses: Q / dO rows (A operand: row = query, 8 head dims)
-  // and transposing Q^T / dO^T reads (A operand of dK^T, dV^T)
-  uint32_t qr_addr[KSTEPS];
+  // ---- LDS read addresses (the ring buffer's offset is folded in and
+  // moved on per tile) ----
+  // Q / dO fragment s of row n + 32 ch: Q at qa[s] + 32 ch rows, dO one
+  // tile further
+  uint32_t qa[KSTEPS];
 #pragma unroll
   for (int s = 0; s < KSTEPS; ++s)
-    qr_addr[s] = n * ROW_BYTES + (((2 * s + h) ^ fwd_swz<D>(n)) << 4);
-  uint32_t qt_addr[DBLK][2];
+    qa[s] = qd_base + n * ROW_BYTES + (((2 * s + h) ^ fwd_swz<D>(n)) << 4);
+  // transposing reads: rows 4 h + i/4 (+ 8), columns 32 db + 16 ((l/16) % 2)
+  // + 4 (i % 4), i = l % 16
+  uint32_t qt[DBLK][2];
   {
     const int tr_i = lane & 15;
     const int tr_row = 4 * h + (tr_i >> 2);
@@ -364,10 +419,11 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
       for (int hh = 0; hh < 2; ++hh) {
         const int r = tr_row + 8 * hh;
         const int col = db * 32 + tr_col;
-        qt_addr[db][hh] = r * ROW_BYTES + ((((col >> 3) ^ fwd_swz<D>(r)) << 4) | ((col & 7) * 2));
+        qt[db][hh] = qd_base + r * ROW_BYTES + ((((col >> 3) ^ fwd_swz<D>(r)) << 4) | ((col & 7) * 2));
       }
   }
-  const uint32_t ql0 = lds_addr(&q_lds[0][0]), dol0 = lds_addr(&do_lds[0][0]);
+  // lse2 / D of rows 32 ch + 8 j + 4 h .. +3
+  uint32_t la = rl_base + 16 * h;
 
   f32x16 dk_acc[DBLK], dv_acc[DBLK];
 #pragma unroll
@@ -375,82 +431,186 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) dk_acc[db][r] = dv_acc[db][r] = 0.f;
 
-  if (n_it > 0) issue_tile(0, 0);
-  if (n_it > 1) issue_tile(1, 1);
-  for (int it = 0; it < n_it; ++it) {
-    const int buf = it & 1;
-    if (it + 1 < n_it) {
-      // the next tile's loads may still be in flight
-      if (wave < 2)
-        wait_vmcnt<2 * BLOCKS_PER_WAVE + 1>();
-      else
-        wait_vmcnt<2 * BLOCKS_PER_WAVE>();
-    } else {
-      wait_vmcnt<0>();
-    }
-    __syncthreads();
-    const int q0 = (qt_first + it % n_qt) * BQ;
-    // rows of this tile this wave's keys can be seen by
-    const bool live = !CAUSAL || q0 + BQ - 1 + off >= kw0;
-    if (live) {
-      const uint32_t qb_base = ql0 + buf * TILE_BYTES, db_base = dol0 + buf * TILE_BYTES;
-      const float* lse_t = &lse_lds[buf][0];
-      const float* dl_t = &dl_lds[buf][0];
-#pragma unroll
-      for (int ch = 0; ch < BQ / 32; ++ch) {
-        // S = Q K^T and dP = dO V^T for query rows 32 ch .. +31
-        f32x16 sq, dp;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sq[r] = dp[r] = 0.f;
-#pragma unroll
-        for (int s = 0; s < KSTEPS; ++s) {
-          const uint32_t ad = qr_addr[s] + ch * 32 * ROW_BYTES;
-          const bf16x8 qa = as_bf16x8(lds_read_b128_at(qb_base + ad));
-          const bf16x8 da = as_bf16x8(lds_read_b128_at(db_base + ad));
-          sq = mfma32(qa, kf[s], sq);
-          dp = mfma32(da, vf[s], dp);
-        }
-        // P and dS; element r is query row 32 ch + 8 (r/4) + 4 h + r % 4
-        bf16x8 pf[2], dsf[2];
-#pragma unroll
-        for (int kc = 0; kc < 2; ++kc) {
-          float pe[8], de[8];
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const int r = 8 * kc + j;
-            const int qr = ch * 32 + 8 * (r >> 2) + 4 * h + (r & 3);  // row within the tile
-            const int qabs = q0 + qr;
-            const bool valid = qabs < a.Sq && key < L && (!CAUSAL || key <= qabs + off);
-            const float p = bwd_prob(sq[r], c, lse_t[qr], valid);
-            pe[j] = p;
-            de[j] = p * (dp[r] - dl_t[qr]);
-          }
-          pf[kc] = to_bf16x8(pe[0], pe[1], pe[2], pe[3], pe[4], pe[5], pe[6], pe[7]);
-          dsf[kc] = to_bf16x8(de[0], de[1], de[2], de[3], de[4], de[5], de[6], de[7]);
-        }
-        // dV^T += dO^T P and dK^T += Q^T dS over the two 16-row chunks
-#pragma unroll
-        for (int kc = 0; kc < 2; ++kc) {
-          const uint32_t roff = (ch * 32 + kc * 16) * ROW_BYTES;
-#pragma unroll
-          for (int db = 0; db < DBLK; ++db) {
-            const bf16x4 dlo = lds_read_tr16_at(db_base + roff + qt_addr[db][0]);
-            const bf16x4 dhi = lds_read_tr16_at(db_base + roff + qt_addr[db][1]);
-            dv_acc[db] = mfma32(cat(dlo, dhi), pf[kc], dv_acc[db]);
-            const bf16x4 qlo = lds_read_tr16_at(qb_base + roff + qt_addr[db][0]);
-            const bf16x4 qhi = lds_read_tr16_at(qb_base + roff + qt_addr[db][1]);
-            dk_acc[db] = mfma32(cat(qlo, qhi), dsf[kc], dk_acc[db]);
-          }
+  f32x16 sacc[2][2];  // [chunk][S, dP]
+  u32x4 lv[8];        // lse2 (j = 0..3) and D (4 + j) of the chunk B works on
+  bf16x8 pf[2], dsf[2];
+  int diag = 0;       // key - off - (first row of the chunk) - 4 h
+
+  // One pipeline step: A(chunk ACH of the tile the fragment addresses point
+  // at) with B(chunk BCH) on the vector ALU in between, then C(chunk BCH),
+  // then the lse2 / D reads for chunk LCH (read by the next step's B).  -1:
+  // no such part.  Elements with diag > 8 (r/4) + r % 4 are masked.
+  auto step = [&](auto ach_tag, auto bch_tag, auto lch_tag) {
+    constexpr int ACH = decltype(ach_tag)::value;
+    constexpr int BCH = decltype(bch_tag)::value;
+    constexpr int LCH = decltype(lch_tag)::value;
+    constexpr int NA = ACH >= 0 ? 2 * KSTEPS : 0;
+    constexpr int NC = BCH >= 0 ? 8 * DBLK : 0;
+    constexpr int NL = LCH >= 0 ? 8 : 0;
+    constexpr int TOT = NA + NC + NL;
+    constexpr int RS = S::RW < TOT ? S::RW : TOT;
+    static_assert(RS >= 4 || NC == 0, "C consumes four reads at a time");
+    u32x4 ar[NA > 0 ? NA : 1];
+    u32x2 cr[NC > 0 ? NC : 1];
+    // item J of the read stream: A fragments (Q s, dO s for s = 0, 1, ..),
+    // then C's transposing reads (kc, db, dO lo / hi, Q lo / hi), then the
+    // lse2 / D rows of chunk LCH
+    auto issue = [&](auto j_tag) {
+      constexpr int J = decltype(j_tag)::value;
+      if constexpr (J < NA) {
+        constexpr int OFF = (J % 2) * TILE_BYTES + (ACH > 0 ? ACH : 0) * 32 * ROW_BYTES;
+        ar[J] = lds_read_b128_async_off<OFF>(qa[J / 2]);
+      } else if constexpr (J < NA + NC) {
+        constexpr int C = J - NA;
+        constexpr int KC = C / (4 * DBLK), DB = (C / 4) % DBLK, W = C % 4;
+        constexpr int OFF = (W < 2 ? TILE_BYTES : 0) + ((BCH > 0 ? BCH : 0) * 32 + KC * 16) * ROW_BYTES;
+        cr[C] = lds_read_tr16_async_off<OFF>(qt[DB][W % 2]);
+      } else if constexpr (J < TOT) {
+        constexpr int Lx = J - NA - NC;
+        constexpr int OFF = (Lx / 4) * BQ * 4 + (LCH > 0 ? LCH : 0) * 128 + (Lx % 4) * 32;
+        lv[Lx] = lds_read_b128_async_off<OFF>(la);
+      }
+    };
+    static_for<0, RS>(issue);
+
+    // B: element r of chunk BCH (row 8 (r/4) + 4 h + r % 4 of the chunk)
+    float pe[8], de[8];
+    auto b_elem = [&](auto r_tag) {
+      constexpr int R = decltype(r_tag)::value;
+      if constexpr (BCH >= 0) {
+        const float sv = sacc[BCH > 0 ? 1 : 0][0][R];
+        const float dp = sacc[BCH > 0 ? 1 : 0][1][R];
+        const float l2 = __uint_as_float(lv[R / 4][R % 4]);
+        const float dl = __uint_as_float(lv[4 + R / 4][R % 4]);
+        float p = fast_exp2(fmaf(sv, c, -l2));
+        p = diag <= 8 * (R / 4) + (R % 4) ? p : 0.f;
+        pe[R % 8] = p;
+        de[R % 8] = p * (dp - dl);
+        if constexpr (R % 8 == 7) {
+          pf[R / 8] = to_bf16x8(pe[0], pe[1], pe[2], pe[3], pe[4], pe[5], pe[6], pe[7]);
+          dsf[R / 8] = to_bf16x8(de[0], de[1], de[2], de[3], de[4], de[5], de[6], de[7]);
         }
       }
+    };
+
+    if constexpr (NA > 0) {
+      constexpr int AC = ACH > 0 ? 1 : 0;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[AC][0][r] = sacc[AC][1][r] = 0.f;
+      constexpr int EPM = 16 / NA;  // B elements per product
+      static_for<0, NA>([&](auto i_tag) {
+        constexpr int I = decltype(i_tag)::value;
+        constexpr int AHEAD = (I + RS < TOT ? I + RS : TOT) - I - 1;
+        lds_wait_lgkm<AHEAD>();
+        lds_ready(ar[I]);
+        if constexpr (I == 0 && BCH >= 0) {
+          // the lse2 / D reads were issued before this step's
+#pragma unroll
+          for (int l = 0; l < 8; ++l) lds_ready(lv[l]);
+        }
+        if constexpr (I % 2 == 0)
+          sacc[AC][0] = mfma32(as_bf16x8(ar[I]), kf[I / 2], sacc[AC][0]);  // S
+        else
+          sacc[AC][1] = mfma32(as_bf16x8(ar[I]), vf[I / 2], sacc[AC][1]);  // dP
+        issue(std::integral_constant<int, I + RS>());
+        static_for<0, EPM>([&](auto e_tag) {
+          b_elem(std::integral_constant<int, I * EPM + decltype(e_tag)::value>());
+        });
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    } else if constexpr (BCH >= 0) {
+      lds_wait_lgkm<RS>();
+#pragma unroll
+      for (int l = 0; l < 8; ++l) lds_ready(lv[l]);
+      static_for<0, 16>(b_elem);
+      __builtin_amdgcn_sched_barrier(0);
     }
+
+    if constexpr (NC > 0) {
+      static_for<0, 2 * DBLK>([&](auto m_tag) {
+        constexpr int M = decltype(m_tag)::value;  // (kc, db) = (M / DBLK, M % DBLK)
+        constexpr int BASE = NA + 4 * M;           // stream index of its first read
+        constexpr int AHEAD = (BASE + RS < TOT ? BASE + RS : TOT) - (BASE + 3) - 1;
+        static_assert(AHEAD >= 0, "read window");
+        lds_wait_lgkm<AHEAD>();
+        u32x2& d0 = cr[4 * M];
+        u32x2& d1 = cr[4 * M + 1];
+        u32x2& q0r = cr[4 * M + 2];
+        u32x2& q1r = cr[4 * M + 3];
+        lds_ready(d0);
+        lds_ready(d1);
+        lds_ready(q0r);
+        lds_ready(q1r);
+        const bf16x8 dt = as_bf16x8(u32x4{d0[0], d0[1], d1[0], d1[1]});
+        const bf16x8 qtf = as_bf16x8(u32x4{q0r[0], q0r[1], q1r[0], q1r[1]});
+        dv_acc[M % DBLK] = mfma32(dt, pf[M / DBLK], dv_acc[M % DBLK]);
+        dk_acc[M % DBLK] = mfma32(qtf, dsf[M / DBLK], dk_acc[M % DBLK]);
+        static_for<0, 4>([&](auto e_tag) {
+          issue(std::integral_constant<int, BASE + RS + decltype(e_tag)::value>());
+        });
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    }
+    // remaining reads of the stream (the lse2 / D rows for the next step)
+    static_for<NA + NC + RS, TOT>(issue);
+  };
+
+  using N1 = std::integral_constant<int, -1>;
+  using C0 = std::integral_constant<int, 0>;
+  using C1 = std::integral_constant<int, 1>;
+
+  if (n_it > 0) {
+    for (int i = 0; i < NBUF - 1 && i < n_it; ++i) issue_tile(i, i);
+    wait_tiles(min(n_it, NBUF - 1) - 1);
     __syncthreads();
-    if (it + 2 < n_it) issue_tile(it + 2, buf);
+    step(C0(), N1(), C0());  // A(tile 0, chunk 0), lse2 / D of chunk 0
+  }
+  const uint32_t ring = NBUF * S::BUF_BYTES;
+  for (int it = 0; it < n_it; ++it) {
+    const int buf = it % NBUF;
+    // ring offset from this tile's buffer to the next one's
+    const int adv = buf == NBUF - 1 ? (int)S::BUF_BYTES - (int)ring : S::BUF_BYTES;
+    const int adv_rl = buf == NBUF - 1 ? S::RL_BYTES - NBUF * S::RL_BYTES : S::RL_BYTES;
+    const int q0 = (qt_first + it % n_qt) * BQ;
+    const bool m0 = CAUSAL && q0 + off < kw0 + 31;
+    const bool m1 = CAUSAL && q0 + 32 + off < kw0 + 31;
+
+    // chunk 0: A(chunk 1) with B(chunk 0), C(chunk 0), rows of chunk 1.
+    // The loop body has no branch around the steps: a branch would make
+    // the compiler move the accumulators between register files at every
+    // product.  So the mask is always applied (an unmasked chunk gets a
+    // threshold every element passes), and the last tile's second step
+    // also forms A of a tile that does not exist (in-bounds reads of a
+    // stale ring buffer, never used).
+    diag = m0 ? key - off - q0 - 4 * h : -0x40000000;
+    step(C1(), C0(), C1());
+
+    // tile it + 1 must have landed; every wave is done with tile it - 1,
+    // whose buffer takes tile it + NBUF - 1
+    wait_tiles(it + 2 < n_it ? 1 : 0);
+    __syncthreads();
+    if (it + NBUF - 1 < n_it) issue_tile(it + NBUF - 1, (it + NBUF - 1) % NBUF);
+#pragma unroll
+    for (int s = 0; s < KSTEPS; ++s) qa[s] += adv;
+    la += adv_rl;
+
+    // chunk 1: A(next tile, chunk 0) with B(chunk 1), C(chunk 1), rows of
+    // the next tile's chunk 0
+    diag = m1 ? key - off - q0 - 32 - 4 * h : -0x40000000;
+    step(C0(), C1(), C0());
+    // the transposing reads move on once C of chunk 1 is done
+#pragma unroll
+    for (int db = 0; db < DBLK; ++db) {
+      qt[db][0] += adv;
+      qt[db][1] += adv;
+    }
   }
 
   // dK = scale * dk_acc^T, dV = dv_acc^T: lane (key n, k-group h) holds
-  // head dims db*32 + 8 (r/4) + 4 h + r % 4 of its key
+  // head dims db*32 + 8 (r/4) + 4 h + r % 4 of its key; keys past the
+  // sequence get zeros
   if (key < a.Skv) {
+    const bool kvalid = key < L;
     uint16_t* dkr = a.dk + (kvh + key) * D;
     uint16_t* dvr = a.dv + (kvh + key) * D;
 #pragma unroll
@@ -458,14 +618,16 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
         const int d = db * 32 + 8 * r4 + 4 * h;
-        const u32x2 wk = {(uint32_t)to_bf16_bits(dk_acc[db][4 * r4 + 0] * a.scale) |
-                              ((uint32_t)to_bf16_bits(dk_acc[db][4 * r4 + 1] * a.scale) << 16),
-                          (uint32_t)to_bf16_bits(dk_acc[db][4 * r4 + 2] * a.scale) |
-                              ((uint32_t)to_bf16_bits(dk_acc[db][4 * r4 + 3] * a.scale) << 16)};
-        const u32x2 wv = {(uint32_t)to_bf16_bits(dv_acc[db][4 * r4 + 0]) |
-                              ((uint32_t)to_bf16_bits(dv_acc[db][4 * r4 + 1]) << 16),
-                          (uint32_t)to_bf16_bits(dv_acc[db][4 * r4 + 2]) |
-                              ((uint32_t)to_bf16_bits(dv_acc[db][4 * r4 + 3]) << 16)};
+        float xk[4], xv[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          xk[e] = kvalid ? dk_acc[db][4 * r4 + e] * a.scale : 0.f;
+          xv[e] = kvalid ? dv_acc[db][4 * r4 + e] : 0.f;
+        }
+        const u32x2 wk = {(uint32_t)to_bf16_bits(xk[0]) | ((uint32_t)to_bf16_bits(xk[1]) << 16),
+                          (uint32_t)to_bf16_bits(xk[2]) | ((uint32_t)to_bf16_bits(xk[3]) << 16)};
+        const u32x2 wv = {(uint32_t)to_bf16_bits(xv[0]) | ((uint32_t)to_bf16_bits(xv[1]) << 16),
+                          (uint32_t)to_bf16_bits(xv[2]) | ((uint32_t)to_bf16_bits(xv[3]) << 16)};
         *reinterpret_cast<u32x2*>(dkr + d) = wk;
         *reinterpret_cast<u32x2*>(dvr + d) = wv;
       }

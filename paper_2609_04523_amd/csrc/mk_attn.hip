@@ -268,9 +268,15 @@ int mk_attn_decode_paged(const void* q, const void* k_pages, const void* v_pages
   return e == hipSuccess ? MK_OK : MK_ERR_HIP;
 }
 
+// Backward workspace: D and LSE log2(e), each [B, Hq, Sq rounded up to
+// 128] fp32, the second at a 256-byte aligned offset.
+size_t bwd_array_bytes(int B, int Hq, int Sq) {
+  return round_up((size_t)B * Hq * round_up((size_t)Sq, 128) * sizeof(float), 256);
+}
+
 size_t mk_attn_bwd_workspace_bytes(int B, int Hq, int Sq) {
   if (B < 1 || Hq < 1 || Sq < 1) return 0;
-  return round_up((size_t)B * Hq * Sq * sizeof(float), 256);
+  return 2 * bwd_array_bytes(B, Hq, Sq);
 }
 
 int mk_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
@@ -289,7 +295,8 @@ int mk_attn_bwd(const void* q, const void* k, const void* v, const void* o, cons
     return MK_ERR_ALIGN;
   if (kv_seqlens && !aligned(kv_seqlens, 4)) return MK_ERR_ALIGN;
   // workgroups of each launch
-  const long long rows = (long long)B * Hq * Sq;
+  const long long sq_pad = (Sq + 127) / 128 * 128;
+  const long long rows = (long long)B * Hq * sq_pad;
   const long long delta_blocks = (rows + 15) / 16;
   const long long dq_blocks = (long long)((Sq + 127) / 128) * B * Hq;
   const long long dkdv_blocks = (long long)((Skv + 127) / 128) * B * Hkv;
@@ -310,6 +317,8 @@ int mk_attn_bwd(const void* q, const void* k, const void* v, const void* o, cons
   a.dk = static_cast<uint16_t*>(dk);
   a.dv = static_cast<uint16_t*>(dv);
   a.delta = static_cast<float*>(workspace);
+  a.lse2 = reinterpret_cast<float*>(static_cast<char*>(workspace) + bwd_array_bytes(B, Hq, Sq));
+  a.sq_pad = (int)sq_pad;
   a.kv_seqlens = kv_seqlens;
   a.B = B;
   a.Hq = Hq;

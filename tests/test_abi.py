@@ -221,8 +221,10 @@ def bwd_rc(lib, *, q=P, k=P, v=P, o=P, do=P, lse=P, dq=P, dk=P, dv=P, B=2, Hq=8,
 
 
 def test_bwd_workspace_bytes(lib):
-    assert lib.mk_attn_bwd_workspace_bytes(2, 8, 100) == 6400  # 1600 fp32, 256-aligned
-    assert lib.mk_attn_bwd_workspace_bytes(1, 1, 1) == 256
+    # two arrays of B * Hq * round_up(Sq, 128) fp32, each 256-byte aligned
+    assert lib.mk_attn_bwd_workspace_bytes(2, 8, 100) == 2 * 2 * 8 * 128 * 4
+    assert lib.mk_attn_bwd_workspace_bytes(1, 1, 1) == 2 * 512
+    assert lib.mk_attn_bwd_workspace_bytes(1, 3, 130) == 2 * 3 * 256 * 4
     assert lib.mk_attn_bwd_workspace_bytes(0, 8, 100) == 0
     assert lib.mk_attn_bwd_workspace_bytes(2, 8, -1) == 0
 
