@@ -165,6 +165,8 @@ def main():
                     help="page size of the paged-decode leg (0 skips the leg)")
     ap.add_argument("--no-varlen", action="store_true",
                     help="skip the packed ragged prefill leg")
+    ap.add_argument("--no-bwd", action="store_true",
+                    help="skip the backward leg (dQ, dK, dV on the prefill shape)")
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="query rows per head timed for the CPU oracle baseline (0: all)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -246,6 +248,20 @@ def main():
                                             extra_pages=64)
         paged = [(kp.to(dev), vp.to(dev), bt.to(dev)) for _ in range(2)]
         del kp, vp, bt
+    bwd = []
+    if not args.no_bwd:
+        # backward on the prefill shape: the forward's bf16 O and LSE
+        # (computed once, untimed), a seeded dO, two input copies
+        gb = torch.Generator().manual_seed(pcfg.seed + 11)
+        dout = torch.randn((pcfg.B, pcfg.Hq, pcfg.S, pcfg.D), generator=gb).to(torch.bfloat16)
+        bws_bytes = mk.mk_attn_bwd_workspace_bytes(pcfg.B, pcfg.Hq, pcfg.S)
+        for i in range(2):
+            q_, k_, v_ = pre[i][:3]
+            o_, lse_ = mk.fwd(q_, k_, v_, causal=pcfg.causal, scale=pcfg.scale)
+            bwd.append((q_, k_, v_, o_, lse_, dout.to(dev), torch.empty_like(q_),
+                        torch.empty_like(k_), torch.empty_like(v_),
+                        torch.empty(bws_bytes, device=dev, dtype=torch.uint8)))
+        del dout
     del kc, vc
     qd = qd.to(dev)
     lens_d = lens.to(dev)
@@ -275,6 +291,12 @@ def main():
         mk.mk_attn_fwd_varlen(vq_, vk_, vv_, vo_, vl_, vcu_, vcu_, VL["B"], VL["Hq"], VL["Hkv"],
                               max(vlens), vq_.shape[0], vk_.shape[0], VL["D"], 1,
                               VL["D"] ** -0.5, stream)
+
+    def backward(i):
+        q_, k_, v_, o_, lse_, do_, dq_, dk_, dv_, bws_ = bwd[i & 1]
+        mk.mk_attn_bwd(q_, k_, v_, o_, do_, lse_, dq_, dk_, dv_, pcfg.B, pcfg.Hq, pcfg.Hkv,
+                       pcfg.S, pcfg.S, pcfg.D, int(pcfg.causal), pcfg.scale, None, bws_,
+                       bws_.numel(), stream)
 
     def decode_paged(i):
         kp_, vp_, bt_ = paged[i & 1]
@@ -343,6 +365,19 @@ def main():
         evp[1].record(stream)
         torch.cuda.synchronize()
         paged_ms = evp[0].elapsed_time(evp[1]) / K
+    bwd_ms = None
+    if bwd:
+        # the backward leg, timed after the step the same way
+        for i in range(args.warmup):
+            backward(i)
+        evb = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        evb[0].record(stream)
+        for i in range(K):
+            backward(i)
+        evb[1].record(stream)
+        torch.cuda.synchronize()
+        bwd_ms = evb[0].elapsed_time(evb[1]) / K
     ms_step = (t1 - t0) * 1e3 / K
     pre_ms = ev[0].elapsed_time(ev[1]) / K  # average launch duration
     dec_ms = ev[1].elapsed_time(ev[2]) / K
@@ -354,7 +389,8 @@ def main():
     log(f"[bench] prefill {pre_ms * 1e3:.1f} us ({tflops:.1f} TFLOP/s), "
         f"decode {dec_ms * 1e3:.1f} us ({dec_gbs:.1f} GB/s), step {ms_step:.3f} ms"
         + (f", varlen prefill {varlen_ms * 1e3:.1f} us" if varlen_ms is not None else "")
-        + (f", paged decode {paged_ms * 1e3:.1f} us" if paged_ms is not None else ""))
+        + (f", paged decode {paged_ms * 1e3:.1f} us" if paged_ms is not None else "")
+        + (f", backward {bwd_ms * 1e3:.1f} us" if bwd_ms is not None else ""))
 
     digest = kernel_source_digest()
     traffic_pre = read_traffic(f"fwd_kernel_{pcfg.name}_counters.md", digest)
@@ -434,6 +470,25 @@ def main():
             "us": round(paged_ms * 1e3, 2),
             "roofline": {"bound": "hbm", "achieved": round(p_gbs, 1), "peak": PEAK_HBM_GBS,
                          "unit": "GB/s", "frac": round(p_gbs / PEAK_HBM_GBS, 4),
+                         "traffic": None},
+        }
+
+    if bwd_ms is not None:
+        # the usual convention for attention backward: 2.5 times the
+        # forward's FLOPs (five products of the forward's size: S, dP, dV,
+        # dK, dQ); the dQ kernel recomputes S and dP, which is not counted
+        b_flops = 5 * pcfg.flops // 2
+        b_tf = b_flops / (bwd_ms * 1e-3) / 1e12
+        result["backward"] = {
+            "workload": (f"{pcfg.name} backward: dQ, dK, dV from O, LSE and a seeded dO, "
+                         f"{'causal' if pcfg.causal else 'non-causal'} B={pcfg.B} Hq={pcfg.Hq} "
+                         f"Hkv={pcfg.Hkv} S={pcfg.S} D={pcfg.D} bf16"),
+            "value": round(b_tf, 2),
+            "unit": "TFLOP/s",
+            "us": round(bwd_ms * 1e3, 2),
+            "flops": b_flops,
+            "roofline": {"bound": "mfma", "achieved": round(b_tf, 2), "peak": PEAK_BF16_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(b_tf / PEAK_BF16_TFLOPS, 4),
                          "traffic": None},
         }
 

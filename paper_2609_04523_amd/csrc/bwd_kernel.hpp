@@ -299,7 +299,7 @@ struct DkdvShape {
   static constexpr int BLOCKS_PER_WAVE = TILE_BYTES / 1024 / WAVES;  // per tensor
   static constexpr int ROW_STEP = WAVES * ROWS_PER_KB;
   static constexpr int RL_BYTES = 2 * BQ * 4;  // lse2 row, then D row, per buffer
-  static constexpr int RW = 4;                 // LDS reads kept in flight
+  static constexpr int RW = 8;                 // LDS reads kept in flight
 };
 
 template <int D, bool CAUSAL>
