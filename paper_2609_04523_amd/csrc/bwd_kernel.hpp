@@ -98,6 +98,41 @@ __device__ __forceinline__ float bwd_prob(float s, float c, float lse2, bool val
   return valid ? p : 0.f;
 }
 
+// Store x * acc^T as 32 bf16 rows of D values: acc[db][r] of lane
+// (n, h) = l % 32, l / 32 is element (row n, column db*32 + 8 (r/4) + 4 h
+// + r % 4).  The wave writes its rows to LDS at `stage` (32 rows x D bf16,
+// 16-byte chunks XOR-swizzled by row), then stores them 16 bytes per lane,
+// 16 (D = 128) or 8 (D = 64) lanes per row; rows >= n_rows are not stored.
+template <int D>
+__device__ __forceinline__ void store_rows_t(const f32x16 (&acc)[D / 32], float x,
+                                             uint32_t stage, int n, int h, int lane,
+                                             uint16_t* dst, int n_rows) {
+  constexpr int CH = D / 8;  // 16-byte chunks per row
+  constexpr int ROW_BYTES = D * 2;
+  const int swz_w = n & (CH - 1);
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const int c = db * 4 + r4;
+      const u32x2 w = {(uint32_t)to_bf16_bits(acc[db][4 * r4] * x) |
+                           ((uint32_t)to_bf16_bits(acc[db][4 * r4 + 1] * x) << 16),
+                       (uint32_t)to_bf16_bits(acc[db][4 * r4 + 2] * x) |
+                           ((uint32_t)to_bf16_bits(acc[db][4 * r4 + 3] * x) << 16)};
+      const uint32_t ad = stage + n * ROW_BYTES + ((c ^ swz_w) << 4) + 8 * h;
+      *(__attribute__((address_space(3))) u32x2*)(uintptr_t)ad = w;
+    }
+  constexpr int ROWS_PER_READ = 64 / CH;
+#pragma unroll
+  for (int i = 0; i < 32 / ROWS_PER_READ; ++i) {
+    const int row = i * ROWS_PER_READ + lane / CH;
+    const int c = lane % CH;
+    const uint32_t ad = stage + row * ROW_BYTES + ((c ^ (row & (CH - 1))) << 4);
+    const u32x4 v = *(const __attribute__((address_space(3))) u32x4*)(uintptr_t)ad;
+    if (row < n_rows) *reinterpret_cast<u32x4*>(dst + (size_t)row * D + c * 8) = v;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // dQ: workgroup = 4 waves x 32 query rows of one (b, hq); 64-key K/V tiles.
 // ---------------------------------------------------------------------------
@@ -255,40 +290,14 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
     if (kt + 2 < n_kt) issue_tile(kt + 2, buf);
   }
 
-  // dQ = scale * acc^T: lane (query n, k-group h) holds head dims
-  // db*32 + 8 (r/4) + 4 h + r % 4
-  if (row_ok) {
-    uint16_t* dst = a.dq + (row0 + qrow) * D;
-#pragma unroll
-    for (int db = 0; db < DBLK; ++db)
-#pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const int d = db * 32 + 8 * r4 + 4 * h;
-        const u32x2 w = {(uint32_t)to_bf16_bits(acc[db][4 * r4 + 0] * a.scale) |
-                             ((uint32_t)to_bf16_bits(acc[db][4 * r4 + 1] * a.scale) << 16),
-                         (uint32_t)to_bf16_bits(acc[db][4 * r4 + 2] * a.scale) |
-                             ((uint32_t)to_bf16_bits(acc[db][4 * r4 + 3] * a.scale) << 16)};
-        *reinterpret_cast<u32x2*>(dst + d) = w;
-      }
-  }
+  // dQ = scale * acc^T (lane (query n, k-group h) holds head dims
+  // db*32 + 8 (r/4) + 4 h + r % 4), staged through the K buffers so that
+  // the stores are whole rows
+  __syncthreads();
+  store_rows_t<D>(acc, a.scale, k0 + wave * 32 * ROW_BYTES, n, h, lane,
+                  a.dq + (row0 + q0 + wave * 32) * D, a.Sq - (q0 + wave * 32));
 }
 
-// ---------------------------------------------------------------------------
-// dK, dV: workgroup = 4 waves x 32 keys of one (b, kv head).  The tiles of
-// 64 query rows of every query head of the group that see a key of the
-// block stream through LDS (NBUF-deep ring of Q, dO and their LSE log2 e
-// and D rows); each wave keeps its keys' K and V in registers and its
-// dK^T, dV^T accumulators in accumulation registers.
-//
-// Per 32-row chunk c of a tile, with S = Q K^T and dP = dO V^T:
-//   A(c):  S(c), dP(c) on the matrix cores (Q, dO fragments from LDS);
-//   B(c):  P = 2^(S c - lse2), dS = P (dP - D) on the vector ALU, as bf16;
-//   C(c):  dV^T += dO^T P, dK^T += Q^T dS (transposing LDS reads).
-// The steps are software-pipelined one chunk deep: A(c + 1) runs on the
-// matrix cores while the vector ALU forms B(c), then C(c) follows, so the
-// exponentials cost no matrix-core time.  LDS reads are issued as inline
-// assembly a few ahead of their use, and waited for by count.
-// ---------------------------------------------------------------------------
 template <int D>
 struct DkdvShape {
   static constexpr int WAVES = 4, BK = 128, BQ = 64, NBUF = 4;
@@ -313,11 +322,19 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 31, h = lane >> 5;
-  // key blocks in ascending order: under the causal mask the first blocks
-  // are seen by the most query rows
-  const int per = a.B * a.Hkv;
-  const int kblk = blockIdx.x / per;
-  const int rem = blockIdx.x - kblk * per;
+  // Workgroup order: groups of GS (batch, kv head) pairs, about as many
+  // key blocks as run at once (256 compute units, one workgroup each), so
+  // the key blocks that read the same Q and dO rows run together; within a
+  // group key blocks ascend (under the causal mask the first blocks are
+  // seen by the most query rows), and the pairs of a group alternate, so
+  // that pair j stays on one XCD (launch order i goes to XCD i % 8).
+  const int BH = a.B * a.Hkv, nkb = a.n_kblocks;
+  const int GS = max(8, 256 / nkb / 8 * 8);
+  const int grp = blockIdx.x / (GS * nkb);
+  const int in_grp = blockIdx.x - grp * GS * nkb;
+  const int gs = min(GS, BH - grp * GS);
+  const int kblk = in_grp / gs;
+  const int rem = grp * GS + (in_grp - kblk * gs);
   const int b = rem / a.Hkv, g = rem - (rem / a.Hkv) * a.Hkv;
   const int G = a.Hq / a.Hkv;
   const int L = a.kv_seqlens ? clamp_len(a.kv_seqlens[b], a.Skv) : a.Skv;
@@ -352,51 +369,49 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   }
 
   // ---- tile loads: Q and dO rows of tile `it` into ring buffer `buf`
-  // (rows past Sq repeat row Sq - 1; their lse2 = +inf zeroes them), the
-  // lse2 row by wave 0 and the D row by wave 1 (one dword per lane) ----
+  // (rows past Sq repeat row Sq - 1; their lse2 = +inf zeroes them), and
+  // the lse2 row (even waves) or the D row (odd waves, the same bytes
+  // twice), one dword per lane.  Tiles past the last are clamped to it, so
+  // every wave issues the same loads every tile and no branch is needed.
   const int dma_row = wave * S::ROWS_PER_KB + lane / S::CHUNKS;
   const int dma_ch = ((lane % S::CHUNKS) ^ fwd_swz<D>(dma_row)) * 16;
   const uint32_t qd_base = lds_addr(&qd_lds[0]);
   const uint32_t rl_base = lds_addr(&rl_lds[0]);
   const uint32_t qd_w = __builtin_amdgcn_readfirstlane(qd_base + wave * 1024);
-  auto issue_tile = [&](int it, int buf) {
+  struct TileSrc {
+    const char* qg;
+    const char* dg;
+    const float* rows;
+    int tlim;  // last valid row of the tile
+    uint32_t lbuf, rdst;
+  };
+  auto tile_src = [&](int it, int buf) {
+    it = min(it, n_it - 1);
     const int hq = g * G + it / n_qt;
     const int q0 = (qt_first + it % n_qt) * BQ;
     const size_t row0 = ((size_t)b * a.Hq + hq) * (size_t)a.Sq;
-    const int tlim = a.Sq - 1 - q0;  // last valid row of the tile
-    const char* qg = reinterpret_cast<const char*>(a.q + (row0 + q0) * D);
-    const char* dg = reinterpret_cast<const char*>(a.dout + (row0 + q0) * D);
-    const uint32_t lbuf = qd_w + buf * S::BUF_BYTES;
-#pragma unroll
-    for (int p = 0; p < S::BLOCKS_PER_WAVE; ++p) {
-      const uint32_t goff = (uint32_t)(min(dma_row + p * S::ROW_STEP, tlim) * ROW_BYTES + dma_ch);
-      load_lds16_at(qg + goff, lbuf + p * S::WAVES * 1024);
-      load_lds16_at(dg + goff, lbuf + TILE_BYTES + p * S::WAVES * 1024);
-    }
-    if (wave < 2) {
-      const size_t prow = ((size_t)b * a.Hq + hq) * (size_t)a.sq_pad + q0 + lane;
-      const float* src = (wave == 0 ? a.lse2 : a.delta) + prow;
-      const uint32_t dst =
-          __builtin_amdgcn_readfirstlane(rl_base + buf * S::RL_BYTES + wave * BQ * 4);
-      __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
-                                       (void __attribute__((address_space(3)))*)(uintptr_t)dst,
-                                       4, 0, 0);
-    }
+    const size_t prow = ((size_t)b * a.Hq + hq) * (size_t)a.sq_pad + q0;
+    TileSrc t;
+    t.qg = reinterpret_cast<const char*>(a.q + (row0 + q0) * D);
+    t.dg = reinterpret_cast<const char*>(a.dout + (row0 + q0) * D);
+    t.rows = ((wave & 1) ? a.delta : a.lse2) + prow;
+    t.tlim = a.Sq - 1 - q0;
+    t.lbuf = qd_w + buf * S::BUF_BYTES;
+    t.rdst = __builtin_amdgcn_readfirstlane(rl_base + buf * S::RL_BYTES + (wave & 1) * BQ * 4);
+    return t;
   };
-  // s_waitcnt vmcnt: at most k tiles' loads issued after the one waited for
-  // remain outstanding (waves 0 and 1 issue one more load per tile)
-  constexpr int LPT = 2 * S::BLOCKS_PER_WAVE;
-  auto wait_tiles = [&](int k) {
-    if (wave < 2) {
-      if (k >= 2) wait_vmcnt<2 * (LPT + 1)>();
-      else if (k == 1) wait_vmcnt<LPT + 1>();
-      else wait_vmcnt<0>();
-    } else {
-      if (k >= 2) wait_vmcnt<2 * LPT>();
-      else if (k == 1) wait_vmcnt<LPT>();
-      else wait_vmcnt<0>();
-    }
+  auto issue_block = [&](const TileSrc& t, int p) {
+    const uint32_t goff = (uint32_t)(min(dma_row + p * S::ROW_STEP, t.tlim) * ROW_BYTES + dma_ch);
+    load_lds16_at(t.qg + goff, t.lbuf + p * S::WAVES * 1024);
+    load_lds16_at(t.dg + goff, t.lbuf + TILE_BYTES + p * S::WAVES * 1024);
   };
+  auto issue_rows = [&](const TileSrc& t) {
+    __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)(t.rows + lane),
+                                     (void __attribute__((address_space(3)))*)(uintptr_t)t.rdst,
+                                     4, 0, 0);
+  };
+  // vector-memory operations per tile and wave
+  constexpr int LPT = 2 * S::BLOCKS_PER_WAVE + 1;
 
   // ---- LDS read addresses (the ring buffer's offset is folded in and
   // moved on per tile) ----
@@ -440,7 +455,9 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   // at) with B(chunk BCH) on the vector ALU in between, then C(chunk BCH),
   // then the lse2 / D reads for chunk LCH (read by the next step's B).  -1:
   // no such part.  Elements with diag > 8 (r/4) + r % 4 are masked.
-  auto step = [&](auto ach_tag, auto bch_tag, auto lch_tag) {
+  // mid() runs between A and C (while C's first reads are in flight), and
+  // dma(M) after C's M-th pair of products.
+  auto step = [&](auto ach_tag, auto bch_tag, auto lch_tag, auto&& mid, auto&& dma) {
     constexpr int ACH = decltype(ach_tag)::value;
     constexpr int BCH = decltype(bch_tag)::value;
     constexpr int LCH = decltype(lch_tag)::value;
@@ -526,6 +543,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
       __builtin_amdgcn_sched_barrier(0);
     }
 
+    mid();
+
     if constexpr (NC > 0) {
       static_for<0, 2 * DBLK>([&](auto m_tag) {
         constexpr int M = decltype(m_tag)::value;  // (kc, db) = (M / DBLK, M % DBLK)
@@ -548,6 +567,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
         static_for<0, 4>([&](auto e_tag) {
           issue(std::integral_constant<int, BASE + RS + decltype(e_tag)::value>());
         });
+        dma(m_tag);
         __builtin_amdgcn_sched_barrier(0);
       });
     }
@@ -559,13 +579,23 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   using C0 = std::integral_constant<int, 0>;
   using C1 = std::integral_constant<int, 1>;
 
+  auto none = [&]() {};
+  auto no_dma = [&](auto) {};
   if (n_it > 0) {
-    for (int i = 0; i < NBUF - 1 && i < n_it; ++i) issue_tile(i, i);
-    wait_tiles(min(n_it, NBUF - 1) - 1);
+    static_for<0, NBUF - 1>([&](auto i_tag) {
+      constexpr int I = decltype(i_tag)::value;
+      const TileSrc t = tile_src(I, I);
+      static_for<0, S::BLOCKS_PER_WAVE>([&](auto p_tag) { issue_block(t, p_tag); });
+      issue_rows(t);
+    });
+    wait_vmcnt<(NBUF - 2) * LPT>();  // tile 0
     __syncthreads();
-    step(C0(), N1(), C0());  // A(tile 0, chunk 0), lse2 / D of chunk 0
+    step(C0(), N1(), C0(), none, no_dma);  // A(tile 0, chunk 0), lse2 / D of chunk 0
   }
   const uint32_t ring = NBUF * S::BUF_BYTES;
+  // C's pairs of products between two Q / dO blocks of the next load
+  constexpr int PAIRS_PER_BLOCK = 2 * DBLK / S::BLOCKS_PER_WAVE;
+  static_assert(PAIRS_PER_BLOCK >= 2 && 2 * DBLK % S::BLOCKS_PER_WAVE == 0, "load spacing");
   for (int it = 0; it < n_it; ++it) {
     const int buf = it % NBUF;
     // ring offset from this tile's buffer to the next one's
@@ -576,20 +606,28 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
     const bool m1 = CAUSAL && q0 + 32 + off < kw0 + 31;
 
     // chunk 0: A(chunk 1) with B(chunk 0), C(chunk 0), rows of chunk 1.
+    // Between A and C: tile it + 1 must have landed, and every wave must be
+    // done with tile it - 1, whose buffer then takes tile it + NBUF - 1
+    // (loaded during C; C's reads of tile it are already in flight).
     // The loop body has no branch around the steps: a branch would make
     // the compiler move the accumulators between register files at every
     // product.  So the mask is always applied (an unmasked chunk gets a
-    // threshold every element passes), and the last tile's second step
-    // also forms A of a tile that does not exist (in-bounds reads of a
-    // stale ring buffer, never used).
+    // threshold every element passes), tiles past the last are loaded
+    // clamped, and the last tile's second step also forms A of a tile that
+    // does not exist (in-bounds reads of a stale ring buffer, never used).
     diag = m0 ? key - off - q0 - 4 * h : -0x40000000;
-    step(C1(), C0(), C1());
-
-    // tile it + 1 must have landed; every wave is done with tile it - 1,
-    // whose buffer takes tile it + NBUF - 1
-    wait_tiles(it + 2 < n_it ? 1 : 0);
-    __syncthreads();
-    if (it + NBUF - 1 < n_it) issue_tile(it + NBUF - 1, (it + NBUF - 1) % NBUF);
+    TileSrc nxt;
+    auto mid = [&]() {
+      wait_vmcnt<LPT>();
+      __syncthreads();
+      nxt = tile_src(it + NBUF - 1, (it + NBUF - 1) % NBUF);
+    };
+    auto dma = [&](auto m_tag) {
+      constexpr int M = decltype(m_tag)::value;
+      if constexpr (M % PAIRS_PER_BLOCK == 0) issue_block(nxt, M / PAIRS_PER_BLOCK);
+      if constexpr (M == 1) issue_rows(nxt);
+    };
+    step(C1(), C0(), C1(), mid, dma);
 #pragma unroll
     for (int s = 0; s < KSTEPS; ++s) qa[s] += adv;
     la += adv_rl;
@@ -597,7 +635,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
     // chunk 1: A(next tile, chunk 0) with B(chunk 1), C(chunk 1), rows of
     // the next tile's chunk 0
     diag = m1 ? key - off - q0 - 32 - 4 * h : -0x40000000;
-    step(C0(), C1(), C0());
+    step(C0(), C1(), C0(), none, no_dma);
     // the transposing reads move on once C of chunk 1 is done
 #pragma unroll
     for (int db = 0; db < DBLK; ++db) {
@@ -605,33 +643,19 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
       qt[db][1] += adv;
     }
   }
+  wait_vmcnt<0>();  // loads of clamped tiles past the last
 
-  // dK = scale * dk_acc^T, dV = dv_acc^T: lane (key n, k-group h) holds
-  // head dims db*32 + 8 (r/4) + 4 h + r % 4 of its key; keys past the
-  // sequence get zeros
-  if (key < a.Skv) {
-    const bool kvalid = key < L;
-    uint16_t* dkr = a.dk + (kvh + key) * D;
-    uint16_t* dvr = a.dv + (kvh + key) * D;
-#pragma unroll
-    for (int db = 0; db < DBLK; ++db)
-#pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const int d = db * 32 + 8 * r4 + 4 * h;
-        float xk[4], xv[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          xk[e] = kvalid ? dk_acc[db][4 * r4 + e] * a.scale : 0.f;
-          xv[e] = kvalid ? dv_acc[db][4 * r4 + e] : 0.f;
-        }
-        const u32x2 wk = {(uint32_t)to_bf16_bits(xk[0]) | ((uint32_t)to_bf16_bits(xk[1]) << 16),
-                          (uint32_t)to_bf16_bits(xk[2]) | ((uint32_t)to_bf16_bits(xk[3]) << 16)};
-        const u32x2 wv = {(uint32_t)to_bf16_bits(xv[0]) | ((uint32_t)to_bf16_bits(xv[1]) << 16),
-                          (uint32_t)to_bf16_bits(xv[2]) | ((uint32_t)to_bf16_bits(xv[3]) << 16)};
-        *reinterpret_cast<u32x2*>(dkr + d) = wk;
-        *reinterpret_cast<u32x2*>(dvr + d) = wv;
-      }
-  }
+  // dK = scale * dk_acc^T, dV = dv_acc^T, staged through LDS so that the
+  // stores are whole rows: lane (key n, k-group h) holds head dims
+  // db*32 + 8 (r/4) + 4 h + r % 4 of its key; keys past the sequence get
+  // zeros.  The ring is free once every wave is past its last read.
+  __syncthreads();
+  const uint32_t stage = qd_base + wave * 2 * 32 * ROW_BYTES;
+  const bool kvalid = key < L;
+  store_rows_t<D>(dk_acc, kvalid ? a.scale : 0.f, stage, n, h, lane,
+                  a.dk + (kvh + kw0) * D, a.Skv - kw0);
+  store_rows_t<D>(dv_acc, kvalid ? 1.f : 0.f, stage + 32 * ROW_BYTES, n, h, lane,
+                  a.dv + (kvh + kw0) * D, a.Skv - kw0);
 }
 
 }  // namespace mk
