@@ -98,41 +98,6 @@ __device__ __forceinline__ float bwd_prob(float s, float c, float lse2, bool val
   return valid ? p : 0.f;
 }
 
-// Store x * acc^T as 32 bf16 rows of D values: acc[db][r] of lane
-// (n, h) = l % 32, l / 32 is element (row n, column db*32 + 8 (r/4) + 4 h
-// + r % 4).  The wave writes its rows to LDS at `stage` (32 rows x D bf16,
-// 16-byte chunks XOR-swizzled by row), then stores them 16 bytes per lane,
-// 16 (D = 128) or 8 (D = 64) lanes per row; rows >= n_rows are not stored.
-template <int D>
-__device__ __forceinline__ void store_rows_t(const f32x16 (&acc)[D / 32], float x,
-                                             uint32_t stage, int n, int h, int lane,
-                                             uint16_t* dst, int n_rows) {
-  constexpr int CH = D / 8;  // 16-byte chunks per row
-  constexpr int ROW_BYTES = D * 2;
-  const int swz_w = n & (CH - 1);
-#pragma unroll
-  for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-    for (int r4 = 0; r4 < 4; ++r4) {
-      const int c = db * 4 + r4;
-      const u32x2 w = {(uint32_t)to_bf16_bits(acc[db][4 * r4] * x) |
-                           ((uint32_t)to_bf16_bits(acc[db][4 * r4 + 1] * x) << 16),
-                       (uint32_t)to_bf16_bits(acc[db][4 * r4 + 2] * x) |
-                           ((uint32_t)to_bf16_bits(acc[db][4 * r4 + 3] * x) << 16)};
-      const uint32_t ad = stage + n * ROW_BYTES + ((c ^ swz_w) << 4) + 8 * h;
-      *(__attribute__((address_space(3))) u32x2*)(uintptr_t)ad = w;
-    }
-  constexpr int ROWS_PER_READ = 64 / CH;
-#pragma unroll
-  for (int i = 0; i < 32 / ROWS_PER_READ; ++i) {
-    const int row = i * ROWS_PER_READ + lane / CH;
-    const int c = lane % CH;
-    const uint32_t ad = stage + row * ROW_BYTES + ((c ^ (row & (CH - 1))) << 4);
-    const u32x4 v = *(const __attribute__((address_space(3))) u32x4*)(uintptr_t)ad;
-    if (row < n_rows) *reinterpret_cast<u32x4*>(dst + (size_t)row * D + c * 8) = v;
-  }
-}
-
 // ---------------------------------------------------------------------------
 // dQ: workgroup = 4 waves x 32 query rows of one (b, hq); 64-key K/V tiles.
 // ---------------------------------------------------------------------------
@@ -295,7 +260,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
   // the stores are whole rows
   __syncthreads();
   store_rows_t<D>(acc, a.scale, k0 + wave * 32 * ROW_BYTES, n, h, lane,
-                  a.dq + (row0 + q0 + wave * 32) * D, a.Sq - (q0 + wave * 32));
+                  a.dq + (row0 + q0 + wave * 32) * D, D, a.Sq - (q0 + wave * 32));
 }
 
 template <int D>
@@ -653,9 +618,9 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   const uint32_t stage = qd_base + wave * 2 * 32 * ROW_BYTES;
   const bool kvalid = key < L;
   store_rows_t<D>(dk_acc, kvalid ? a.scale : 0.f, stage, n, h, lane,
-                  a.dk + (kvh + kw0) * D, a.Skv - kw0);
+                  a.dk + (kvh + kw0) * D, D, a.Skv - kw0);
   store_rows_t<D>(dv_acc, kvalid ? 1.f : 0.f, stage + 32 * ROW_BYTES, n, h, lane,
-                  a.dv + (kvh + kw0) * D, a.Skv - kw0);
+                  a.dv + (kvh + kw0) * D, D, a.Skv - kw0);
 }
 
 }  // namespace mk

@@ -532,32 +532,33 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
     }
   }
 
-  // ---- epilogue: O = O_acc / l, LSE = ln 2 * (m + log2 l) ----
+  // ---- epilogue: O = O_acc / l, LSE = ln 2 * (m + log2 l).  bf16 O is
+  // staged through the (now free) K buffers so that the stores are whole
+  // rows; fp32 O goes out 16 bytes per lane directly. ----
+  if constexpr (!OUT_F32) __syncthreads();
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int qrow = qw0 + qb * 32 + n;
     const float lsum = sum_xor32(l_run[qb]);
-    if (qrow >= Sq) continue;
     const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
-    const size_t obase = o_base + qrow * q_stride;
+    if constexpr (!OUT_F32) {
+      store_rows_t<D>(o_acc[qb], inv, lds_addr(&k_lds[0][0]) + wave * 32 * ROW_BYTES, n, h,
+                      lane, static_cast<uint16_t*>(a.o) + o_base + (qw0 + qb * 32) * q_stride,
+                      q_stride, Sq - (qw0 + qb * 32));
+    }
+    if (qrow >= Sq) continue;
+    if constexpr (OUT_F32) {
+      const size_t obase = o_base + qrow * q_stride;
 #pragma unroll
-    for (int db = 0; db < S::DBLK; ++db)
+      for (int db = 0; db < S::DBLK; ++db)
 #pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const int d = db * 32 + 8 * r4 + 4 * h;
-        const float v0 = o_acc[qb][db][4 * r4 + 0] * inv;
-        const float v1 = o_acc[qb][db][4 * r4 + 1] * inv;
-        const float v2 = o_acc[qb][db][4 * r4 + 2] * inv;
-        const float v3 = o_acc[qb][db][4 * r4 + 3] * inv;
-        if (OUT_F32) {
-          const f32x4 w = {v0, v1, v2, v3};
+        for (int r4 = 0; r4 < 4; ++r4) {
+          const int d = db * 32 + 8 * r4 + 4 * h;
+          const f32x4 w = {o_acc[qb][db][4 * r4 + 0] * inv, o_acc[qb][db][4 * r4 + 1] * inv,
+                           o_acc[qb][db][4 * r4 + 2] * inv, o_acc[qb][db][4 * r4 + 3] * inv};
           *reinterpret_cast<f32x4*>(static_cast<float*>(a.o) + obase + d) = w;
-        } else {
-          const u32x2 w = {(uint32_t)to_bf16_bits(v0) | ((uint32_t)to_bf16_bits(v1) << 16),
-                           (uint32_t)to_bf16_bits(v2) | ((uint32_t)to_bf16_bits(v3) << 16)};
-          *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(a.o) + obase + d) = w;
         }
-      }
+    }
     if (h == 0 && lse_base)
       lse_base[qrow] = lsum > 0.f ? (m_run[qb] + log2f(lsum)) * kLn2 : kNegInf;
   }
