@@ -77,3 +77,27 @@ def attention_f(q, k, v, *, causal: bool, scale: float, kv_seqlens=None):
                                for d in range(D)]
                 lse[b][hq][i] = math.log(z)
     return o, lse
+
+
+def mla_decode(q, ckv, kv_seqlens, *, Dc: int, scale: float):
+    """MLA decode by brute force.  q: nested lists [B][H][Dc+Dr] of bf16 bit
+    patterns; ckv: [B][Smax][Dc+Dr].  Scores use every column of the cache
+    row, outputs the first Dc columns.  Returns (o [B][H][Dc], lse [B][H])."""
+    B, H = len(q), len(q[0])
+    Smax = len(ckv[0])
+    o = [[[0.0] * Dc for _ in range(H)] for _ in range(B)]
+    lse = [[0.0] * H for _ in range(B)]
+    for b in range(B):
+        L = max(0, min(Smax, int(kv_seqlens[b])))
+        rows = [[bf16_bits_to_float(x) for x in ckv[b][j]] for j in range(L)]
+        for h in range(H):
+            qv = [bf16_bits_to_float(x) for x in q[b][h]]
+            if L == 0:
+                lse[b][h] = -math.inf
+                continue
+            w = [math.exp(scale * math.fsum(a * c for a, c in zip(qv, row))) for row in rows]
+            z = math.fsum(w)
+            lse[b][h] = math.log(z)
+            for e in range(Dc):
+                o[b][h][e] = math.fsum(w[j] * rows[j][e] for j in range(L)) / z
+    return o, lse

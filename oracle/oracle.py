@@ -72,6 +72,8 @@ def _declare(lib):
     lib.oracle_attn_bwd.argtypes = [_u16p, _u16p, _u16p, _u16p, i, i, i, i, i, i, i, d, _i32p,
                                     _f64p, _f64p, _f64p]
     lib.oracle_attn_bwd.restype = i
+    lib.oracle_mla_decode.argtypes = [_u16p, _u16p, i, i, i, i, i, d, _i32p, _f64p, _f64p]
+    lib.oracle_mla_decode.restype = i
     lib.oracle_version.restype = i
     return lib
 
@@ -271,4 +273,23 @@ def lse_combine(o_part, lse_part, lib=None):
                                 _ptr(o, _f64p), _ptr(lse, _f64p))
     if rc != 0:
         raise ValueError(f"oracle_lse_combine failed ({rc})")
+    return o, lse
+
+
+def mla_decode(q, ckv, kv_seqlens, *, Dc: int, scale: float, lib=None):
+    """MLA decode.  q [B,H,Dc+Dr], ckv [B,Smax,Dc+Dr] (bf16 bits), lengths [B]
+    -> (o [B,H,Dc], lse [B,H]) float64."""
+    lib = lib or load()
+    q, ckv = _u16(q), _u16(ckv)
+    B, H, Dk = q.shape
+    _, Smax, Dk2 = ckv.shape
+    if Dk2 != Dk or not 0 < Dc <= Dk:
+        raise ValueError("q and ckv must share the last dim, Dc within it")
+    sl = _seqlens(kv_seqlens, B)
+    o = np.empty((B, H, Dc), np.float64)
+    lse = np.empty((B, H), np.float64)
+    rc = lib.oracle_mla_decode(_ptr(q, _u16p), _ptr(ckv, _u16p), B, H, Dc, Dk - Dc, Smax,
+                               float(scale), _ptr(sl, _i32p), _ptr(o, _f64p), _ptr(lse, _f64p))
+    if rc != 0:
+        raise ValueError(f"oracle_mla_decode failed ({rc})")
     return o, lse

@@ -3,8 +3,9 @@
  * scaled-dot-product attention (forward), its split-KV decode form,
  * decode over a paged cache (the "Paged Attention" workload of Table 2),
  * the forward over packed variable-length sequences (the ragged batches of
- * the "Ragged Paged Attention" workload of Table 2), and the backward
- * (gradients of the output with respect to q, k and v).
+ * the "Ragged Paged Attention" workload of Table 2), the backward
+ * (gradients of the output with respect to q, k and v), and the decode
+ * step of multi-head latent attention (the "MLA Attention" workload).
  *
  * TEST INFRASTRUCTURE ONLY.  This file is the checker the GPU path is
  * measured against; it is loaded by the test suite, by the smoke check and
@@ -44,7 +45,8 @@
  * equals unsplit, paged decode equals decode on the cache gathered through
  * the block table, a packed ragged batch equals each of its sequences run
  * alone, the backward equals central finite differences of an independent
- * forward) and hand-derived values stored under tests/golden/.
+ * forward, MLA decode equals a decode over the same rows used as K and as
+ * zero-padded V) and hand-derived values stored under tests/golden/.
  *
  * Build: plain C11, no -ffast-math, libm only (gcc -O2 -shared -fPIC).
  */
@@ -636,4 +638,61 @@ int oracle_attn_bwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
     return 0;
 }
 
-int oracle_version(void) { return 4; }
+/* ------------------------------------------------------------------ */
+/* MLA decode: a shared latent cache with a latent and a rotary part    */
+/* ------------------------------------------------------------------ */
+
+/*
+ * One decode step of multi-head latent attention in its absorbed form (the
+ * "MLA Attention" workload of Table 2; the paper gives no shapes).  Every
+ * query head reads the same cache row per key: its first Dc values are the
+ * latent vector, which serves as the value, and the last Dr values the
+ * rotary key part.  The query head carries the matching Dc + Dr values (the
+ * latent part already multiplied into the latent space).  For each b, h:
+ *   L   = clamp(kv_seqlens[b], 0, Smax)
+ *   s_j = scale * sum_{d < Dc+Dr} q[b,h,d] * ckv[b,j,d]        (j < L)
+ *   O[b,h,e] = sum_j softmax(s)_j * ckv[b,j,e]                 (e < Dc)
+ *   LSE[b,h] = log sum_j exp(s_j) ;  L = 0 -> O = 0, LSE = -inf
+ * q [B,H,Dc+Dr], ckv [B,Smax,Dc+Dr] bf16 bits; o [B,H,Dc], lse [B,H] double.
+ */
+int oracle_mla_decode(const uint16_t *q, const uint16_t *ckv, int B, int H,
+                      int Dc, int Dr, int Smax, double scale,
+                      const int32_t *kv_seqlens, double *o, double *lse)
+{
+    if (!q || !ckv || !kv_seqlens || !o || !lse) return -1;
+    if (B < 1 || H < 1 || Dc < 1 || Dr < 0 || Smax < 1) return -2;
+    const int Dk = Dc + Dr;
+    double *s = (double *)malloc(sizeof(double) * (size_t)Smax);
+    if (!s) return -3;
+    for (int b = 0; b < B; ++b) {
+        const int L = clamp_len(kv_seqlens[b], Smax);
+        const uint16_t *cache = ckv + (size_t)b * Smax * Dk;
+        for (int h = 0; h < H; ++h) {
+            const uint16_t *q_row = q + ((size_t)b * H + h) * Dk;
+            double *o_row = o + ((size_t)b * H + h) * Dc;
+            for (int e = 0; e < Dc; ++e) o_row[e] = 0.0;
+            if (L == 0) { lse[(size_t)b * H + h] = -INFINITY; continue; }
+            double m = -INFINITY;
+            for (int j = 0; j < L; ++j) {
+                double dot = 0.0;
+                for (int d = 0; d < Dk; ++d)
+                    dot += bf16_bits_to_double(q_row[d]) *
+                           bf16_bits_to_double(cache[(size_t)j * Dk + d]);
+                s[j] = scale * dot;
+                if (s[j] > m) m = s[j];
+            }
+            double l = 0.0;
+            for (int j = 0; j < L; ++j) { s[j] = exp(s[j] - m); l += s[j]; }
+            for (int j = 0; j < L; ++j) {
+                const double p = s[j] / l;
+                for (int e = 0; e < Dc; ++e)
+                    o_row[e] += p * bf16_bits_to_double(cache[(size_t)j * Dk + e]);
+            }
+            lse[(size_t)b * H + h] = m + log(l);
+        }
+    }
+    free(s);
+    return 0;
+}
+
+int oracle_version(void) { return 5; }

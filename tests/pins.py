@@ -461,9 +461,73 @@ def pin_bwd_gqa_sums_repeated_heads(lib):
     _close(dv, dv2.reshape(B, Hkv, G, S, D).sum(axis=2), 1e-13, "GQA dv = group sum")
 
 
+MLA_CASES = [
+    # B, H, Dc, Dr, Smax, lengths
+    (1, 1, 4, 2, 5, [5]),
+    (2, 3, 8, 4, 7, [7, 3]),
+    (3, 2, 6, 0, 4, [0, 4, 9]),        # no rotary part; an empty and a clamped sequence
+    (2, 4, 16, 8, 6, [-2, 6]),
+]
+
+
+def _mla_inputs(B, H, Dc, Dr, Smax, seed):
+    return _rand((B, H, Dc + Dr), seed), _rand((B, Smax, Dc + Dr), seed + 1)
+
+
+def pin_mla_brute_force(lib):
+    for n, (B, H, Dc, Dr, Smax, lens) in enumerate(MLA_CASES):
+        q, ckv = _mla_inputs(B, H, Dc, Dr, Smax, 300 + 2 * n)
+        scale = 0.6 / math.sqrt(Dc + Dr)
+        o, lse = orc.mla_decode(q, ckv, lens, Dc=Dc, scale=scale, lib=lib)
+        ob, lb = brute.mla_decode(q.tolist(), ckv.tolist(), lens, Dc=Dc, scale=scale)
+        _close(o, np.array(ob), 1e-12, f"MLA brute case {n} O")
+        _close(lse, np.array(lb), 1e-12, f"MLA brute case {n} LSE")
+
+
+def pin_mla_equals_padded_decode(lib):
+    """MLA decode = the plain decode with one kv head whose K rows are the
+    whole cache rows and whose V rows are the same rows with the rotary
+    part zeroed, output truncated to the latent part."""
+    B, H, Dc, Dr, Smax = 3, 8, 32, 16, 20
+    lens = [20, 7, 1]
+    q, ckv = _mla_inputs(B, H, Dc, Dr, Smax, 320)
+    scale = 1.0 / math.sqrt(Dc + Dr)
+    o, lse = orc.mla_decode(q, ckv, lens, Dc=Dc, scale=scale, lib=lib)
+    v = ckv.copy()
+    v[:, :, Dc:] = 0
+    od, ld = orc.decode(q, ckv[:, None], v[:, None], np.array(lens, np.int32), scale=scale,
+                        lib=lib)
+    _close(o, od[:, :, :Dc], 1e-13, "MLA = padded decode O")
+    assert np.all(od[:, :, Dc:] == 0.0)
+    _close(lse, ld, 1e-13, "MLA = padded decode LSE")
+
+
+def pin_mla_single_key_and_rope(lib):
+    B, H, Dc, Dr, Smax = 1, 3, 8, 4, 6
+    q, ckv = _mla_inputs(B, H, Dc, Dr, Smax, 340)
+    o, lse = orc.mla_decode(q, ckv, [1], Dc=Dc, scale=0.4, lib=lib)
+    qf, cf = _f(q), _f(ckv)
+    for h in range(H):
+        assert np.array_equal(o[0, h], cf[0, 0, :Dc]), "one key: O is the latent row"
+        _close(lse[0, h], 0.4 * math.fsum(qf[0, h] * cf[0, 0]), 1e-15, "one key LSE")
+    # with the query's rotary part zero, the cache's rotary part cannot matter
+    q0 = q.copy()
+    q0[:, :, Dc:] = 0
+    ckv2 = ckv.copy()
+    ckv2[:, :, Dc:] = _rand((B, Smax, Dr), 341)
+    a = orc.mla_decode(q0, ckv, [Smax], Dc=Dc, scale=0.4, lib=lib)
+    b = orc.mla_decode(q0, ckv2, [Smax], Dc=Dc, scale=0.4, lib=lib)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    # and with it nonzero, the rotary part enters the scores
+    c = orc.mla_decode(q, ckv2, [Smax], Dc=Dc, scale=0.4, lib=lib)
+    d = orc.mla_decode(q, ckv, [Smax], Dc=Dc, scale=0.4, lib=lib)
+    assert np.abs(c[1] - d[1]).max() > 1e-6
+
+
 ALL_PINS = [pin_golden, pin_brute_force, pin_rows_sum_to_one, pin_equal_value_rows,
             pin_causal_row0, pin_single_key, pin_scale_zero, pin_gqa_equals_repeated_mha,
             pin_decode_equals_last_prefill_row, pin_split_combine, pin_row_subset,
             pin_paged_equals_gathered, pin_paged_table_clamp_and_unused_pages,
             pin_varlen_equals_each_sequence, pin_varlen_gaps_and_clamped_offsets,
-            pin_bwd_finite_differences, pin_bwd_gqa_sums_repeated_heads]
+            pin_bwd_finite_differences, pin_bwd_gqa_sums_repeated_heads,
+            pin_mla_brute_force, pin_mla_equals_padded_decode, pin_mla_single_key_and_rope]

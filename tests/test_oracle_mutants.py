@@ -53,6 +53,16 @@ MUTANTS = {
                        "dv[kv0 + (size_t)j * D + d] += ds *", 1),
     "bwd_dq_from_values": ("dq[qi + d] += scale * ds * bf16_bits_to_double(k[kv0",
                            "dq[qi + d] += scale * ds * bf16_bits_to_double(v[kv0", 1),
+    "mla_rope_not_in_scores": ("for (int d = 0; d < Dk; ++d)\n                    dot +=",
+                               "for (int d = 0; d < Dc; ++d)\n                    dot +=", 1),
+    "mla_value_past_rope": ("o_row[e] += p * bf16_bits_to_double(cache[(size_t)j * Dk + e]);",
+                            "o_row[e] += p * bf16_bits_to_double(cache[(size_t)j * Dk + Dr + e]);", 1),
+    "mla_cache_of_batch_zero": ("const uint16_t *cache = ckv + (size_t)b * Smax * Dk;",
+                                "const uint16_t *cache = ckv;", 1),
+    "mla_scale_dropped": ("s[j] = scale * dot;\n                if (s[j] > m) m = s[j];\n            }\n"
+                          "            double l = 0.0;\n            for (int j = 0; j < L; ++j) { s[j] = exp",
+                          "s[j] = dot;\n                if (s[j] > m) m = s[j];\n            }\n"
+                          "            double l = 0.0;\n            for (int j = 0; j < L; ++j) { s[j] = exp", 1),
     "varlen_key_start_ignored": ("const uint16_t *k_row = k + ((size_t)(k0 + j) * Hkv + g) * D;",
                                  "const uint16_t *k_row = k + ((size_t)(j) * Hkv + g) * D;", 1),
 }
