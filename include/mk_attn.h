@@ -3,8 +3,10 @@
  *
  * The operation is the attention forward of the paper's "Flash Attention"
  * and "GQA Attention" workloads (Table 2; tolerances in Table 4,
- * Appendix A), and the one-token decode step of its "Paged Attention" /
- * "Ragged Paged Attention" family (Table 2) over a contiguous cache:
+ * Appendix A), the one-token decode step of its "Paged Attention" /
+ * "Ragged Paged Attention" family (Table 2) over a contiguous or paged
+ * cache, packed ragged batches, the backward, and the decode step of its
+ * "MLA Attention" workload:
  *
  *   O = softmax(Q K^T * scale + mask) V,   LSE = log(sum_j exp(s_j))
  *
@@ -224,6 +226,37 @@ int mk_attn_bwd(const void *q, const void *k, const void *v, const void *o, cons
  * fp32 (D_i and LSE_i log2 e), each rounded up to 256 bytes; 0 for invalid
  * sizes. */
 size_t mk_attn_bwd_workspace_bytes(int B, int Hq, int Sq);
+
+/*
+ * Decode step of multi-head latent attention in its absorbed form (the
+ * "MLA Attention" workload of Table 2; the paper gives no shapes, this
+ * library builds H = 16 query heads -- one eighth of a 128-head model,
+ * the rest on other GPUs -- with Dc = 512 latent and Dr = 64 rotary
+ * values).  Every head reads the same cache row per key: all Dc + Dr
+ * values enter the score, the first Dc values are the value:
+ *   L_b = clamp(kv_seqlens[b], 0, Smax)
+ *   s_hj = scale * q[b,h,:] . ckv[b,j,:]                  (j < L_b)
+ *   O[b,h,:] = sum_j softmax(s_h)_j ckv[b,j,0:Dc],  LSE[b,h] = log sum_j exp(s_hj)
+ * L_b = 0 gives O = 0 and LSE = -inf.
+ *   q     [B, H, Dc + Dr] bf16 (the latent part already multiplied into
+ *         the latent space)
+ *   ckv   [B, Smax, Dc + Dr] bf16 latent cache (rows past L_b never read)
+ *   o     [B, H, Dc] bf16 (written);  lse [B, H] fp32 or NULL
+ *   kv_seqlens [B] int32, device, required
+ *   n_parts, workspace: as mk_attn_decode (the key stream of all sequences
+ *         is cut into n_parts equal parts; 0 selects one per compute unit);
+ *         size from mk_attn_mla_decode_workspace_bytes().
+ * MK_ERR_UNSUPPORTED unless H = 16, Dc = 512, Dr = 64.  Other errors as
+ * mk_attn_decode.
+ */
+int mk_attn_mla_decode(const void *q, const void *ckv, void *o, float *lse, int B, int H,
+                       int Dc, int Dr, int Smax, float scale, const int *kv_seqlens,
+                       int n_parts, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Bytes of MLA decode workspace: per part two partial outputs [2, H, Dc]
+ * fp32 and their LSEs [2, H] fp32, the two regions 256-byte aligned;
+ * n_parts = 0 selects the default.  Returns 0 for unsupported sizes. */
+size_t mk_attn_mla_decode_workspace_bytes(int H, int Dc, int n_parts);
 
 /* Static string naming a status code ("MK_OK", ...); never NULL. */
 const char *mk_status_str(int status);

@@ -26,6 +26,7 @@ MK_STATUS = {0: "MK_OK", 1: "MK_ERR_NULL", 2: "MK_ERR_SHAPE", 3: "MK_ERR_UNSUPPO
 EXPORTS = ("mk_attn_fwd", "mk_attn_fwd_o32", "mk_attn_fwd_varlen",
            "mk_attn_decode_workspace_bytes", "mk_attn_decode", "mk_attn_decode_paged",
            "mk_attn_decode_default_parts", "mk_attn_bwd", "mk_attn_bwd_workspace_bytes",
+           "mk_attn_mla_decode", "mk_attn_mla_decode_workspace_bytes",
            "mk_status_str", "mk_attn_version")
 
 
@@ -68,6 +69,10 @@ def lib():
         h.mk_attn_bwd.restype = i
         h.mk_attn_bwd_workspace_bytes.argtypes = [i, i, i]
         h.mk_attn_bwd_workspace_bytes.restype = sz
+        h.mk_attn_mla_decode.argtypes = [vp, vp, vp, vp, i, i, i, i, i, f, vp, i, vp, sz, vp]
+        h.mk_attn_mla_decode.restype = i
+        h.mk_attn_mla_decode_workspace_bytes.argtypes = [i, i, i]
+        h.mk_attn_mla_decode_workspace_bytes.restype = sz
         h.mk_status_str.argtypes = [i]
         h.mk_status_str.restype = ctypes.c_char_p
         h.mk_attn_version.argtypes = []
@@ -94,6 +99,10 @@ def mk_attn_decode_workspace_bytes(Hq: int, Hkv: int, D: int, n_parts: int = 0) 
 
 def mk_attn_bwd_workspace_bytes(B: int, Hq: int, Sq: int) -> int:
     return int(lib().mk_attn_bwd_workspace_bytes(B, Hq, Sq))
+
+
+def mk_attn_mla_decode_workspace_bytes(H: int, Dc: int, n_parts: int = 0) -> int:
+    return int(lib().mk_attn_mla_decode_workspace_bytes(H, Dc, n_parts))
 
 
 def _check(rc: int):
@@ -165,6 +174,13 @@ def mk_attn_bwd(q, k, v, o, dout, lse, dq, dk, dv, B, Hq, Hkv, Sq, Skv, D, causa
                              int(workspace_bytes), _stream(stream)))
 
 
+def mk_attn_mla_decode(q, ckv, o, lse, B, H, Dc, Dr, Smax, scale, kv_seqlens, n_parts,
+                       workspace, workspace_bytes, stream=None):
+    _check(lib().mk_attn_mla_decode(_ptr(q), _ptr(ckv), _ptr(o), _ptr(lse), B, H, Dc, Dr, Smax,
+                                    float(scale), _ptr(kv_seqlens), int(n_parts),
+                                    _ptr(workspace), int(workspace_bytes), _stream(stream)))
+
+
 # ---------------------------------------------------------------------------
 # conveniences: allocate outputs with torch, then call the entry points above
 # ---------------------------------------------------------------------------
@@ -223,6 +239,28 @@ def bwd(q, k, v, o, lse, dout, *, causal: bool = True, scale: float | None = Non
     mk_attn_bwd(q, k, v, o, dout, lse, dq, dk, dv, B, Hq, Hkv, Sq, Skv, D, causal, scale,
                 kv_seqlens, workspace, workspace.numel() * workspace.element_size(), stream)
     return dq, dk, dv
+
+
+def mla_decode(q, ckv, kv_seqlens, *, Dc: int = 512, scale: float | None = None,
+               n_parts: int = 0, workspace=None, stream=None):
+    """MLA decode.  q [B,H,Dc+Dr], ckv [B,Smax,Dc+Dr] bf16, kv_seqlens int32 [B]
+    -> (o [B,H,Dc] bf16, lse [B,H] fp32)."""
+    import torch
+    _require(q, "q", torch.bfloat16, 3)
+    _require(ckv, "ckv", torch.bfloat16, 3)
+    _require(kv_seqlens, "kv_seqlens", torch.int32, 1)
+    B, H, Dk = q.shape
+    _, Smax, _ = ckv.shape
+    if scale is None:
+        scale = Dk ** -0.5
+    need = mk_attn_mla_decode_workspace_bytes(H, Dc, n_parts)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), device=q.device, dtype=torch.uint8)
+    o = torch.empty((B, H, Dc), device=q.device, dtype=torch.bfloat16)
+    lse = torch.empty((B, H), device=q.device, dtype=torch.float32)
+    mk_attn_mla_decode(q, ckv, o, lse, B, H, Dc, Dk - Dc, Smax, scale, kv_seqlens, n_parts,
+                       workspace, workspace.numel() * workspace.element_size(), stream)
+    return o, lse
 
 
 def fwd_varlen(q, k, v, cu_seqlens_q, cu_seqlens_k, max_seqlen_q: int, *, causal: bool = True,

@@ -495,7 +495,9 @@ __device__ __forceinline__ float wave_sum(float x) {
 template <int D>
 __global__ __launch_bounds__(256) void dec_merge_kernel(DecArgs a) {
   constexpr int PER_LANE = D / 64;
-  constexpr int CHUNK = 16;  // pieces whose partial outputs are loaded together
+  // pieces whose partial outputs are loaded together (fewer at wide rows,
+  // to bound the registers they take)
+  constexpr int CHUNK = PER_LANE > 2 ? 8 : 16;
   const int lane = threadIdx.x & 63;
   // b * Hq + hq (wave-uniform: scalar registers, scalar loads)
   const int row = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);

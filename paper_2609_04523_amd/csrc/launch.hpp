@@ -1,6 +1,6 @@
 // launch.hpp -- host launchers of the kernel families, each in translation
 // units of its own (fwd_launch_d128.hip, fwd_launch_d64.hip,
-// fwd_varlen_launch.hip, dec_launch.hip, bwd_launch.hip) so that the library compiles in
+// fwd_varlen_launch.hip, dec_launch.hip, bwd_launch.hip, mla_launch.hip) so that the library compiles in
 // parallel.  Arguments are validated by the callers in mk_attn.hip; these
 // only pick the instantiation and enqueue.
 #pragma once
@@ -30,5 +30,9 @@ hipError_t launch_decode(const DecArgs& a, int D, int qblocks, bool paged, hipSt
 // dkdv_blocks is 0), then the dQ kernel.
 hipError_t launch_bwd(const BwdArgs& a, unsigned delta_blocks, unsigned dq_blocks,
                       unsigned dkdv_blocks, int D, bool causal, hipStream_t st);
+
+// MLA decode (q [B, 16, 576], latent cache [B, Smax, 576] in kc, O
+// [B, 16, 512]): the part kernel, then the merge kernel.
+hipError_t launch_mla_decode(const DecArgs& a, hipStream_t st);
 
 }  // namespace mk

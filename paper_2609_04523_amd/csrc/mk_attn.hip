@@ -8,10 +8,11 @@
 
 #include "../../include/mk_attn.h"
 #include "launch.hpp"
+#include "mla_kernel.hpp"
 
 namespace {
 
-constexpr int kVersion = 5;
+constexpr int kVersion = 6;
 constexpr int kComputeUnits = 256;    // MI355X
 constexpr int kLdsPerCu = 160 * 1024; // gfx950
 constexpr int kMaxParts = 1 << 20;    // decode parts per call
@@ -94,6 +95,21 @@ bool dec_layout(int Hq, int Hkv, int D, int n_parts, DecLayout* out) {
   l.o_bytes = (size_t)l.parts * 2 * G * D * sizeof(float);
   l.lse_off = round_up(l.o_bytes, 256);
   l.total = l.lse_off + round_up((size_t)l.parts * 2 * G * sizeof(float), 256);
+  *out = l;
+  return true;
+}
+
+// MLA decode workspace: o_part [P, 2, H, Dc] fp32, then lse_part [P, 2, H]
+// at a 256-byte aligned offset; the default P is one part per compute unit
+// (its four-wave workgroup holds 144 KB of LDS).
+bool mla_layout(int H, int Dc, int n_parts, DecLayout* out) {
+  if (H != mk::MlaShape::H || Dc != mk::MlaShape::DC) return false;
+  if (n_parts < 0 || n_parts > kMaxParts) return false;
+  DecLayout l;
+  l.parts = n_parts == 0 ? kComputeUnits : n_parts;
+  l.o_bytes = (size_t)l.parts * 2 * H * Dc * sizeof(float);
+  l.lse_off = round_up(l.o_bytes, 256);
+  l.total = l.lse_off + round_up((size_t)l.parts * 2 * H * sizeof(float), 256);
   *out = l;
   return true;
 }
@@ -213,6 +229,37 @@ int mk_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o, flo
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool pos = scale > 0.f;
   const hipError_t e = mk::launch_fwd_varlen(a, (unsigned)nblocks, D, causal, pos, st);
+  return e == hipSuccess ? MK_OK : MK_ERR_HIP;
+}
+
+size_t mk_attn_mla_decode_workspace_bytes(int H, int Dc, int n_parts) {
+  DecLayout l;
+  if (!mla_layout(H, Dc, n_parts, &l)) return 0;
+  return l.total;
+}
+
+int mk_attn_mla_decode(const void* q, const void* ckv, void* o, float* lse, int B, int H,
+                       int Dc, int Dr, int Smax, float scale, const int* kv_seqlens,
+                       int n_parts, void* workspace, size_t workspace_bytes, void* stream) {
+  using S = mk::MlaShape;
+  if (!q || !ckv || !o || !kv_seqlens) return MK_ERR_NULL;
+  if (B < 1 || H < 1 || Dc < 1 || Dr < 0 || Smax < 1) return MK_ERR_SHAPE;
+  const long long max_stages = (long long)B * ((Smax + mk::kDecStageKeys - 1) / mk::kDecStageKeys);
+  if ((long long)B * H > 0x7fffffffLL || max_stages > 0x7fffffffLL) return MK_ERR_SHAPE;
+  if (H != S::H || Dc != S::DC || Dr != S::DR) return MK_ERR_UNSUPPORTED;
+  if (n_parts < 0 || n_parts > kMaxParts) return MK_ERR_ARG;
+  if (!isfinite(scale)) return MK_ERR_ARG;
+  if (!aligned(q, 16) || !aligned(ckv, 16) || !aligned(o, 16) || !aligned(kv_seqlens, 4))
+    return MK_ERR_ALIGN;
+  if (lse && !aligned(lse, 4)) return MK_ERR_ALIGN;
+  DecLayout l;
+  if (!mla_layout(H, Dc, n_parts, &l)) return MK_ERR_SHAPE;
+  if (!workspace || workspace_bytes < l.total) return MK_ERR_WORKSPACE;
+  if (!aligned(workspace, 256)) return MK_ERR_ALIGN;
+  // the cache is one kv head of rows of Dc + Dr values; the merge works at
+  // the latent width
+  mk::DecArgs a = dec_args(q, ckv, ckv, o, lse, B, H, 1, Smax, scale, kv_seqlens, l, workspace);
+  const hipError_t e = mk::launch_mla_decode(a, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? MK_OK : MK_ERR_HIP;
 }
 

@@ -43,7 +43,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert mk.mk_attn_version() == 5
+    assert mk.mk_attn_version() == 6
     names = ["MK_OK", "MK_ERR_NULL", "MK_ERR_SHAPE", "MK_ERR_UNSUPPORTED", "MK_ERR_ALIGN",
              "MK_ERR_WORKSPACE", "MK_ERR_HIP", "MK_ERR_ARG"]
     for code, name in enumerate(names):
@@ -246,3 +246,40 @@ def test_bwd_validation(lib):
     assert bwd_rc(lib, ws=None) == 5
     assert bwd_rc(lib, ws_bytes=lib.mk_attn_bwd_workspace_bytes(2, 8, 100) - 1) == 5
     assert bwd_rc(lib, ws=P + 16) == 4
+
+
+def mla_rc(lib, *, q=P, ckv=P, o=P, lse=None, B=4, H=16, Dc=512, Dr=64, Smax=1000, scale=0.07,
+           seqlens=P, parts=0, ws=P, ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = lib.mk_attn_mla_decode_workspace_bytes(16, 512, max(parts, 0))
+    return lib.mk_attn_mla_decode(q, ckv, o, lse, B, H, Dc, Dr, Smax, scale, seqlens, parts, ws,
+                                  ws_bytes, None)
+
+
+def test_mla_workspace_bytes(lib):
+    # default: 256 parts x 2 pieces x 16 heads x 512 fp32, then 256 x 2 x 16 fp32
+    assert lib.mk_attn_mla_decode_workspace_bytes(16, 512, 0) == 256 * 2 * 16 * 512 * 4 + 32768
+    assert lib.mk_attn_mla_decode_workspace_bytes(16, 512, 3) == 3 * 2 * 16 * 512 * 4 + 512
+    assert lib.mk_attn_mla_decode_workspace_bytes(8, 512, 0) == 0
+    assert lib.mk_attn_mla_decode_workspace_bytes(16, 256, 0) == 0
+
+
+def test_mla_decode_validation(lib):
+    for name in ("q", "ckv", "o", "seqlens"):
+        assert mla_rc(lib, **{name: None}) == 1
+    for name in ("B", "H", "Dc", "Smax"):
+        assert mla_rc(lib, **{name: 0}) == 2
+    assert mla_rc(lib, Dr=-1) == 2
+    assert mla_rc(lib, B=1 << 20, Smax=1 << 20) == 2  # key stages past 32-bit indexing
+    assert mla_rc(lib, H=32) == 3
+    assert mla_rc(lib, Dc=256) == 3
+    assert mla_rc(lib, Dr=0) == 3
+    assert mla_rc(lib, parts=-1) == 7
+    assert mla_rc(lib, scale=math.nan) == 7
+    for name in ("q", "ckv", "o"):
+        assert mla_rc(lib, **{name: P_ODD}) == 4
+    assert mla_rc(lib, seqlens=P + 2) == 4
+    assert mla_rc(lib, lse=P + 1) == 4
+    assert mla_rc(lib, ws=None) == 5
+    assert mla_rc(lib, ws_bytes=lib.mk_attn_mla_decode_workspace_bytes(16, 512, 0) - 1) == 5
+    assert mla_rc(lib, ws=P + 16) == 4

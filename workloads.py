@@ -117,6 +117,25 @@ def decode_inputs(B: int, Hq: int, Hkv: int, Smax: int, D: int, seed: int,
     return q.to(torch.bfloat16), kc.to(torch.bfloat16), vc.to(torch.bfloat16), lens
 
 
+# MLA decode workload: the per-GPU share (16 of 128 query heads) of a
+# DeepSeek-V3-style absorbed MLA decode, latent 512 + rotary 64, with the
+# decode workload's batch and length recipe; the scale is 1/sqrt(192), the
+# head dim of the un-absorbed query-key product (128 + 64).
+MLA = dict(name="mla_decode_b64", B=64, H=16, Dc=512, Dr=64, Smax=4096, lmin=512, lmax=4096,
+           seed=1007, scale=float(torch.tensor(192 ** -0.5, dtype=torch.float32)))
+
+
+def mla_inputs(B: int, H: int, Dc: int, Dr: int, Smax: int, seed: int, lmin: int = 512,
+               lmax: int = 4096):
+    """(q [B,H,Dc+Dr] bf16, ckv [B,Smax,Dc+Dr] bf16, lens int32 [B]): lengths
+    U{lmin..lmax} first, then N(0,1) draws rounded to bf16."""
+    g = _gen(seed)
+    lens = torch.randint(lmin, lmax + 1, (B,), generator=g, dtype=torch.int64).to(torch.int32)
+    q = torch.randn((B, H, Dc + Dr), generator=g, dtype=torch.float32)
+    ckv = torch.randn((B, Smax, Dc + Dr), generator=g, dtype=torch.float32)
+    return q.to(torch.bfloat16), ckv.to(torch.bfloat16), lens
+
+
 def varlen_inputs(B: int, Hq: int, Hkv: int, D: int, lmin: int, lmax: int, seed: int):
     """Packed ragged prefill batch: lengths U{lmin..lmax} (queries = keys per
     sequence), then q [total,Hq,D], k/v [total,Hkv,D] bf16 N(0,1), and
