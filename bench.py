@@ -167,6 +167,7 @@ def main():
                     help="skip the packed ragged prefill leg")
     ap.add_argument("--no-bwd", action="store_true",
                     help="skip the backward leg (dQ, dK, dV on the prefill shape)")
+    ap.add_argument("--no-mla", action="store_true", help="skip the MLA decode leg")
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="query rows per head timed for the CPU oracle baseline (0: all)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -176,7 +177,7 @@ def main():
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print per-launch HBM bytes from FETCH_SIZE / WRITE_SIZE runs and exit")
     ap.add_argument("--kernels", default=None,
-                    help="comma-separated kernel name fragments for --summarize-pmc "
+                    help="semicolon-separated kernel name fragments for --summarize-pmc "
                          "(default fwd_kernel) or --summarize-trace (default all)")
     ap.add_argument("--command", action="append", default=[],
                     help="command line(s) recorded in a summary")
@@ -186,12 +187,12 @@ def main():
         args.kernels = "fwd_kernel"
 
     if args.summarize_trace:
-        kern = args.kernels.split(",") if args.kernels_given else None
+        kern = args.kernels.split(";") if args.kernels_given else None
         print(summarize_trace(args.summarize_trace, "; ".join(args.command), kern), end="")
         return
     if args.summarize_pmc:
         print(summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1],
-                            args.kernels.split(","), args.calib_copy_mib << 20, args.command),
+                            args.kernels.split(";"), args.calib_copy_mib << 20, args.command),
               end="")
         return
 
@@ -262,6 +263,21 @@ def main():
                         torch.empty_like(k_), torch.empty_like(v_),
                         torch.empty(bws_bytes, device=dev, dtype=torch.uint8)))
         del dout
+    mla = []
+    MW = workloads.MLA
+    if not args.no_mla:
+        # MLA decode: 64 sequences, 16 heads, latent 512 + rotary 64; two
+        # copies of the latent cache, used alternately
+        mq, mckv, mlens = workloads.mla_inputs(MW["B"], MW["H"], MW["Dc"], MW["Dr"], MW["Smax"],
+                                               MW["seed"], MW["lmin"], MW["lmax"])
+        mws_bytes = mk.mk_attn_mla_decode_workspace_bytes(MW["H"], MW["Dc"], 0)
+        mla_bytes = (int(mlens.clamp(0, MW["Smax"]).sum()) * (MW["Dc"] + MW["Dr"]) * 2
+                     + MW["B"] * MW["H"] * ((MW["Dc"] + MW["Dr"]) * 2 + MW["Dc"] * 2 + 4))
+        mla = [(mq.to(dev), mckv.to(dev) if i == 0 else mckv.to(dev).clone(), mlens.to(dev),
+                torch.empty((MW["B"], MW["H"], MW["Dc"]), device=dev, dtype=torch.bfloat16),
+                torch.empty((MW["B"], MW["H"]), device=dev, dtype=torch.float32),
+                torch.empty(mws_bytes, device=dev, dtype=torch.uint8)) for i in range(2)]
+        del mq, mckv
     del kc, vc
     qd = qd.to(dev)
     lens_d = lens.to(dev)
@@ -297,6 +313,11 @@ def main():
         mk.mk_attn_bwd(q_, k_, v_, o_, do_, lse_, dq_, dk_, dv_, pcfg.B, pcfg.Hq, pcfg.Hkv,
                        pcfg.S, pcfg.S, pcfg.D, int(pcfg.causal), pcfg.scale, None, bws_,
                        bws_.numel(), stream)
+
+    def mla_decode(i):
+        mq_, mc_, ml_, mo_, mlse_, mws_ = mla[i & 1]
+        mk.mk_attn_mla_decode(mq_, mc_, mo_, mlse_, MW["B"], MW["H"], MW["Dc"], MW["Dr"],
+                              MW["Smax"], MW["scale"], ml_, 0, mws_, mws_.numel(), stream)
 
     def decode_paged(i):
         kp_, vp_, bt_ = paged[i & 1]
@@ -378,6 +399,19 @@ def main():
         evb[1].record(stream)
         torch.cuda.synchronize()
         bwd_ms = evb[0].elapsed_time(evb[1]) / K
+    mla_ms = None
+    if mla:
+        # the MLA decode leg, timed after the step the same way
+        for i in range(args.warmup):
+            mla_decode(i)
+        evm = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        evm[0].record(stream)
+        for i in range(K):
+            mla_decode(i)
+        evm[1].record(stream)
+        torch.cuda.synchronize()
+        mla_ms = evm[0].elapsed_time(evm[1]) / K
     ms_step = (t1 - t0) * 1e3 / K
     pre_ms = ev[0].elapsed_time(ev[1]) / K  # average launch duration
     dec_ms = ev[1].elapsed_time(ev[2]) / K
@@ -390,7 +424,8 @@ def main():
         f"decode {dec_ms * 1e3:.1f} us ({dec_gbs:.1f} GB/s), step {ms_step:.3f} ms"
         + (f", varlen prefill {varlen_ms * 1e3:.1f} us" if varlen_ms is not None else "")
         + (f", paged decode {paged_ms * 1e3:.1f} us" if paged_ms is not None else "")
-        + (f", backward {bwd_ms * 1e3:.1f} us" if bwd_ms is not None else ""))
+        + (f", backward {bwd_ms * 1e3:.1f} us" if bwd_ms is not None else "")
+        + (f", MLA decode {mla_ms * 1e3:.1f} us" if mla_ms is not None else ""))
 
     digest = kernel_source_digest()
     traffic_pre = read_traffic(f"fwd_kernel_{pcfg.name}_counters.md", digest)
@@ -489,6 +524,21 @@ def main():
             "flops": b_flops,
             "roofline": {"bound": "mfma", "achieved": round(b_tf, 2), "peak": PEAK_BF16_TFLOPS,
                          "unit": "TFLOP/s", "frac": round(b_tf / PEAK_BF16_TFLOPS, 4),
+                         "traffic": None},
+        }
+
+    if mla_ms is not None:
+        m_gbs = mla_bytes / (mla_ms * 1e-3) / 1e9
+        result["mla_decode"] = {
+            "workload": (f"{MW['name']}: MLA decode B={MW['B']} H={MW['H']} latent {MW['Dc']} + "
+                         f"rotary {MW['Dr']}, lengths U[{MW['lmin']},{MW['lmax']}], shared "
+                         "latent cache, split-KV (equal-work parts) + LSE merge"),
+            "value": round(m_gbs, 1),
+            "unit": "GB/s",
+            "us": round(mla_ms * 1e3, 2),
+            "bytes": mla_bytes,
+            "roofline": {"bound": "hbm", "achieved": round(m_gbs, 1), "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": round(m_gbs / PEAK_HBM_GBS, 4),
                          "traffic": None},
         }
 
