@@ -109,8 +109,8 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
   constexpr int ROWS_PER_KB = 512 / D;
   constexpr int BLOCKS_PER_WAVE = BN * D * 2 / 1024 / WAVES;
   constexpr int LOADS_PER_TILE = 2 * BLOCKS_PER_WAVE;
-  __shared__ __attribute__((aligned(1024))) uint16_t k_lds[2][TILE];
-  __shared__ __attribute__((aligned(1024))) uint16_t v_lds[2][TILE];
+  // K tiles in buffers 0 and 1, V tiles in 2 and 3
+  __shared__ __attribute__((aligned(1024))) uint16_t kv_lds[4][TILE];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 31, h = lane >> 5;
@@ -157,8 +157,9 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
   constexpr int ROW_STEP = WAVES * ROWS_PER_KB;
   const int dma_row = wave * ROWS_PER_KB + lane / CHUNKS;
   const int dma_ch = ((lane % CHUNKS) ^ fwd_swz<D>(dma_row)) * 16;
-  const uint32_t k_lds_w = __builtin_amdgcn_readfirstlane(lds_addr(&k_lds[0][0]) + wave * 1024);
-  const uint32_t v_lds_w = __builtin_amdgcn_readfirstlane(lds_addr(&v_lds[0][0]) + wave * 1024);
+  const uint32_t k0 = lds_addr(&kv_lds[0][0]);
+  const uint32_t k_lds_w = __builtin_amdgcn_readfirstlane(k0 + wave * 1024);
+  const uint32_t v_lds_w = __builtin_amdgcn_readfirstlane(k0 + 2 * TILE_BYTES + wave * 1024);
   auto issue_tile = [&](int kt, int buf) {
     const int tlim = L - 1 - kt * BN;
 #pragma unroll
@@ -171,12 +172,13 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
     }
   };
 
-  // LDS read addresses: K / V rows (A operand, 32 keys x 8 head dims) and
+  // LDS read addresses (in K buffer 0; the buffer, the key block and V are
+  // immediate offsets): K / V rows (A operand, 32 keys x 8 head dims) and
   // transposing K^T reads (A operand of dQ^T = K^T dS^T)
   uint32_t kr_addr[KSTEPS];
 #pragma unroll
   for (int s = 0; s < KSTEPS; ++s)
-    kr_addr[s] = n * ROW_BYTES + (((2 * s + h) ^ fwd_swz<D>(n)) << 4);
+    kr_addr[s] = k0 + n * ROW_BYTES + (((2 * s + h) ^ fwd_swz<D>(n)) << 4);
   uint32_t kt_addr[DBLK][2];
   {
     const int tr_i = lane & 15;
@@ -188,10 +190,10 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
       for (int hh = 0; hh < 2; ++hh) {
         const int r = tr_row + 8 * hh;
         const int col = db * 32 + tr_col;
-        kt_addr[db][hh] = r * ROW_BYTES + ((((col >> 3) ^ fwd_swz<D>(r)) << 4) | ((col & 7) * 2));
+        kt_addr[db][hh] =
+            k0 + r * ROW_BYTES + ((((col >> 3) ^ fwd_swz<D>(r)) << 4) | ((col & 7) * 2));
       }
   }
-  const uint32_t k0 = lds_addr(&k_lds[0][0]), v0 = lds_addr(&v_lds[0][0]);
 
   f32x16 acc[DBLK];
 #pragma unroll
@@ -199,32 +201,52 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[db][r] = 0.f;
 
-  if (n_kt > 0) issue_tile(0, 0);
-  if (n_kt > 1) issue_tile(1, 1);
-  for (int kt = 0; kt < n_kt; ++kt) {
-    const int buf = kt & 1;
+  // One 64-key tile in buffer BUF.  Its LDS reads form one stream -- the
+  // K and V fragments of the score products (key block kb, step s, K then
+  // V), then the transposing K reads of dQ^T (chunk kc, block db, low /
+  // high rows) -- kept RW reads ahead of their use and waited for by count.
+  constexpr int NA = 4 * KSTEPS, NC = 8 * DBLK, TOT = NA + NC, RW = 6;
+  auto tile = [&](int kt, auto buf_tag) {
+    constexpr int BUF = decltype(buf_tag)::value;
     if (kt + 1 < n_kt)
       wait_vmcnt<LOADS_PER_TILE>();
     else
       wait_vmcnt<0>();
     __syncthreads();
-    const uint32_t kb_base = k0 + buf * TILE_BYTES, vb_base = v0 + buf * TILE_BYTES;
     const int key0 = kt * BN;
+    u32x4 ar[NA];
+    u32x2 cr[NC];
+    auto issue = [&](auto j_tag) {
+      constexpr int J = decltype(j_tag)::value;
+      if constexpr (J < NA) {
+        constexpr int KB = J / (2 * KSTEPS), ST = (J / 2) % KSTEPS, W = J % 2;
+        constexpr int OFF = (2 * W + BUF) * TILE_BYTES + KB * 32 * ROW_BYTES;
+        ar[J] = lds_read_b128_async_off<OFF>(kr_addr[ST]);
+      } else if constexpr (J < TOT) {
+        constexpr int C = J - NA, KC = C / (2 * DBLK), DB = (C / 2) % DBLK, HH = C % 2;
+        constexpr int OFF = BUF * TILE_BYTES + KC * 16 * ROW_BYTES;
+        cr[C] = lds_read_tr16_async_off<OFF>(kt_addr[DB][HH]);
+      }
+    };
+    static_for<0, RW>(issue);
     // S^T = K Q^T and dP^T = V dO^T for the tile's two 32-key blocks
     f32x16 st[2], dpt[2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) st[kb][r] = dpt[kb][r] = 0.f;
-#pragma unroll
-      for (int s = 0; s < KSTEPS; ++s) {
-        const uint32_t ad = kr_addr[s] + kb * 32 * ROW_BYTES;
-        const bf16x8 kf = as_bf16x8(lds_read_b128_at(kb_base + ad));
-        const bf16x8 vf = as_bf16x8(lds_read_b128_at(vb_base + ad));
-        st[kb] = mfma32(kf, qf[s], st[kb]);
-        dpt[kb] = mfma32(vf, df[s], dpt[kb]);
-      }
-    }
+    static_for<0, NA>([&](auto i_tag) {
+      constexpr int I = decltype(i_tag)::value;
+      constexpr int KB = I / (2 * KSTEPS), ST = (I / 2) % KSTEPS;
+      constexpr int AHEAD = (I + RW < TOT ? I + RW : TOT) - I - 1;
+      lds_wait_lgkm<AHEAD>();
+      lds_ready(ar[I]);
+      if constexpr (I % 2 == 0)
+        st[KB] = mfma32(as_bf16x8(ar[I]), qf[ST], st[KB]);
+      else
+        dpt[KB] = mfma32(as_bf16x8(ar[I]), df[ST], dpt[KB]);
+      issue(std::integral_constant<int, I + RW>());
+    });
     // dS^T = P^T (dP^T - D) as bf16, 16-key chunk kc = rows 8 (kc % 2) .. +7
     // of key block kc / 2
     bf16x8 dsf[4];
@@ -241,18 +263,28 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
       dsf[kc] = to_bf16x8(e[0], e[1], e[2], e[3], e[4], e[5], e[6], e[7]);
     }
     // dQ^T += K^T dS^T over the four 16-key chunks
-#pragma unroll
-    for (int kc = 0; kc < 4; ++kc) {
-#pragma unroll
-      for (int db = 0; db < DBLK; ++db) {
-        const uint32_t base = kb_base + kc * 16 * ROW_BYTES;
-        const bf16x4 lo = lds_read_tr16_at(base + kt_addr[db][0]);
-        const bf16x4 hi = lds_read_tr16_at(base + kt_addr[db][1]);
-        acc[db] = mfma32(cat(lo, hi), dsf[kc], acc[db]);
-      }
-    }
+    static_for<0, 4 * DBLK>([&](auto m_tag) {
+      constexpr int M = decltype(m_tag)::value;  // (kc, db) = (M / DBLK, M % DBLK)
+      constexpr int BASE = NA + 2 * M;
+      constexpr int AHEAD = (BASE + RW < TOT ? BASE + RW : TOT) - (BASE + 1) - 1;
+      lds_wait_lgkm<AHEAD>();
+      lds_ready(cr[2 * M]);
+      lds_ready(cr[2 * M + 1]);
+      const u32x4 w = {cr[2 * M][0], cr[2 * M][1], cr[2 * M + 1][0], cr[2 * M + 1][1]};
+      acc[M % DBLK] = mfma32(as_bf16x8(w), dsf[M / DBLK], acc[M % DBLK]);
+      issue(std::integral_constant<int, BASE + RW>());
+      issue(std::integral_constant<int, BASE + RW + 1>());
+    });
     __syncthreads();
-    if (kt + 2 < n_kt) issue_tile(kt + 2, buf);
+    if (kt + 2 < n_kt) issue_tile(kt + 2, BUF);
+  };
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  if (n_kt > 0) issue_tile(0, 0);
+  if (n_kt > 1) issue_tile(1, 1);
+  for (int kt = 0; kt < n_kt; kt += 2) {
+    tile(kt, B0());
+    if (kt + 1 < n_kt) tile(kt + 1, B1());
   }
 
   // dQ = scale * acc^T (lane (query n, k-group h) holds head dims
