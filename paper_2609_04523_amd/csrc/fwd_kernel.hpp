@@ -3,7 +3,7 @@
 // One workgroup = 4 waves = BM query rows of one (batch, query head); wave w
 // owns QB blocks of 32 consecutive rows.  The workgroup streams the 64-key
 // K and V tiles of its KV head (hq / (Hq/Hkv)) from HBM straight into LDS
-// (global_load_lds_dwordx4, double-buffered), up to the causal
+// (LDS-DMA loads, double-buffered), up to the causal
 // diagonal, and keeps the softmax state and the output accumulator in
 // registers: online softmax, an exact rewrite of softmax(Q K^T * scale) V
 // folded tile by tile.
@@ -19,7 +19,10 @@
 // Softmax bookkeeping (exp2 domain, c = scale * log2 e):
 //   m    running row maximum of c*s, raised only when a tile's maximum
 //        exceeds it by more than kRescaleSlack, so exp2(c*s - m) <= 2^8 and
-//        the O accumulator is rescaled on few tiles;
+//        the O accumulator is rescaled on few tiles.  The first tile and
+//        masked tiles take their row maximum; the other tiles are weighed
+//        against m directly, and one whose weights sum past 2^8 in any lane
+//        (scores that rose steeply) is formed again against its maximum;
 //   l    running sum of the fp32 weights (each half-wave sums its own
 //        keys; the halves are added at the end);
 //   O    sum of bf16(weight) * V in fp32;
@@ -76,6 +79,11 @@ struct FwdShape {
 };
 
 constexpr float kRescaleSlack = 8.0f;
+// A tile whose weights were formed against the running maximum without its
+// own is accepted when every lane's share of each row's weights sums to at
+// most 2^kRescaleSlack (so no weight exceeds it); otherwise its scores are
+// formed again and the tile is weighed against their maximum.
+constexpr float kSumLimit = 256.0f;
 
 // Work-item order.  Longest causal q-tiles are issued first.  When the
 // number of (batch, kv head) groups is a multiple of 8, consecutive
@@ -208,8 +216,9 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   const uint32_t k_lds_w = __builtin_amdgcn_readfirstlane(lds_addr(&k_lds[0][0]) + wave * 1024);
   const uint32_t v_lds_w = __builtin_amdgcn_readfirstlane(lds_addr(&v_lds[0][0]) + wave * 1024);
   // Block p of tile kt of one tensor (K or V) into LDS buffer BUF.  FULL:
-  // the tile lies inside the sequence, so no row needs clamping and the
-  // lane offsets are the precomputed full_off[p].
+  // the tile lies inside the sequence, so no row needs clamping: the load
+  // goes through a buffer resource on the tile with the precomputed lane
+  // offset full_off[p].
   uint32_t full_off[S::BLOCKS_PER_WAVE];
 #pragma unroll
   for (int p = 0; p < S::BLOCKS_PER_WAVE; ++p)
@@ -218,16 +227,16 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
                         auto full_tag) {
     constexpr int BUF = decltype(buf_tag)::value;
     constexpr int P = decltype(p_tag)::value;
-    uint32_t goff;
+    constexpr uint32_t lds_off = BUF * TILE_BYTES + P * S::WAVES * 1024;
+    const char* tile = g + (size_t)kt * BN * kv_stride;
     if constexpr (decltype(full_tag)::value) {
-      goff = full_off[P];
+      load_lds16_buf(tile, (uint32_t)(BN * kv_stride), full_off[P], lds_w + lds_off);
     } else {
       const int lim = L - 1 - kt * BN;  // last valid row of the tile
-      goff = (uint32_t)(min(dma_row, lim - P * ROW_STEP) * kv_stride + dma_ch) +
-             (uint32_t)(P * ROW_STEP * kv_stride);
+      const uint32_t goff = (uint32_t)(min(dma_row, lim - P * ROW_STEP) * kv_stride + dma_ch) +
+                            (uint32_t)(P * ROW_STEP * kv_stride);
+      load_lds16_at(tile + goff, lds_w + lds_off);
     }
-    constexpr uint32_t lds_off = BUF * TILE_BYTES + P * S::WAVES * 1024;
-    load_lds16_at(g + (size_t)kt * BN * kv_stride + goff, lds_w + lds_off);
   };
 
   float m_run[QB], l_run[QB];
@@ -306,6 +315,10 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
     constexpr bool PV = decltype(pv_tag)::value;
     constexpr bool MASK = decltype(mask_tag)::value;
     constexpr bool STEADY = decltype(steady_tag)::value;
+    // MAXP: tile t gets its row maximum (and the lazy rescale) in this step.
+    // Unmasked tiles after the first skip it when scale > 0: their weights
+    // are formed against the running maximum and checked by their sums.
+    constexpr bool MAXP = MASK || !PV || !POS_SCALE;
     constexpr int KBUF = PAR, VBUF = 1 - PAR;
     auto& s_new = pick<PAR>(s_even, s_odd);
     auto& s_old = pick<1 - PAR>(s_even, s_odd);
@@ -348,6 +361,9 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
     // their sum.
     const float cc = POS_SCALE ? c : 1.f;
     bf16x8 pf[QB][4];
+    float l_tile[QB];  // this lane's share of the row sums of tile t - 1
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) l_tile[qb] = 0.f;
     // The exponentials of chunk kc come in PER_EXP parts (one per score
     // product they are interleaved with); exp_finish then forms the chunk's
     // fragment and sum.
@@ -371,8 +387,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
       for (int qb = 0; qb < QB; ++qb) {
         const f32x16& x = s_old[qb][KC / 2];
         constexpr int R = 8 * (KC % 2);
-        l_run[qb] += ((x[R] + x[R + 1]) + (x[R + 2] + x[R + 3])) +
-                     ((x[R + 4] + x[R + 5]) + (x[R + 6] + x[R + 7]));
+        l_tile[qb] += ((x[R] + x[R + 1]) + (x[R + 2] + x[R + 3])) +
+                      ((x[R + 4] + x[R + 5]) + (x[R + 6] + x[R + 7]));
         pf[qb][KC] = to_bf16x8(x[R], x[R + 1], x[R + 2], x[R + 3], x[R + 4], x[R + 5], x[R + 6],
                                x[R + 7]);
       }
@@ -380,6 +396,66 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
     auto exp_chunk = [&](auto kc_tag) {
       static_for<0, PER_EXP>([&](auto j_tag) { exp_part(kc_tag, j_tag); });
       exp_finish(kc_tag);
+    };
+    // The weights of tile t - 1 are complete.  Rows whose sums overran
+    // kSumLimit (a tile weighed without its own maximum whose scores rose
+    // well above the running one) get the tile's scores again, from K in
+    // global memory (its LDS buffer is being refilled by now), a lazy
+    // rescale to the exact maximum, and new weights.  Then the sums join the
+    // running ones.
+    auto settle = [&]() {
+      if constexpr (POS_SCALE) {
+        // only tiles 1 .. n_free - 1 are weighed without their maximum; they
+        // lie wholly inside the sequence, so their K rows can be read again
+        const bool check = t >= 2 && t - 1 < n_free;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+          if (check && __ballot(l_tile[qb] > kSumLimit)) {
+            const char* kt_rows = kg + (size_t)(t - 1) * BN * kv_stride;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+              for (int r = 0; r < 16; ++r) s_old[qb][kb][r] = 0.f;
+#pragma unroll
+              for (int st = 0; st < S::KSTEPS; ++st) {
+                const u32x4 u = *reinterpret_cast<const u32x4*>(
+                    kt_rows + (size_t)(32 * kb + n) * kv_stride + (16 * st + 8 * h) * 2);
+                s_old[qb][kb] = mfma32(as_bf16x8(u), qf[qb][st], s_old[qb][kb]);
+                __builtin_amdgcn_sched_barrier(0);  // one fragment in registers at a time
+              }
+            }
+            float mx = kNegInf;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+              for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s_old[qb][kb][r]);
+            mx = max_xor32(mx) * c;
+            const float m_new = fmaxf(m_run[qb], mx);
+            const float alpha = (m_new == kNegInf) ? 1.f : fast_exp2(m_run[qb] - m_new);
+            m_run[qb] = m_new;
+            l_run[qb] *= alpha;
+#pragma unroll
+            for (int db = 0; db < S::DBLK; ++db)
+#pragma unroll
+              for (int r = 0; r < 16; ++r) o_acc[qb][db][r] *= alpha;
+            m_use[qb] = (m_new == kNegInf) ? 0.f : m_new;
+            l_tile[qb] = 0.f;
+            static_for<0, 4>([&](auto kc_tag) {
+              constexpr int KC = decltype(kc_tag)::value;
+              constexpr int R = 8 * (KC % 2);
+              f32x16& x = s_old[qb][KC / 2];
+#pragma unroll
+              for (int e = 0; e < 8; ++e) x[R + e] = fast_exp2(fmaf(x[R + e], c, -m_use[qb]));
+              l_tile[qb] += ((x[R] + x[R + 1]) + (x[R + 2] + x[R + 3])) +
+                            ((x[R + 4] + x[R + 5]) + (x[R + 6] + x[R + 7]));
+              pf[qb][KC] = to_bf16x8(x[R], x[R + 1], x[R + 2], x[R + 3], x[R + 4], x[R + 5],
+                                     x[R + 6], x[R + 7]);
+            });
+          }
+        }
+      }
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) l_run[qb] += l_tile[qb];
     };
 
 
@@ -419,6 +495,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
       static_for<0, S::BLOCKS_PER_WAVE>(load_block);
       if constexpr (PV) static_for<0, 4>(exp_chunk);
     }
+    if constexpr (PV) settle();
 
     // ---- softmax head of tile t: scale (scale <= 0), mask, row max, in
     // eight parts interleaved with the P V products of tile t - 1 (key block
@@ -467,16 +544,16 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
           o_acc[qb][M % S::DBLK] = mfma32(vf, pf[qb][M / S::DBLK], o_acc[qb][M % S::DBLK]);
         issue_read(std::integral_constant<int, NKS + RS + 2 * M>());
         issue_read(std::integral_constant<int, NKS + RS + 2 * M + 1>());
-        if constexpr (QK && M % PER_HEAD == PER_HEAD - 1)
+        if constexpr (QK && MAXP && M % PER_HEAD == PER_HEAD - 1)
           head_part(std::integral_constant<int, M / PER_HEAD>());
         __builtin_amdgcn_sched_barrier(0);
       });
-    } else if constexpr (QK) {
+    } else if constexpr (QK && MAXP) {
       static_for<0, 8>(head_part);
     }
 
     // ---- softmax head of tile t, end: lazy rescale of the running state ----
-    if constexpr (QK) {
+    if constexpr (QK && MAXP) {
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
         float mx = max_xor32(fmaxf(mx0[qb], mx1[qb]));

@@ -168,3 +168,31 @@ def test_stream_argument_is_used():
     s.synchronize()
     o_ref, lse_ref = oracle_fwd(q, k, v, causal=True, scale=128 ** -0.5)
     assert_parity("side_stream", o, lse, o_ref, lse_ref)
+
+
+# Scores that rise steeply after the first tiles: tiles after the first are
+# weighed against the running maximum without their own, so these rows make
+# the kernel re-form a tile against its maximum (with q x12 and the later
+# keys x4, c*s reaches ~166 > 128 above the first tile's maximum, where the
+# first weighing overflows fp32).  name, Hq, Hkv, S, causal, q_mult, k_low,
+# k_high, tiles of low keys
+RISE_CASES = [
+    ("rise_finite_causal", 4, 2, 512, True, 8.0, 0.05, 2.0, 1),
+    ("rise_overflow_causal", 4, 2, 512, True, 12.0, 0.05, 4.0, 3),
+    ("rise_overflow_noncausal_tail", 2, 1, 300, False, 12.0, 0.05, 4.0, 2),
+]
+
+
+@pytest.mark.parametrize("case", RISE_CASES, ids=[c[0] for c in RISE_CASES])
+def test_fwd_steeply_rising_scores(case):
+    name, Hq, Hkv, S, causal, qm, klo, khi, ntl = case
+    q, k, v = workloads.prefill_inputs(1, Hq, Hkv, S, S, 128, seed=zlib.crc32(name.encode()) % 100000)
+    q = (q.float() * qm).to(torch.bfloat16)
+    kf = k.float()
+    kf[:, :, :64 * ntl] *= klo
+    kf[:, :, 64 * ntl:] *= khi
+    k = kf.to(torch.bfloat16)
+    scale = 128 ** -0.5
+    o, lse = run_fwd(q, k, v, causal=causal, scale=scale)
+    o_ref, lse_ref = oracle_fwd(q, k, v, causal=causal, scale=scale)
+    assert_parity(name, o, lse, o_ref, lse_ref)
