@@ -492,6 +492,22 @@ __device__ __forceinline__ float wave_sum(float x) {
 // row's pieces (lane i: piece i) and the partial outputs of its first
 // CHUNK pieces (lanes: head dims) -- is issued before any is used, so a
 // cut row costs about two memory round trips and an uncut row one.
+// N consecutive floats (N * 4 bytes aligned to min(16, N * 4)) into x.
+template <int N>
+__device__ __forceinline__ void load_row_part(const float* p, float (&x)[N]) {
+  if constexpr (N % 4 == 0) {
+#pragma unroll
+    for (int j = 0; j < N / 4; ++j) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(p + 4 * j);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) x[4 * j + k] = v[k];
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < N; ++k) x[k] = p[k];
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(256) void dec_merge_kernel(DecArgs a) {
   constexpr int PER_LANE = D / 64;
@@ -548,13 +564,15 @@ __global__ __launch_bounds__(256) void dec_merge_kernel(DecArgs a) {
   const bool lane_holds = lane < n_pc && holds(lane);
   const unsigned long long held = __ballot(lane_holds);  // pieces 0..63
   const float ls0 = lane_holds ? a.lse_part[entry(lane)] : kNegInf;
+  // The first CHUNK pieces' partial outputs, loaded together.  A piece that
+  // is not held gets weight 0 below; its load reads piece 0 (always held:
+  // its part contains the pair's first stage), so every load is a plain
+  // vector load with no branch around it.
   float part[CHUNK][PER_LANE];
 #pragma unroll
   for (int i = 0; i < CHUNK; ++i) {
     const bool use = (held >> i) & 1;
-#pragma unroll
-    for (int k = 0; k < PER_LANE; ++k)
-      part[i][k] = use ? a.o_part[entry(i) * D + lane * PER_LANE + k] : 0.f;
+    load_row_part<PER_LANE>(a.o_part + entry(use ? i : 0) * D + lane * PER_LANE, part[i]);
   }
   float M = ls0;
   for (int i = 64 + lane; i < n_pc; i += 64)
