@@ -411,15 +411,19 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
           if (check && __ballot(l_tile[qb] > kSumLimit)) {
-            const char* kt_rows = kg + (size_t)(t - 1) * BN * kv_stride;
+            // the tile's rows through a buffer resource (32-bit lane
+            // offsets formed here, so no 64-bit address stays live)
+            const __amdgpu_buffer_rsrc_t rows = __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<char*>(kg + (size_t)(t - 1) * BN * kv_stride), 0,
+                (int)(BN * kv_stride), 0x00020000);
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
               for (int r = 0; r < 16; ++r) s_old[qb][kb][r] = 0.f;
 #pragma unroll
               for (int st = 0; st < S::KSTEPS; ++st) {
-                const u32x4 u = *reinterpret_cast<const u32x4*>(
-                    kt_rows + (size_t)(32 * kb + n) * kv_stride + (16 * st + 8 * h) * 2);
+                const u32x4 u = __builtin_amdgcn_raw_buffer_load_b128(
+                    rows, (uint32_t)((32 * kb + n) * kv_stride + (16 * st + 8 * h) * 2), 0, 0);
                 s_old[qb][kb] = mfma32(as_bf16x8(u), qf[qb][st], s_old[qb][kb]);
                 __builtin_amdgcn_sched_barrier(0);  // one fragment in registers at a time
               }
