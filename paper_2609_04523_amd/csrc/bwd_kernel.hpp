@@ -167,8 +167,8 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
       const uint32_t goff = (uint32_t)(min(dma_row + p * ROW_STEP, tlim) * ROW_BYTES + dma_ch);
       const size_t toff = (size_t)kt * BN * ROW_BYTES;
       const uint32_t lds_off = buf * TILE_BYTES + p * WAVES * 1024;
-      load_lds16_at(kg + toff + goff, k_lds_w + lds_off);
-      load_lds16_at(vg + toff + goff, v_lds_w + lds_off);
+      load_lds16_buf(kg + toff, TILE_BYTES, goff, k_lds_w + lds_off);
+      load_lds16_buf(vg + toff, TILE_BYTES, goff, v_lds_w + lds_off);
     }
   };
 
@@ -399,8 +399,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
   };
   auto issue_block = [&](const TileSrc& t, int p) {
     const uint32_t goff = (uint32_t)(min(dma_row + p * S::ROW_STEP, t.tlim) * ROW_BYTES + dma_ch);
-    load_lds16_at(t.qg + goff, t.lbuf + p * S::WAVES * 1024);
-    load_lds16_at(t.dg + goff, t.lbuf + TILE_BYTES + p * S::WAVES * 1024);
+    load_lds16_buf(t.qg, TILE_BYTES, goff, t.lbuf + p * S::WAVES * 1024);
+    load_lds16_buf(t.dg, TILE_BYTES, goff, t.lbuf + TILE_BYTES + p * S::WAVES * 1024);
   };
   auto issue_rows = [&](const TileSrc& t) {
     __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)(t.rows + lane),
