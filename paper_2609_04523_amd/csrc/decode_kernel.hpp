@@ -254,8 +254,8 @@ __global__ __launch_bounds__(64) void dec_part_kernel(DecArgs a) {
         const int r = dma_row + blk * S::ROWS_PER_KB;
         const int ch = ((lane % S::CHUNKS) ^ chunk_swz<D>(r)) * 16;
         const uint32_t goff = (uint32_t)(min(r, lim) * RB + ch);
-        load_lds16_at(kt_g + goff, slot + blk * 1024);
-        load_lds16_at(vt_g + goff, slot + S::TILE_BYTES + blk * 1024);
+        load_lds16_buf(kt_g, S::TILE_BYTES, goff, slot + blk * 1024);
+        load_lds16_buf(vt_g, S::TILE_BYTES, goff, slot + S::TILE_BYTES + blk * 1024);
       }
     }
     const char* q_g = reinterpret_cast<const char*>(a.q) + ((size_t)c.b * a.Hq + c.g * G) * RB;
@@ -263,7 +263,8 @@ __global__ __launch_bounds__(64) void dec_part_kernel(DecArgs a) {
     for (int blk = 0; blk < QBLOCKS; ++blk) {
       const int r = dma_row + blk * S::ROWS_PER_KB;
       const int ch = ((lane % S::CHUNKS) ^ chunk_swz<D>(r)) * 16;
-      load_lds16_at(q_g + min(r, G - 1) * RB + ch, slot + S::Q_OFF + blk * 1024);
+      load_lds16_buf(q_g, (uint32_t)(G * RB), (uint32_t)(min(r, G - 1) * RB + ch),
+                     slot + S::Q_OFF + blk * 1024);
     }
   };
 

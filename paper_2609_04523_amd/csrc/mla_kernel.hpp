@@ -93,7 +93,7 @@ __global__ __launch_bounds__(256, 1) void mla_part_kernel(DecArgs a) {
       const int r = o / RB;
       const int p = (o - r * RB) >> 4;
       const int lc = p ^ mla_swz(r);
-      load_lds16_at(g + (size_t)min(r, lim) * RB + lc * 16, dst0 + blk * 1024);
+      load_lds16_buf(g, S::SLOT_BYTES, (uint32_t)(min(r, lim) * RB + lc * 16), dst0 + blk * 1024);
     }
   };
   auto issue_q = [&](int b, uint32_t qbuf) {
@@ -106,7 +106,7 @@ __global__ __launch_bounds__(256, 1) void mla_part_kernel(DecArgs a) {
       const int r = o / RB;
       const int p = (o - r * RB) >> 4;
       const int lc = p ^ mla_swz(r);
-      load_lds16_at(g + (size_t)r * RB + lc * 16, dst0 + blk * 1024);
+      load_lds16_buf(g, S::Q_BYTES, (uint32_t)(r * RB + lc * 16), dst0 + blk * 1024);
     }
   };
 
