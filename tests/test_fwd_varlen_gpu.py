@@ -111,3 +111,26 @@ def test_varlen_deterministic_bitwise():
     a = run_varlen(q, k, v, cq, ck, causal=True, scale=128 ** -0.5)
     b = run_varlen(q, k, v, cq, ck, causal=True, scale=128 ** -0.5)
     assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+
+
+def test_varlen_steeply_rising_scores():
+    # Keys after each sequence's first 128 are scaled up steeply (q x12, the
+    # later keys x4 against x0.05 for the first ones), so tiles weighed
+    # against the running maximum overflow and are formed again from K read
+    # with the packed row stride.
+    seqs = [(400, 400), (1, 300), (260, 520)]
+    Hq, Hkv, D = 4, 2, 128
+    q, k, v, cq, ck = packed(seqs, Hq, Hkv, D, seed=4242)
+    q = (q.float() * 12.0).to(torch.bfloat16)
+    kf = k.float()
+    for b in range(len(seqs)):
+        s0, s1 = int(ck[b]), int(ck[b + 1])
+        kf[s0:min(s0 + 128, s1)] *= 0.05
+        kf[min(s0 + 128, s1):s1] *= 4.0
+    k = kf.to(torch.bfloat16)
+    scale = D ** -0.5
+    o, lse = run_varlen(q, k, v, cq, ck, causal=True, scale=scale)
+    o_ref, lse_ref = orc.attn_fwd_varlen(workloads.bits(q), workloads.bits(k), workloads.bits(v),
+                                         cq, ck, causal=True, scale=scale)
+    assert_parity("varlen_rising", o.permute(1, 0, 2)[None], lse[None],
+                  o_ref.transpose(1, 0, 2)[None], lse_ref[None])
