@@ -152,6 +152,65 @@ def summarize_pmc(fetch_path: str, write_path: str, kernels, calib_bytes: int,
     return "\n".join(out)
 
 
+def summarize_sq(paths, kernel: str, commands) -> str:
+    """Per-dispatch SQ/GRBM counters of the dispatches of `kernel` from one or
+    more --pmc runs (one counter pass each), averaged over the dispatches, and
+    the ratios derived from them.  SQ_* counters are summed over the chip;
+    GRBM_GUI_ACTIVE over the 8 XCDs, so the engine cycles of the kernel are
+    GRBM_GUI_ACTIVE / 8; MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x
+    those cycles); the wave-cycle counters count in units of 4 cycles, so
+    their ratios to SQ_WAVE_CYCLES are fractions of wave time."""
+    vals = {}
+    for path in paths:
+        for counter_rows in [_pmc_all(path)]:
+            for (name, counter), v in counter_rows.items():
+                if kernel in name:
+                    vals.setdefault(counter, []).extend(v)
+    avg = {c: sum(v) / len(v) for c, v in vals.items()}
+    out = ["# rocprofv3 SQ counters", ""]
+    for c in commands:
+        out.append(f"command: `{c}`")
+    out += ["", f"kernel_source_digest: {kernel_source_digest()}", "",
+            f"kernel: `{kernel}`", "", "| counter | per dispatch |", "|---|---|"]
+    for c in sorted(avg):
+        out.append(f"| {c} | {avg[c]:.4g} |")
+    out.append("")
+    g = avg.get("GRBM_GUI_ACTIVE")
+    if g:
+        cyc = g / 8.0
+        out.append(f"engine cycles per dispatch (GRBM_GUI_ACTIVE / 8): {cyc:.4g}")
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in avg:
+            out.append(f"MFMA busy: {100 * avg['SQ_VALU_MFMA_BUSY_CYCLES'] / (1024 * cyc):.1f} % "
+                       "of SIMD cycles")
+        if "SQ_INSTS_MFMA" in avg:
+            out.append(f"MFMA instructions per dispatch: {avg['SQ_INSTS_MFMA']:.4g}")
+    w = avg.get("SQ_WAVE_CYCLES")
+    if w:
+        for c in ("SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_WAIT_INST_LDS", "SQ_ACTIVE_INST_VALU",
+                  "SQ_ACTIVE_INST_LDS"):
+            if c in avg:
+                out.append(f"{c} / SQ_WAVE_CYCLES: {100 * avg[c] / w:.1f} %")
+    if "SQ_INSTS_VALU" in avg and "SQ_INSTS_MFMA" in avg:
+        out.append(f"vector instructions per MFMA (SQ_INSTS_VALU less MFMA): "
+                   f"{(avg['SQ_INSTS_VALU'] - avg['SQ_INSTS_MFMA']) / avg['SQ_INSTS_MFMA']:.2f}")
+    return "\n".join(out) + "\n"
+
+
+def _pmc_all(path: str):
+    import sqlite3
+    db = sqlite3.connect(_find_db(path))
+    rows = db.execute("select dispatch_id, name, counter_name, counter_value from pmc_events"
+                      ).fetchall()
+    per_disp = {}
+    for disp, name, counter, val in rows:
+        key = (disp, _short(name), counter)
+        per_disp[key] = per_disp.get(key, 0.0) + val
+    out = {}
+    for (disp, name, counter), val in per_disp.items():
+        out.setdefault((name, counter), []).append(val)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -176,6 +235,8 @@ def main():
                     help="print a summary of a rocprofv3 --kernel-trace output and exit")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print per-launch HBM bytes from FETCH_SIZE / WRITE_SIZE runs and exit")
+    ap.add_argument("--summarize-sq", nargs="+", metavar="DIR",
+                    help="print SQ/GRBM counters of --kernels (one name) from --pmc runs and exit")
     ap.add_argument("--kernels", default=None,
                     help="semicolon-separated kernel name fragments for --summarize-pmc "
                          "(default fwd_kernel) or --summarize-trace (default all)")
@@ -189,6 +250,9 @@ def main():
     if args.summarize_trace:
         kern = args.kernels.split(";") if args.kernels_given else None
         print(summarize_trace(args.summarize_trace, "; ".join(args.command), kern), end="")
+        return
+    if args.summarize_sq:
+        print(summarize_sq(args.summarize_sq, args.kernels, args.command), end="")
         return
     if args.summarize_pmc:
         print(summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1],
