@@ -1,8 +1,9 @@
 """Seeded random sweeps on the GPU against the fp64 oracle, through the C ABI:
 dense forward (mixed head groups, head dims, causal or not, ragged and
 clamped lengths, scales of either sign or zero, sharpened keys), packed
-ragged forward, decode with random lengths and part counts, and the
-backward (gradients against the oracle's backward).  Every
+ragged forward, decode with random lengths and part counts (contiguous and
+paged caches), MLA decode, and the backward (gradients against the
+oracle's backward).  Every
 configuration is drawn from a fixed seed, so a failure names a case that
 reruns identically."""
 
@@ -18,7 +19,7 @@ from parity import assert_parity
 pytestmark = pytest.mark.gpu
 
 DEV = "cuda:0"
-N_FWD, N_VARLEN, N_DEC, N_BWD = 48, 20, 24, 10
+N_FWD, N_VARLEN, N_DEC, N_BWD, N_PAGED, N_MLA = 48, 20, 24, 10, 12, 8
 
 
 def _fwd_case(i):
@@ -137,3 +138,48 @@ def test_bwd_random(i):
           f"lens={seqlens} k_mult={k_mult}", flush=True)
     check(f"bwd_random_{i}", B, Hq, Hkv, Sq, Skv, D, causal, seed=9900 + i, seqlens=seqlens,
           k_mult=k_mult)
+
+
+@pytest.mark.parametrize("i", range(N_PAGED))
+def test_decode_paged_random(i):
+    r = np.random.default_rng(9700 + i)
+    B = int(r.integers(1, 13))
+    D = int(r.choice([64, 128]))
+    Hkv = int(r.integers(1, 4))
+    G = int(r.choice([1, 4, 8]))
+    ps = int(r.choice([16, 32, 48, 64, 256]))
+    Smax = ps * int(r.integers(1, max(2, 2048 // ps)))
+    lens = [int(x) for x in r.integers(0, Smax + 1, size=B)]
+    n_parts = int(r.choice([0, 1, 50, 700]))
+    scale = D ** -0.5
+    print(f"[case] paged {i}: B={B} Hq={G * Hkv} Hkv={Hkv} D={D} page={ps} Smax={Smax} "
+          f"parts={n_parts} lens={lens}", flush=True)
+    q, kc, vc, _ = workloads.decode_inputs(B, G * Hkv, Hkv, Smax, D, seed=9700 + i, lmin=0,
+                                           lmax=Smax)
+    kp, vp, bt = workloads.paged_layout(kc, vc, ps, seed=9700 + i, extra_pages=int(r.integers(0, 9)),
+                                        lens=torch.tensor(lens))
+    sl = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    o, lse = mk.decode_paged(q.to(DEV), kp.to(DEV), vp.to(DEV), bt.to(DEV), sl, scale=scale,
+                             n_parts=n_parts)
+    torch.cuda.synchronize()
+    o_ref, lse_ref = orc.decode_paged(workloads.bits(q), workloads.bits(kp), workloads.bits(vp),
+                                      bt.numpy(), np.asarray(lens, dtype=np.int32), scale=scale)
+    assert_parity(f"paged_random_{i}", o, lse, o_ref, lse_ref)
+
+
+@pytest.mark.parametrize("i", range(N_MLA))
+def test_mla_random(i):
+    W = workloads.MLA
+    r = np.random.default_rng(9600 + i)
+    B = int(r.integers(1, 17))
+    Smax = int(r.choice([32, 600, 2500]))
+    lens = [int(x) for x in r.integers(0, Smax + 1, size=B)]
+    n_parts = int(r.choice([0, 1, 13, 300]))
+    print(f"[case] mla {i}: B={B} Smax={Smax} parts={n_parts} lens={lens}", flush=True)
+    q, ckv, _ = workloads.mla_inputs(B, W["H"], W["Dc"], W["Dr"], Smax, 9600 + i, 0, Smax)
+    o, lse = mk.mla_decode(q.to(DEV), ckv.to(DEV), torch.tensor(lens, dtype=torch.int32).to(DEV),
+                           Dc=W["Dc"], scale=W["scale"], n_parts=n_parts)
+    torch.cuda.synchronize()
+    o_ref, lse_ref = orc.mla_decode(workloads.bits(q), workloads.bits(ckv),
+                                    np.asarray(lens, np.int32), Dc=W["Dc"], scale=W["scale"])
+    assert_parity(f"mla_random_{i}", o, lse, o_ref, lse_ref)
