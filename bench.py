@@ -214,8 +214,8 @@ def _pmc_all(path: str):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--prefill", default="c2_mha_s2k")
     ap.add_argument("--decode", default="c5_decode_b64")
     ap.add_argument("--parts", type=int, default=0, help="decode parts (0 = library default)")
