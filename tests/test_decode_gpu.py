@@ -44,7 +44,7 @@ def oracle_decode(q, kc, vc, lens, scale):
                       np.asarray(lens, dtype=np.int32), scale=scale)
 
 
-def test_decode_config5_full_with_poisoned_padding():
+def test_decode_b64_ragged_full_with_poisoned_padding():
     cfg = workloads.CONFIGS["c5_decode_b64"]
     q, kc, vc, lens = workloads.config_inputs(cfg)
     kcp, vcp = poison_padding(kc, lens.tolist()), poison_padding(vc, lens.tolist())

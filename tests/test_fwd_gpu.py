@@ -73,19 +73,19 @@ def _config_parity(cfg, rows_per_head=0):
     return assert_parity(cfg.name, o, lse, o_ref, lse_ref)
 
 
-def test_fwd_config1_full():
+def test_fwd_mha_s128_d64_full():
     _config_parity(workloads.CONFIGS["c1_mha_s128_d64"])
 
 
-def test_fwd_config2_full():
+def test_fwd_mha_s2k_full():
     _config_parity(workloads.CONFIGS["c2_mha_s2k"])
 
 
-def test_fwd_config3_sampled_rows():
+def test_fwd_gqa_s8k_k2_sampled_rows():
     _config_parity(workloads.CONFIGS["c3_gqa_s8k_k2"], rows_per_head=256)
 
 
-def test_fwd_config4_sampled_rows():
+def test_fwd_gqa_s32k_sampled_rows():
     cfg = workloads.CONFIGS["c4_gqa_s32k"]
     _config_parity(cfg, rows_per_head=cfg.sample_rows)
 
