@@ -82,10 +82,22 @@ def summarize_trace(path: str, command: str, kernels=None) -> str:
     (the GPU-time share stays relative to all kernels of the run)."""
     import sqlite3
     db = sqlite3.connect(_find_db(path))
-    rows = db.execute("select name, duration from kernels").fetchall()
+    try:
+        rows = db.execute("select name, duration, grid_x / max(workgroup_x, 1) from kernels"
+                          ).fetchall()
+    except sqlite3.OperationalError:  # a trace without launch geometry
+        rows = [(n, d, 0) for n, d in db.execute("select name, duration from kernels")]
+    # launches of one kernel with different grids (one kernel timed on two
+    # workloads) get a row per workgroup count
+    grids = {}
+    for name, _, wgs in rows:
+        grids.setdefault(_short(name), set()).add(wgs)
     agg = {}
-    for name, dur in rows:
-        agg.setdefault(_short(name), []).append(dur / 1e3)  # ns -> us
+    for name, dur, wgs in rows:
+        key = _short(name)
+        if len(grids[key]) > 1:
+            key = f"{key} [{wgs} workgroups]"
+        agg.setdefault(key, []).append(dur / 1e3)  # ns -> us
     total = sum(sum(v) for v in agg.values())
     if kernels:
         agg = {k: v for k, v in agg.items() if any(f in k for f in kernels)}
@@ -227,6 +239,8 @@ def main():
     ap.add_argument("--no-bwd", action="store_true",
                     help="skip the backward leg (dQ, dK, dV on the prefill shape)")
     ap.add_argument("--no-mla", action="store_true", help="skip the MLA decode leg")
+    ap.add_argument("--long", default="c4_gqa_s32k",
+                    help="workload of the long-context prefill leg ('' skips the leg)")
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="query rows per head timed for the CPU oracle baseline (0: all)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -476,6 +490,39 @@ def main():
         evm[1].record(stream)
         torch.cuda.synchronize()
         mla_ms = evm[0].elapsed_time(evm[1]) / K
+    long_ms, lcfg = None, None
+    if args.long:
+        # the long-context prefill leg: the same kernel on a long causal
+        # workload (two input copies alternating), a few launches after two
+        # untimed ones, timed after the step the same way
+        lcfg = workloads.CONFIGS[args.long]
+        lq, lk, lv = workloads.config_inputs(lcfg)
+        lin = []
+        for _ in range(2):
+            lin.append((lq.to(dev), lk.to(dev), lv.to(dev),
+                        torch.empty(lq.shape, device=dev,
+                                    dtype=torch.float32 if lcfg.out_fp32 else torch.bfloat16),
+                        torch.empty(lq.shape[:3], device=dev, dtype=torch.float32)))
+        del lq, lk, lv
+        lentry = mk.mk_attn_fwd_o32 if lcfg.out_fp32 else mk.mk_attn_fwd
+
+        def long_prefill(i):
+            q_, k_, v_, o_, l_ = lin[i & 1]
+            lentry(q_, k_, v_, o_, l_, lcfg.B, lcfg.Hq, lcfg.Hkv, lcfg.S, lcfg.S, lcfg.D, 1,
+                   lcfg.scale, None, stream)
+        for i in range(2):
+            long_prefill(i)
+        KL = max(2, min(K, 10))
+        evl = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        evl[0].record(stream)
+        for i in range(KL):
+            long_prefill(i)
+        evl[1].record(stream)
+        torch.cuda.synchronize()
+        long_ms = evl[0].elapsed_time(evl[1]) / KL
+        del lin
+        torch.cuda.empty_cache()
     ms_step = (t1 - t0) * 1e3 / K
     pre_ms = ev[0].elapsed_time(ev[1]) / K  # average launch duration
     dec_ms = ev[1].elapsed_time(ev[2]) / K
@@ -489,7 +536,8 @@ def main():
         + (f", varlen prefill {varlen_ms * 1e3:.1f} us" if varlen_ms is not None else "")
         + (f", paged decode {paged_ms * 1e3:.1f} us" if paged_ms is not None else "")
         + (f", backward {bwd_ms * 1e3:.1f} us" if bwd_ms is not None else "")
-        + (f", MLA decode {mla_ms * 1e3:.1f} us" if mla_ms is not None else ""))
+        + (f", MLA decode {mla_ms * 1e3:.1f} us" if mla_ms is not None else "")
+        + (f", long prefill {long_ms * 1e3:.1f} us" if long_ms is not None else ""))
 
     digest = kernel_source_digest()
     traffic_pre = read_traffic(f"fwd_kernel_{pcfg.name}_counters.md", digest)
@@ -603,6 +651,19 @@ def main():
             "bytes": mla_bytes,
             "roofline": {"bound": "hbm", "achieved": round(m_gbs, 1), "peak": PEAK_HBM_GBS,
                          "unit": "GB/s", "frac": round(m_gbs / PEAK_HBM_GBS, 4),
+                         "traffic": None},
+        }
+
+    if long_ms is not None:
+        l_tf = lcfg.flops / (long_ms * 1e-3) / 1e12
+        result["long_prefill"] = {
+            "workload": (f"{lcfg.name}: causal attention fwd B={lcfg.B} Hq={lcfg.Hq} "
+                         f"Hkv={lcfg.Hkv} S={lcfg.S} D={lcfg.D} bf16"),
+            "value": round(l_tf, 2),
+            "unit": "TFLOP/s",
+            "us": round(long_ms * 1e3, 1),
+            "roofline": {"bound": "mfma", "achieved": round(l_tf, 2), "peak": PEAK_BF16_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(l_tf / PEAK_BF16_TFLOPS, 4),
                          "traffic": None},
         }
 
