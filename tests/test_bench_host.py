@@ -84,3 +84,23 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_summarize_trace_splits_one_kernel_by_grid(tmp_path):
+    d = str(tmp_path / "g")
+    os.makedirs(d)
+    con = sqlite3.connect(os.path.join(d, "x_results.db"))
+    con.execute("create table kernels (name text, duration integer, grid_x integer, "
+                "workgroup_x integer)")
+    con.executemany("insert into kernels values (?, ?, ?, ?)",
+                    [(FWD, 80_000, 1024 * 256, 256), (FWD, 7_000_000, 8192 * 256, 256),
+                     (FWD, 82_000, 1024 * 256, 256)])
+    con.commit()
+    con.close()
+    out = bench.summarize_trace(d, "cmd", ["fwd_kernel"])
+    rows = {l.split("`")[1]: l for l in out.splitlines() if l.startswith("| `")}
+    assert set(rows) == {"mk::fwd_kernel<128, true, false, 1, true, false> [1024 workgroups]",
+                         "mk::fwd_kernel<128, true, false, 1, true, false> [8192 workgroups]"}
+    small = [c.strip() for c in rows["mk::fwd_kernel<128, true, false, 1, true, false> "
+                                     "[1024 workgroups]"].split("|")]
+    assert small[2] == "2" and small[3] == "81.00"
