@@ -101,3 +101,30 @@ def mla_decode(q, ckv, kv_seqlens, *, Dc: int, scale: float):
             for e in range(Dc):
                 o[b][h][e] = math.fsum(w[j] * rows[j][e] for j in range(L)) / z
     return o, lse
+
+
+def probs(q, k, *, causal: bool, scale: float, kv_seqlens=None):
+    """The normalised attention weights by brute force: the whole masked
+    score matrix (-inf where a key is not admissible), exp without
+    max-subtraction, each row divided by its fsum.  q: nested lists
+    [B][Hq][Sq][D] of bf16 bit patterns; k: [B][Hkv][Skv][D].  Returns
+    p [B][Hq][Sq][Skv] (rows without an admissible key are all zero)."""
+    dec = lambda t: [[[[bf16_bits_to_float(x) for x in row] for row in h] for h in bb] for bb in t]
+    qf, kf = dec(q), dec(k)
+    B, Hq, Sq, D = len(qf), len(qf[0]), len(qf[0][0]), len(qf[0][0][0])
+    Hkv, Skv = len(kf[0]), len(kf[0][0])
+    G = Hq // Hkv
+    out = [[[[0.0] * Skv for _ in range(Sq)] for _ in range(Hq)] for _ in range(B)]
+    for b in range(B):
+        L = Skv if kv_seqlens is None else max(0, min(Skv, int(kv_seqlens[b])))
+        allowed = _mask(Sq, Skv, L, causal)
+        for hq in range(Hq):
+            Kh = kf[b][hq // G]
+            for i in range(Sq):
+                qi = qf[b][hq][i]
+                e = [math.exp(scale * math.fsum(qi[d] * Kh[j][d] for d in range(D)))
+                     if allowed[i][j] else 0.0 for j in range(Skv)]
+                z = math.fsum(e)
+                if z > 0.0:
+                    out[b][hq][i] = [x / z for x in e]
+    return out

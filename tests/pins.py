@@ -147,6 +147,34 @@ def pin_rows_sum_to_one(lib):
                     assert np.all(row[:, :lim] > 0.0), "zero weight on an admissible key"
 
 
+def pin_probs_brute_force(lib):
+    """The weights themselves: equal to the brute-force exp(s) / sum exp(s)
+    (materialised mask, no max-subtraction) on the brute cases, which fixes
+    the scale, the head mapping and the mask inside them."""
+    for n, (B, Hq, Hkv, Sq, Skv, D, causal, sl) in enumerate(BRUTE_CASES):
+        q = _rand((B, Hq, Sq, D), 10 + n)
+        k = _rand((B, Hkv, Skv, D), 20 + n)
+        scale = 0.7 / math.sqrt(D)
+        p = orc.attn_probs(q, k, causal=causal, scale=scale, kv_seqlens=sl, lib=lib)
+        pb = brute.probs(q.tolist(), k.tolist(), causal=causal, scale=scale, kv_seqlens=sl)
+        _close(p, np.array(pb), 1e-13, f"brute case {n} P")
+
+
+def pin_probs_times_values(lib):
+    """P V (a numpy product, V's heads repeated G times in order) equals the
+    forward's O: the weights are the ones the output is formed with."""
+    B, Hq, Hkv, Sq, Skv, D = 2, 6, 2, 7, 11, 8
+    q = _rand((B, Hq, Sq, D), 61, -3, 3)
+    k = _rand((B, Hkv, Skv, D), 62, -3, 3)
+    v = _rand((B, Hkv, Skv, D), 63)
+    vr = np.repeat(_f(v), Hq // Hkv, axis=1)
+    for causal in (True, False):
+        for sl in (None, [11, 4]):
+            p = orc.attn_probs(q, k, causal=causal, scale=0.8, kv_seqlens=sl, lib=lib)
+            o, _ = orc.attn_fwd(q, k, v, causal=causal, scale=0.8, kv_seqlens=sl, lib=lib)
+            _close(p @ vr, o, 1e-13, "P V against O")
+
+
 def pin_equal_value_rows(lib):
     B, Hq, Hkv, S, D = 1, 4, 2, 33, 16
     q = _rand((B, Hq, S, D), 51, -4, 4)
@@ -524,7 +552,8 @@ def pin_mla_single_key_and_rope(lib):
     assert np.abs(c[1] - d[1]).max() > 1e-6
 
 
-ALL_PINS = [pin_golden, pin_brute_force, pin_rows_sum_to_one, pin_equal_value_rows,
+ALL_PINS = [pin_golden, pin_brute_force, pin_rows_sum_to_one, pin_probs_brute_force,
+            pin_probs_times_values, pin_equal_value_rows,
             pin_causal_row0, pin_single_key, pin_scale_zero, pin_gqa_equals_repeated_mha,
             pin_decode_equals_last_prefill_row, pin_split_combine, pin_row_subset,
             pin_paged_equals_gathered, pin_paged_table_clamp_and_unused_pages,

@@ -63,6 +63,10 @@ MUTANTS = {
                           "            double l = 0.0;\n            for (int j = 0; j < L; ++j) { s[j] = exp",
                           "s[j] = dot;\n                if (s[j] > m) m = s[j];\n            }\n"
                           "            double l = 0.0;\n            for (int j = 0; j < L; ++j) { s[j] = exp", 1),
+    "probs_scale_dropped": ("s[j] = scale * dot;\n                }\n                double m = s[0];",
+                            "s[j] = dot;\n                }\n                double m = s[0];", 1),
+    "probs_gqa_interleaved_heads": ("int g = hq / G;\n                int L = clamp_len(",
+                                    "int g = hq % Hkv;\n                int L = clamp_len(", 1),
     "varlen_key_start_ignored": ("const uint16_t *k_row = k + ((size_t)(k0 + j) * Hkv + g) * D;",
                                  "const uint16_t *k_row = k + ((size_t)(j) * Hkv + g) * D;", 1),
 }
