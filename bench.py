@@ -1,8 +1,8 @@
 """Benchmark of the attention hot path on one MI355X.
 
 One step = one pass over the whole path on resident synthetic inputs:
-  * the fused causal attention forward on the prefill workload
-    (causal MHA B=4 H=16 S=2048 D=128 bf16 by default), then
+  * the fused causal attention forward on the long-context workload
+    (causal GQA B=1 Hq=32 Hkv=8 S=32768 D=128 bf16, the largest one), then
   * the split-KV decode (equal-work part kernel + LSE merge kernel) on the
     ragged decode batch (B=64 Hq=32 Hkv=8 D=128, lengths in [512, 4096]).
 Each workload alternates between two copies of its inputs so the 256 MB
@@ -11,7 +11,13 @@ last-level cache cannot hand one launch the previous launch's data.
 The K timed steps run as K prefill launches back to back, then K decode
 launches back to back, on torch's current stream; HIP events recorded on
 that stream before, between and after give each kernel's average launch
-duration.  Prints ONE JSON line on stdout; progress goes to stderr.
+duration.  After the step, legs time the other workloads the same way
+(each with warm-up launches of its own just before its timed block): the
+8k and 2k prefill workloads, the small one, the decode alone over a fixed
+number of launches, and the rows built beyond the forward (packed ragged
+prefill, paged decode, backward, MLA decode).  Then the CPU oracle is timed
+on every workload (a baseline, not a target).  Prints ONE JSON line on
+stdout; progress goes to stderr.
 """
 from __future__ import annotations
 
@@ -111,11 +117,27 @@ def summarize_trace(path: str, command: str, kernels=None) -> str:
     return "\n".join(out) + "\n"
 
 
+def _dispatch_grids(db):
+    """dispatch id -> workgroup count, from the trace tables of a run (empty
+    for databases without launch geometry)."""
+    import sqlite3
+    try:
+        rows = db.execute("select dispatch_id, grid_x / max(workgroup_x, 1) from kernels"
+                          ).fetchall()
+    except sqlite3.OperationalError:
+        return {}
+    return {d: int(w) for d, w in rows}
+
+
 def _pmc_per_kernel(path: str, counter: str):
+    """Counter values per dispatch, keyed by kernel name and also by
+    'name@N' for the dispatches with N workgroups (one kernel timed on
+    several workloads)."""
     import sqlite3
     db = sqlite3.connect(_find_db(path))
     rows = db.execute("select dispatch_id, name, counter_name, counter_value from pmc_events "
                       "where counter_name = ?", (counter,)).fetchall()
+    grids = _dispatch_grids(db)
     per_disp = {}
     for disp, name, _, val in rows:
         key = (disp, _short(name))
@@ -123,7 +145,17 @@ def _pmc_per_kernel(path: str, counter: str):
     per_kernel = {}
     for (disp, name), val in per_disp.items():
         per_kernel.setdefault(name, []).append(val)
+        if disp in grids:
+            per_kernel.setdefault(f"{name}@{grids[disp]}", []).append(val)
     return per_kernel
+
+
+def _match_kernel(names, frag: str):
+    """Kernel key for a fragment 'part' or 'part@N' (N workgroups)."""
+    if "@" in frag:
+        part, wgs = frag.split("@")
+        return [n for n in names if n.endswith(f"@{wgs}") and part in n]
+    return [n for n in names if frag in n and "@" not in n]
 
 
 def summarize_pmc(fetch_path: str, write_path: str, kernels, calib_bytes: int,
@@ -133,7 +165,7 @@ def summarize_pmc(fetch_path: str, write_path: str, kernels, calib_bytes: int,
     for the plain device copy of calib_bytes in the same run."""
     fetch = _pmc_per_kernel(fetch_path, "FETCH_SIZE")
     write = _pmc_per_kernel(write_path, "WRITE_SIZE")
-    copy = [k for k in fetch if "copyBuffer" in k]
+    copy = [k for k in fetch if "copyBuffer" in k and "@" not in k]
     if not copy:
         raise SystemExit("no calibration copy kernel in the FETCH_SIZE run")
     # the calibration copy is the largest copyBuffer dispatch
@@ -152,10 +184,12 @@ def summarize_pmc(fetch_path: str, write_path: str, kernels, calib_bytes: int,
             "scaled read bytes | scaled write bytes |", "|---|---|---|---|---|---|"]
     total = 0.0
     for k in kernels:
-        name = [n for n in fetch if k in n]
+        name = _match_kernel(list(fetch), k)
         if not name:
             raise SystemExit(f"kernel {k} not in the counter runs")
-        fv, wv = fetch[name[0]], write[name[0]]
+        fv, wv = fetch[name[0]], write.get(name[0], [])
+        if not wv:
+            raise SystemExit(f"kernel {k} not in the WRITE_SIZE run")
         f_avg, w_avg = sum(fv) / len(fv), sum(wv) / len(wv)
         rb, wb = f_avg * 1024 * f_fac, w_avg * 1024 * w_fac
         total += rb + wb
@@ -175,8 +209,10 @@ def summarize_sq(paths, kernel: str, commands) -> str:
     vals = {}
     for path in paths:
         for counter_rows in [_pmc_all(path)]:
+            names = sorted({n for n, _ in counter_rows})
+            keep = set(_match_kernel(names, kernel))
             for (name, counter), v in counter_rows.items():
-                if kernel in name:
+                if name in keep:
                     vals.setdefault(counter, []).extend(v)
     avg = {c: sum(v) / len(v) for c, v in vals.items()}
     out = ["# rocprofv3 SQ counters", ""]
@@ -209,10 +245,13 @@ def summarize_sq(paths, kernel: str, commands) -> str:
 
 
 def _pmc_all(path: str):
+    """Every counter per dispatch, keyed (kernel, counter) and also
+    (kernel@N, counter) for the dispatches with N workgroups."""
     import sqlite3
     db = sqlite3.connect(_find_db(path))
     rows = db.execute("select dispatch_id, name, counter_name, counter_value from pmc_events"
                       ).fetchall()
+    grids = _dispatch_grids(db)
     per_disp = {}
     for disp, name, counter, val in rows:
         key = (disp, _short(name), counter)
@@ -220,29 +259,157 @@ def _pmc_all(path: str):
     out = {}
     for (disp, name, counter), val in per_disp.items():
         out.setdefault((name, counter), []).append(val)
+        if disp in grids:
+            out.setdefault((f"{name}@{grids[disp]}", counter), []).append(val)
     return out
+
+
+LEGS_ALL = "c3,c2,c1,decode,varlen,paged,bwd,mla"
+
+
+def prefill_alg_bytes(cfg) -> int:
+    """Algorithmic HBM bytes of one forward launch: q, k, v read once, o and
+    lse written once."""
+    q = cfg.B * cfg.Hq * cfg.S * cfg.D * 2
+    kv = 2 * cfg.B * cfg.Hkv * cfg.S * cfg.D * 2
+    o = cfg.B * cfg.Hq * cfg.S * cfg.D * (4 if cfg.out_fp32 else 2)
+    lse = cfg.B * cfg.Hq * cfg.S * 4
+    return q + kv + o + lse
+
+
+def decode_alg_bytes(B, Hq, Hkv, D, sum_l) -> int:
+    """Algorithmic HBM bytes of one decode: each valid cached key and value
+    row once per kv head, q read, o (bf16) and lse written."""
+    return 4 * D * Hkv * sum_l + (B * Hq * D * 2) * 2 + B * Hq * 4
+
+
+def prefill_record(cfg, us, traffic):
+    flops = cfg.flops
+    tf = flops / (us * 1e-6) / 1e12
+    nbytes = prefill_alg_bytes(cfg)
+    gbs = nbytes / (us * 1e-6) / 1e9
+    rec = {
+        "workload": (f"{cfg.name}: causal attention fwd B={cfg.B} Hq={cfg.Hq} Hkv={cfg.Hkv} "
+                     f"S={cfg.S} D={cfg.D} bf16 in, {'fp32' if cfg.out_fp32 else 'bf16'} O"
+                     + (f", K x{cfg.k_mult:g}" if cfg.k_mult != 1.0 else "")),
+        "us": round(us, 2),
+        "tflops": round(tf, 2),
+        "frac_mfma_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+        "flops": flops,
+        "alg_bytes": nbytes,
+        "gbs": round(gbs, 1),
+        "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 5),
+        "counter_bytes": traffic,
+        "counter_gbs": None if traffic is None else round(traffic / (us * 1e-6) / 1e9, 1),
+    }
+    return rec
+
+
+def time_block(stream, fn, warmup: int, n: int) -> float:
+    """Average duration (ms) of n launches of fn(i) issued back to back after
+    `warmup` untimed ones, between two events on `stream`."""
+    import torch
+    for i in range(warmup):
+        fn(i)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    for i in range(n):
+        fn(i)
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    return ev[0].elapsed_time(ev[1]) / n
+
+
+def cpu_baselines(args, dec_sum_l):
+    """The oracle as it stands, timed on the host: every workload, the 32k one
+    on its 256-row-per-head sample (plus a labelled extrapolation to all
+    rows), and single-thread times for the small workloads."""
+    import workloads
+    from oracle import oracle as orc  # timed CPU baseline only
+    threads = orc.default_threads()
+    runs = []
+
+    def prefill_run(cfg, nthreads, rows_per_head=0, batches=None):
+        q, k, v = workloads.config_inputs(cfg)
+        if batches is not None:
+            q, k, v = q[:batches], k[:batches], v[:batches]
+        B = q.shape[0]
+        qb, kb, vb = workloads.bits(q), workloads.bits(k), workloads.bits(v)
+        del q, k, v
+        if rows_per_head:
+            rows = workloads.sample_rows(B, cfg.Hq, cfg.S, rows_per_head, seed=cfg.seed)
+            pairs = int((rows.long() + 1).sum())  # causal row i sees i + 1 keys
+            rows_np = rows.numpy()
+            what = f"{rows_per_head} seeded query rows per head"
+        else:
+            rows_np = None
+            pairs = B * cfg.Hq * cfg.pairs_per_head
+            what = "every query row" + (f" of batch entries 0..{B - 1}" if batches else "")
+        log(f"[bench] cpu oracle: {cfg.name}, {what}, {nthreads} threads")
+        t0 = time.perf_counter()
+        orc.attn_fwd(qb, kb, vb, causal=True, scale=cfg.scale, rows=rows_np, threads=nthreads)
+        sec = time.perf_counter() - t0
+        rec = {"config": cfg.name, "rows": what, "threads": nthreads, "seconds": round(sec, 3),
+               "pairs": pairs, "fp64_tflops": 4 * cfg.D * pairs / sec / 1e12}
+        full_pairs = cfg.B * cfg.Hq * cfg.pairs_per_head
+        if pairs != full_pairs:
+            rec["extrapolated_full_seconds"] = round(sec * full_pairs / pairs, 1)
+        runs.append(rec)
+        return rec
+
+    def decode_run(cfg, nthreads):
+        qd, kc, vc, lens = workloads.config_inputs(cfg)
+        args_ = (workloads.bits(qd), workloads.bits(kc), workloads.bits(vc), lens.numpy())
+        del kc, vc
+        log(f"[bench] cpu oracle: {cfg.name}, {nthreads} threads")
+        t0 = time.perf_counter()
+        orc.decode(*args_, scale=cfg.scale, threads=nthreads)
+        sec = time.perf_counter() - t0
+        pairs = cfg.Hq * dec_sum_l
+        runs.append({"config": cfg.name, "rows": "every sequence", "threads": nthreads,
+                     "seconds": round(sec, 3), "pairs": pairs,
+                     "fp64_tflops": 4 * cfg.D * pairs / sec / 1e12})
+
+    C = workloads.CONFIGS
+    head = prefill_run(C["c4_gqa_s32k"], threads, rows_per_head=C["c4_gqa_s32k"].sample_rows)
+    if args.cpu_baseline == "all":
+        prefill_run(C["c1_mha_s128_d64"], threads)
+        prefill_run(C["c1_mha_s128_d64"], 1)
+        prefill_run(C["c2_mha_s2k"], threads)
+        prefill_run(C["c2_mha_s2k"], 1, batches=1)
+        prefill_run(C["c3_gqa_s8k_k2"], threads)
+        decode_run(C["c5_decode_b64"], threads)
+        decode_run(C["c5_decode_b64"], 1)
+    return {
+        "value": round(head["fp64_tflops"], 6),
+        "unit": "TFLOP/s",
+        "cores": threads,
+        "host_cpus": os.cpu_count(),
+        "kind": "oracle",
+        "sample": (f"{head['rows']} of c4_gqa_s32k ({head['pairs']} query-key pairs, fp64, "
+                   f"{head['seconds']:.2f} s on {threads} threads; all rows extrapolate to "
+                   f"{head['extrapolated_full_seconds']} s); per_config lists every workload"),
+        "per_config": runs,
+    }
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--prefill", default="c2_mha_s2k")
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--prefill", default="c4_gqa_s32k")
     ap.add_argument("--decode", default="c5_decode_b64")
     ap.add_argument("--parts", type=int, default=0, help="decode parts (0 = library default)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--page-size", type=int, default=16,
-                    help="page size of the paged-decode leg (0 skips the leg)")
-    ap.add_argument("--no-varlen", action="store_true",
-                    help="skip the packed ragged prefill leg")
-    ap.add_argument("--no-bwd", action="store_true",
-                    help="skip the backward leg (dQ, dK, dV on the prefill shape)")
-    ap.add_argument("--no-mla", action="store_true", help="skip the MLA decode leg")
-    ap.add_argument("--long", default="c4_gqa_s32k",
-                    help="workload of the long-context prefill leg ('' skips the leg)")
-    ap.add_argument("--cpu-rows", type=int, default=0,
-                    help="query rows per head timed for the CPU oracle baseline (0: all)")
+    ap.add_argument("--legs", default=LEGS_ALL,
+                    help="comma-separated legs timed after the step ('' for none): "
+                         + LEGS_ALL)
+    ap.add_argument("--decode-launches", type=int, default=200,
+                    help="launches of the stand-alone decode leg (after 50 warm-up ones)")
+    ap.add_argument("--cpu-baseline", choices=("all", "headline", "none"), default="all",
+                    help="oracle timing: every workload, the headline sample only, or none")
+    ap.add_argument("--page-size", type=int, default=16, help="page size of the paged leg")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this size (counter calibration)")
     ap.add_argument("--summarize-trace", metavar="DIR",
@@ -252,7 +419,8 @@ def main():
     ap.add_argument("--summarize-sq", nargs="+", metavar="DIR",
                     help="print SQ/GRBM counters of --kernels (one name) from --pmc runs and exit")
     ap.add_argument("--kernels", default=None,
-                    help="semicolon-separated kernel name fragments for --summarize-pmc "
+                    help="semicolon-separated kernel name fragments, each optionally "
+                         "'name@N' for its launches with N workgroups, for --summarize-pmc "
                          "(default fwd_kernel) or --summarize-trace (default all)")
     ap.add_argument("--command", action="append", default=[],
                     help="command line(s) recorded in a summary")
@@ -279,8 +447,11 @@ def main():
               "(the path would shard by (batch, kv head) groups, one group set per GPU)",
               file=sys.stderr)
         sys.exit(2)
+    legs = [x for x in args.legs.split(",") if x]
+    unknown = set(legs) - set(LEGS_ALL.split(","))
+    if unknown:
+        raise SystemExit(f"unknown legs {sorted(unknown)}")
 
-    import numpy as np
     import torch
 
     import paper_2609_04523_amd as mk
@@ -292,71 +463,36 @@ def main():
     mk.lib()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    digest = kernel_source_digest()
+
+    def prefill_inputs_on_device(cfg):
+        """Two copies of a prefill workload's tensors, used alternately."""
+        q, k, v = workloads.config_inputs(cfg)
+        out = []
+        for _ in range(2):
+            o = torch.empty(q.shape, device=dev,
+                            dtype=torch.float32 if cfg.out_fp32 else torch.bfloat16)
+            lse = torch.empty(q.shape[:3], device=dev, dtype=torch.float32)
+            out.append((q.to(dev), k.to(dev), v.to(dev), o, lse))
+        return out
+
+    def prefill_fn(cfg, bufs):
+        entry = mk.mk_attn_fwd_o32 if cfg.out_fp32 else mk.mk_attn_fwd
+
+        def run(i):
+            q, k, v, o, lse = bufs[i & 1]
+            entry(q, k, v, o, lse, cfg.B, cfg.Hq, cfg.Hkv, cfg.S, cfg.S, cfg.D, 1, cfg.scale,
+                  None, stream)
+        return run
 
     pcfg = workloads.CONFIGS[args.prefill]
     dcfg = workloads.CONFIGS[args.decode]
     log(f"[bench] inputs: prefill {pcfg.name}, decode {dcfg.name}")
-    q, k, v = workloads.config_inputs(pcfg)
-    # two copies of the prefill tensors, used alternately, so that the
-    # 256 MB last-level cache cannot hand one launch the previous one's data
-    pre = []
-    for _ in range(2):
-        o = torch.empty(q.shape, device=dev,
-                        dtype=torch.float32 if pcfg.out_fp32 else torch.bfloat16)
-        lse = torch.empty(q.shape[:3], device=dev, dtype=torch.float32)
-        pre.append((q.to(dev), k.to(dev), v.to(dev), o, lse))
-    del q, k, v
+    pre = prefill_inputs_on_device(pcfg)
+    prefill = prefill_fn(pcfg, pre)
     qd, kc, vc, lens = workloads.config_inputs(dcfg)
-    caches = [(kc.to(dev), vc.to(dev)), (kc.to(dev).clone(), vc.to(dev).clone())]
-    # packed ragged prefill batch: 16 causal sequences, lengths U{256..8192}
-    VL = dict(B=16, Hq=32, Hkv=8, D=128, lmin=256, lmax=8192, seed=1006)
-    varlen = []
-    if not args.no_varlen:
-        vq, vk, vv, vcu = workloads.varlen_inputs(**VL)
-        vlens = (vcu[1:] - vcu[:-1]).tolist()
-        varlen = [(vq.to(dev), vk.to(dev), vv.to(dev), vcu.to(dev),
-                   torch.empty(vq.shape, device=dev, dtype=torch.bfloat16),
-                   torch.empty((VL["Hq"], vq.shape[0]), device=dev, dtype=torch.float32))
-                  for _ in range(2)]
-        del vq, vk, vv
-    paged = []
-    if args.page_size:
-        # the same keys scattered over pages in a seeded random order (two
-        # copies of the pools, used alternately like the caches above)
-        kp, vp, bt = workloads.paged_layout(kc, vc, args.page_size, seed=dcfg.seed + 7,
-                                            extra_pages=64)
-        paged = [(kp.to(dev), vp.to(dev), bt.to(dev)) for _ in range(2)]
-        del kp, vp, bt
-    bwd = []
-    if not args.no_bwd:
-        # backward on the prefill shape: the forward's bf16 O and LSE
-        # (computed once, untimed), a seeded dO, two input copies
-        gb = torch.Generator().manual_seed(pcfg.seed + 11)
-        dout = torch.randn((pcfg.B, pcfg.Hq, pcfg.S, pcfg.D), generator=gb).to(torch.bfloat16)
-        bws_bytes = mk.mk_attn_bwd_workspace_bytes(pcfg.B, pcfg.Hq, pcfg.S)
-        for i in range(2):
-            q_, k_, v_ = pre[i][:3]
-            o_, lse_ = mk.fwd(q_, k_, v_, causal=pcfg.causal, scale=pcfg.scale)
-            bwd.append((q_, k_, v_, o_, lse_, dout.to(dev), torch.empty_like(q_),
-                        torch.empty_like(k_), torch.empty_like(v_),
-                        torch.empty(bws_bytes, device=dev, dtype=torch.uint8)))
-        del dout
-    mla = []
-    MW = workloads.MLA
-    if not args.no_mla:
-        # MLA decode: 64 sequences, 16 heads, latent 512 + rotary 64; two
-        # copies of the latent cache, used alternately
-        mq, mckv, mlens = workloads.mla_inputs(MW["B"], MW["H"], MW["Dc"], MW["Dr"], MW["Smax"],
-                                               MW["seed"], MW["lmin"], MW["lmax"])
-        mws_bytes = mk.mk_attn_mla_decode_workspace_bytes(MW["H"], MW["Dc"], 0)
-        mla_bytes = (int(mlens.clamp(0, MW["Smax"]).sum()) * (MW["Dc"] + MW["Dr"]) * 2
-                     + MW["B"] * MW["H"] * ((MW["Dc"] + MW["Dr"]) * 2 + MW["Dc"] * 2 + 4))
-        mla = [(mq.to(dev), mckv.to(dev) if i == 0 else mckv.to(dev).clone(), mlens.to(dev),
-                torch.empty((MW["B"], MW["H"], MW["Dc"]), device=dev, dtype=torch.bfloat16),
-                torch.empty((MW["B"], MW["H"]), device=dev, dtype=torch.float32),
-                torch.empty(mws_bytes, device=dev, dtype=torch.uint8)) for i in range(2)]
-        del mq, mckv
-    del kc, vc
+    caches = [(kc.to(dev), vc.to(dev)), (kc.to(dev), vc.to(dev))]
     qd = qd.to(dev)
     lens_d = lens.to(dev)
     B, Hq, D = qd.shape
@@ -365,43 +501,13 @@ def main():
     ws = torch.empty(ws_bytes, device=dev, dtype=torch.uint8)
     od = torch.empty((B, Hq, D), device=dev, dtype=torch.bfloat16)
     lsed = torch.empty((B, Hq), device=dev, dtype=torch.float32)
-    torch.cuda.synchronize()
-
-    fwd_entry = mk.mk_attn_fwd_o32 if pcfg.out_fp32 else mk.mk_attn_fwd
-    stream = torch.cuda.current_stream()
-
-    def prefill(i):
-        q, k, v, o, lse = pre[i & 1]
-        fwd_entry(q, k, v, o, lse, pcfg.B, pcfg.Hq, pcfg.Hkv, pcfg.S, pcfg.S, pcfg.D, 1,
-                  pcfg.scale, None, stream)
+    sum_l = int(lens.clamp(0, Smax).sum())
+    dec_bytes = decode_alg_bytes(B, Hq, Hkv, D, sum_l)
 
     def decode(i):
         kcc, vcc = caches[i & 1]
         mk.mk_attn_decode(qd, kcc, vcc, od, lsed, B, Hq, Hkv, Smax, D, dcfg.scale, lens_d,
                           args.parts, ws, ws_bytes, stream)
-
-    def prefill_varlen(i):
-        vq_, vk_, vv_, vcu_, vo_, vl_ = varlen[i & 1]
-        mk.mk_attn_fwd_varlen(vq_, vk_, vv_, vo_, vl_, vcu_, vcu_, VL["B"], VL["Hq"], VL["Hkv"],
-                              max(vlens), vq_.shape[0], vk_.shape[0], VL["D"], 1,
-                              VL["D"] ** -0.5, stream)
-
-    def backward(i):
-        q_, k_, v_, o_, lse_, do_, dq_, dk_, dv_, bws_ = bwd[i & 1]
-        mk.mk_attn_bwd(q_, k_, v_, o_, do_, lse_, dq_, dk_, dv_, pcfg.B, pcfg.Hq, pcfg.Hkv,
-                       pcfg.S, pcfg.S, pcfg.D, int(pcfg.causal), pcfg.scale, None, bws_,
-                       bws_.numel(), stream)
-
-    def mla_decode(i):
-        mq_, mc_, ml_, mo_, mlse_, mws_ = mla[i & 1]
-        mk.mk_attn_mla_decode(mq_, mc_, mo_, mlse_, MW["B"], MW["H"], MW["Dc"], MW["Dr"],
-                              MW["Smax"], MW["scale"], ml_, 0, mws_, mws_.numel(), stream)
-
-    def decode_paged(i):
-        kp_, vp_, bt_ = paged[i & 1]
-        mk.mk_attn_decode_paged(qd, kp_, vp_, bt_, od, lsed, B, Hq, Hkv, args.page_size,
-                                bt_.shape[1], kp_.shape[0], D, dcfg.scale, lens_d, args.parts,
-                                ws, ws_bytes, stream)
 
     if args.calib_copy_mib:
         n = args.calib_copy_mib << 20
@@ -413,16 +519,14 @@ def main():
         log(f"[bench] calibration copy of {n} bytes done")
         del src, dst
 
+    # ---- the step: K prefill launches, then K decode launches ----
     log(f"[bench] warmup {args.warmup}")
     for i in range(args.warmup):
         prefill(i)
         decode(i)
     torch.cuda.synchronize()
-
     K = args.steps
-    # The K steps run as K prefill launches back to back, then K decode
-    # launches back to back (each alternating its two input copies), with
-    # one event before, between and after: a marker between two kernels
+    # One event before, between and after: a marker between two kernels
     # costs the command processor several microseconds, which per-launch
     # events would add to every launch's measured duration.
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
@@ -438,114 +542,185 @@ def main():
     ev[2].record(stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    varlen_ms = None
-    if varlen:
-        # the packed ragged prefill leg, timed after the step the same way
-        for i in range(args.warmup):
-            prefill_varlen(i)
-        evv = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-        torch.cuda.synchronize()
-        evv[0].record(stream)
-        for i in range(K):
-            prefill_varlen(i)
-        evv[1].record(stream)
-        torch.cuda.synchronize()
-        varlen_ms = evv[0].elapsed_time(evv[1]) / K
-    paged_ms = None
-    if paged:
-        # the paged-decode leg, timed after the step the same way
-        for i in range(args.warmup):
-            decode_paged(i)
-        evp = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-        torch.cuda.synchronize()
-        evp[0].record(stream)
-        for i in range(K):
-            decode_paged(i)
-        evp[1].record(stream)
-        torch.cuda.synchronize()
-        paged_ms = evp[0].elapsed_time(evp[1]) / K
-    bwd_ms = None
-    if bwd:
-        # the backward leg, timed after the step the same way
-        for i in range(args.warmup):
-            backward(i)
-        evb = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-        torch.cuda.synchronize()
-        evb[0].record(stream)
-        for i in range(K):
-            backward(i)
-        evb[1].record(stream)
-        torch.cuda.synchronize()
-        bwd_ms = evb[0].elapsed_time(evb[1]) / K
-    mla_ms = None
-    if mla:
-        # the MLA decode leg, timed after the step the same way
-        for i in range(args.warmup):
-            mla_decode(i)
-        evm = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-        torch.cuda.synchronize()
-        evm[0].record(stream)
-        for i in range(K):
-            mla_decode(i)
-        evm[1].record(stream)
-        torch.cuda.synchronize()
-        mla_ms = evm[0].elapsed_time(evm[1]) / K
-    long_ms, lcfg = None, None
-    if args.long:
-        # the long-context prefill leg: the same kernel on a long causal
-        # workload (two input copies alternating), a few launches after two
-        # untimed ones, timed after the step the same way
-        lcfg = workloads.CONFIGS[args.long]
-        lq, lk, lv = workloads.config_inputs(lcfg)
-        lin = []
-        for _ in range(2):
-            lin.append((lq.to(dev), lk.to(dev), lv.to(dev),
-                        torch.empty(lq.shape, device=dev,
-                                    dtype=torch.float32 if lcfg.out_fp32 else torch.bfloat16),
-                        torch.empty(lq.shape[:3], device=dev, dtype=torch.float32)))
-        del lq, lk, lv
-        lentry = mk.mk_attn_fwd_o32 if lcfg.out_fp32 else mk.mk_attn_fwd
-
-        def long_prefill(i):
-            q_, k_, v_, o_, l_ = lin[i & 1]
-            lentry(q_, k_, v_, o_, l_, lcfg.B, lcfg.Hq, lcfg.Hkv, lcfg.S, lcfg.S, lcfg.D, 1,
-                   lcfg.scale, None, stream)
-        for i in range(2):
-            long_prefill(i)
-        KL = max(2, min(K, 10))
-        evl = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-        torch.cuda.synchronize()
-        evl[0].record(stream)
-        for i in range(KL):
-            long_prefill(i)
-        evl[1].record(stream)
-        torch.cuda.synchronize()
-        long_ms = evl[0].elapsed_time(evl[1]) / KL
-        del lin
-        torch.cuda.empty_cache()
     ms_step = (t1 - t0) * 1e3 / K
-    pre_ms = ev[0].elapsed_time(ev[1]) / K  # average launch duration
-    dec_ms = ev[1].elapsed_time(ev[2]) / K
-    flops = pcfg.flops
-    tflops = flops / (pre_ms * 1e-3) / 1e12
-    sum_l = int(lens.clamp(0, Smax).sum())
-    dec_bytes = 4 * D * Hkv * sum_l + (B * Hq * D * 2) * 2 + B * Hq * 4  # K+V, q, o, lse
-    dec_gbs = dec_bytes / (dec_ms * 1e-3) / 1e9
-    log(f"[bench] prefill {pre_ms * 1e3:.1f} us ({tflops:.1f} TFLOP/s), "
-        f"decode {dec_ms * 1e3:.1f} us ({dec_gbs:.1f} GB/s), step {ms_step:.3f} ms"
-        + (f", varlen prefill {varlen_ms * 1e3:.1f} us" if varlen_ms is not None else "")
-        + (f", paged decode {paged_ms * 1e3:.1f} us" if paged_ms is not None else "")
-        + (f", backward {bwd_ms * 1e3:.1f} us" if bwd_ms is not None else "")
-        + (f", MLA decode {mla_ms * 1e3:.1f} us" if mla_ms is not None else "")
-        + (f", long prefill {long_ms * 1e3:.1f} us" if long_ms is not None else ""))
+    pre_ms = ev[0].elapsed_time(ev[1]) / K
+    dec_step_ms = ev[1].elapsed_time(ev[2]) / K
+    del pre
+    torch.cuda.empty_cache()
+    log(f"[bench] step: prefill {pcfg.name} {pre_ms * 1e3:.1f} us, decode {dec_step_ms * 1e3:.1f} "
+        f"us, {ms_step:.3f} ms per step")
 
-    digest = kernel_source_digest()
-    traffic_pre = read_traffic(f"fwd_kernel_{pcfg.name}_counters.md", digest)
-    traffic_dec = read_traffic(f"dec_part_kernel_{dcfg.name}_counters.md", digest)
+    def traffic_of(cfg_name, kernel="fwd_kernel"):
+        return read_traffic(f"{kernel}_{cfg_name}_counters.md", digest)
 
+    configs = {pcfg.name: prefill_record(pcfg, pre_ms * 1e3, traffic_of(pcfg.name))}
+
+    # ---- legs ----
+    dec_ms = None
+    if "decode" in legs:
+        # the decode alone, its figure independent of --steps: a fixed number
+        # of launches right after warm-up launches of its own
+        dec_ms = time_block(stream, decode, 50, args.decode_launches)
+        log(f"[bench] decode leg: {dec_ms * 1e3:.1f} us over {args.decode_launches} launches")
+    for leg, cname, warm, n in (("c3", "c3_gqa_s8k_k2", 2, 10), ("c2", "c2_mha_s2k", 20, 100),
+                                ("c1", "c1_mha_s128_d64", 20, 100)):
+        if leg not in legs or cname == pcfg.name:
+            continue
+        cfg = workloads.CONFIGS[cname]
+        bufs = prefill_inputs_on_device(cfg)
+        ms = time_block(stream, prefill_fn(cfg, bufs), warm, n)
+        configs[cname] = prefill_record(cfg, ms * 1e3, traffic_of(cname))
+        log(f"[bench] {cname}: {ms * 1e3:.1f} us ({configs[cname]['tflops']} TFLOP/s)")
+        del bufs
+        torch.cuda.empty_cache()
+    d_us = (dec_ms if dec_ms is not None else dec_step_ms) * 1e3
+    d_gbs = dec_bytes / (d_us * 1e-6) / 1e9
+    d_traffic = read_traffic(f"dec_part_kernel_{dcfg.name}_counters.md", digest)
+    configs[dcfg.name] = {
+        "workload": (f"{dcfg.name}: decode B={B} Hq={Hq} Hkv={Hkv} D={D} Smax={Smax} lengths "
+                     f"U[{dcfg.lmin},{dcfg.lmax}] (sum {sum_l}), split-KV in equal-work parts "
+                     "+ LSE merge"),
+        "us": round(d_us, 2),
+        "us_in_step": round(dec_step_ms * 1e3, 2),
+        "launches": args.decode_launches if dec_ms is not None else K,
+        "gbs": round(d_gbs, 1),
+        "frac_hbm_peak": round(d_gbs / PEAK_HBM_GBS, 4),
+        "alg_bytes": dec_bytes,
+        "tflops": round(16384 * sum_l / (d_us * 1e-6) / 1e12, 3),
+        "counter_bytes": d_traffic,
+        "counter_gbs": None if d_traffic is None else round(d_traffic / (d_us * 1e-6) / 1e9, 1),
+    }
+
+    extra = {}
+    if "varlen" in legs:
+        VL = dict(B=16, Hq=32, Hkv=8, D=128, lmin=256, lmax=8192, seed=1006)
+        vq, vk, vv, vcu = workloads.varlen_inputs(**VL)
+        vlens = (vcu[1:] - vcu[:-1]).tolist()
+        vb = [(vq.to(dev), vk.to(dev), vv.to(dev), vcu.to(dev),
+               torch.empty(vq.shape, device=dev, dtype=torch.bfloat16),
+               torch.empty((VL["Hq"], vq.shape[0]), device=dev, dtype=torch.float32))
+              for _ in range(2)]
+
+        def prefill_varlen(i):
+            q_, k_, v_, cu_, o_, l_ = vb[i & 1]
+            mk.mk_attn_fwd_varlen(q_, k_, v_, o_, l_, cu_, cu_, VL["B"], VL["Hq"], VL["Hkv"],
+                                  max(vlens), q_.shape[0], k_.shape[0], VL["D"], 1,
+                                  VL["D"] ** -0.5, stream)
+        ms = time_block(stream, prefill_varlen, 5, 20)
+        v_flops = 4 * VL["D"] * VL["Hq"] * sum(L * (L + 1) // 2 for L in vlens)
+        v_tf = v_flops / (ms * 1e-3) / 1e12
+        extra["varlen_prefill"] = {
+            "workload": (f"packed ragged causal prefill: B={VL['B']} sequences, lengths "
+                         f"U[{VL['lmin']},{VL['lmax']}] (total {sum(vlens)} tokens), "
+                         f"Hq={VL['Hq']} Hkv={VL['Hkv']} D={VL['D']}"),
+            "value": round(v_tf, 2), "unit": "TFLOP/s", "us": round(ms * 1e3, 2),
+            "flops": v_flops,
+            "roofline": {"bound": "mfma", "achieved": round(v_tf, 2), "peak": PEAK_BF16_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(v_tf / PEAK_BF16_TFLOPS, 4),
+                         "traffic": None},
+        }
+        log(f"[bench] varlen prefill: {ms * 1e3:.1f} us")
+        del vb, vq, vk, vv
+    if "paged" in legs:
+        # the decode's keys scattered over pages in a seeded random order
+        kp, vp, bt = workloads.paged_layout(kc, vc, args.page_size, seed=dcfg.seed + 7,
+                                            extra_pages=64)
+        pg = [(kp.to(dev), vp.to(dev), bt.to(dev)) for _ in range(2)]
+        del kp, vp, bt
+
+        def decode_paged(i):
+            kp_, vp_, bt_ = pg[i & 1]
+            mk.mk_attn_decode_paged(qd, kp_, vp_, bt_, od, lsed, B, Hq, Hkv, args.page_size,
+                                    bt_.shape[1], kp_.shape[0], D, dcfg.scale, lens_d,
+                                    args.parts, ws, ws_bytes, stream)
+        ms = time_block(stream, decode_paged, 20, 100)
+        p_gbs = dec_bytes / (ms * 1e-3) / 1e9
+        extra["paged_decode"] = {
+            "workload": (f"{dcfg.name} with its cache in {args.page_size}-key pages "
+                         "in a seeded random order (block table)"),
+            "value": round(p_gbs, 1), "unit": "GB/s", "us": round(ms * 1e3, 2),
+            "roofline": {"bound": "hbm", "achieved": round(p_gbs, 1), "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": round(p_gbs / PEAK_HBM_GBS, 4),
+                         "traffic": None},
+        }
+        log(f"[bench] paged decode: {ms * 1e3:.1f} us")
+        del pg
+    del caches
+    torch.cuda.empty_cache()
+    if "bwd" in legs:
+        # backward on the 2k workload's shape: the forward's bf16 O and LSE
+        # (computed once, untimed), a seeded dO, two input copies
+        bcfg = workloads.CONFIGS["c2_mha_s2k"]
+        gb = torch.Generator().manual_seed(bcfg.seed + 11)
+        dout = torch.randn((bcfg.B, bcfg.Hq, bcfg.S, bcfg.D), generator=gb).to(torch.bfloat16)
+        bws_bytes = mk.mk_attn_bwd_workspace_bytes(bcfg.B, bcfg.Hq, bcfg.S)
+        bb = []
+        for q_, k_, v_, _, _ in prefill_inputs_on_device(bcfg):
+            o_, lse_ = mk.fwd(q_, k_, v_, causal=True, scale=bcfg.scale)
+            bb.append((q_, k_, v_, o_, lse_, dout.to(dev), torch.empty_like(q_),
+                       torch.empty_like(k_), torch.empty_like(v_),
+                       torch.empty(bws_bytes, device=dev, dtype=torch.uint8)))
+
+        def backward(i):
+            q_, k_, v_, o_, lse_, do_, dq_, dk_, dv_, bws_ = bb[i & 1]
+            mk.mk_attn_bwd(q_, k_, v_, o_, do_, lse_, dq_, dk_, dv_, bcfg.B, bcfg.Hq, bcfg.Hkv,
+                           bcfg.S, bcfg.S, bcfg.D, 1, bcfg.scale, None, bws_, bws_.numel(),
+                           stream)
+        ms = time_block(stream, backward, 10, 50)
+        # the usual convention: 2.5 times the forward's FLOPs (five products
+        # of the forward's size: S, dP, dV, dK, dQ)
+        b_flops = 5 * bcfg.flops // 2
+        b_tf = b_flops / (ms * 1e-3) / 1e12
+        extra["backward"] = {
+            "workload": (f"{bcfg.name} backward: dQ, dK, dV from O, LSE and a seeded dO, causal "
+                         f"B={bcfg.B} Hq={bcfg.Hq} Hkv={bcfg.Hkv} S={bcfg.S} D={bcfg.D} bf16"),
+            "value": round(b_tf, 2), "unit": "TFLOP/s", "us": round(ms * 1e3, 2),
+            "flops": b_flops,
+            "roofline": {"bound": "mfma", "achieved": round(b_tf, 2), "peak": PEAK_BF16_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(b_tf / PEAK_BF16_TFLOPS, 4),
+                         "traffic": read_traffic(f"bwd_kernels_{bcfg.name}_counters.md",
+                                                 digest)},
+        }
+        log(f"[bench] backward: {ms * 1e3:.1f} us")
+        del bb, dout
+        torch.cuda.empty_cache()
+    if "mla" in legs:
+        MW = workloads.MLA
+        mq, mckv, mlens = workloads.mla_inputs(MW["B"], MW["H"], MW["Dc"], MW["Dr"], MW["Smax"],
+                                               MW["seed"], MW["lmin"], MW["lmax"])
+        mws_bytes = mk.mk_attn_mla_decode_workspace_bytes(MW["H"], MW["Dc"], 0)
+        mla_bytes = (int(mlens.clamp(0, MW["Smax"]).sum()) * (MW["Dc"] + MW["Dr"]) * 2
+                     + MW["B"] * MW["H"] * ((MW["Dc"] + MW["Dr"]) * 2 + MW["Dc"] * 2 + 4))
+        mb = [(mq.to(dev), mckv.to(dev), mlens.to(dev),
+               torch.empty((MW["B"], MW["H"], MW["Dc"]), device=dev, dtype=torch.bfloat16),
+               torch.empty((MW["B"], MW["H"]), device=dev, dtype=torch.float32),
+               torch.empty(mws_bytes, device=dev, dtype=torch.uint8)) for _ in range(2)]
+        del mq, mckv
+
+        def mla_decode(i):
+            mq_, mc_, ml_, mo_, mlse_, mws_ = mb[i & 1]
+            mk.mk_attn_mla_decode(mq_, mc_, mo_, mlse_, MW["B"], MW["H"], MW["Dc"], MW["Dr"],
+                                  MW["Smax"], MW["scale"], ml_, 0, mws_, mws_.numel(), stream)
+        ms = time_block(stream, mla_decode, 20, 100)
+        m_gbs = mla_bytes / (ms * 1e-3) / 1e9
+        extra["mla_decode"] = {
+            "workload": (f"{MW['name']}: MLA decode B={MW['B']} H={MW['H']} latent {MW['Dc']} + "
+                         f"rotary {MW['Dr']}, lengths U[{MW['lmin']},{MW['lmax']}], shared "
+                         "latent cache, split-KV (equal-work parts) + LSE merge"),
+            "value": round(m_gbs, 1), "unit": "GB/s", "us": round(ms * 1e3, 2),
+            "bytes": mla_bytes,
+            "roofline": {"bound": "hbm", "achieved": round(m_gbs, 1), "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": round(m_gbs / PEAK_HBM_GBS, 4),
+                         "traffic": read_traffic(f"mla_part_kernel_{MW['name']}_counters.md",
+                                                 digest)},
+        }
+        log(f"[bench] MLA decode: {ms * 1e3:.1f} us")
+        del mb
+
+    head = configs[pcfg.name]
     result = {
         "metric": "attention fwd TFLOP/s and % bf16 MFMA peak (prefill); HBM GB/s (decode)",
-        "value": round(tflops, 2),
+        "value": head["tflops"],
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": K,
@@ -557,142 +732,40 @@ def main():
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) bf16, generated on the host, resident in HBM)",
         "config": {
-            "workload": (f"{pcfg.name}: causal attention fwd B={pcfg.B} Hq={pcfg.Hq} "
-                         f"Hkv={pcfg.Hkv} S={pcfg.S} D={pcfg.D} bf16 in, "
-                         f"{'fp32' if pcfg.out_fp32 else 'bf16'} O + fp32 LSE; then "
-                         f"{dcfg.name}: decode B={B} Hq={Hq} Hkv={Hkv} D={D} "
-                         f"lengths U[{dcfg.lmin},{dcfg.lmax}] split-KV (equal-work parts) + LSE merge"),
-            "prefill_flops_per_step": flops,
+            "workload": (f"{head['workload']} + fp32 LSE; then {configs[dcfg.name]['workload']}"),
+            "prefill_flops_per_step": pcfg.flops,
             "decode_bytes_per_step": dec_bytes,
             "decode_sum_kv_len": sum_l,
             "kernel_source_digest": digest,
         },
-        "prefill_us": round(pre_ms * 1e3, 2),
+        "prefill_us": head["us"],
         "roofline": {
             "bound": "mfma",
-            "achieved": round(tflops, 2),
+            "achieved": head["tflops"],
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
-            "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
-            "traffic": traffic_pre,
+            "frac": head["frac_mfma_peak"],
+            "traffic": head["counter_bytes"],
         },
         "decode": {
-            "value": round(dec_gbs, 1),
+            "value": configs[dcfg.name]["gbs"],
             "unit": "GB/s",
-            "us": round(dec_ms * 1e3, 2),
+            "us": configs[dcfg.name]["us"],
             "roofline": {
                 "bound": "hbm",
-                "achieved": round(dec_gbs, 1),
+                "achieved": configs[dcfg.name]["gbs"],
                 "peak": PEAK_HBM_GBS,
                 "unit": "GB/s",
-                "frac": round(dec_gbs / PEAK_HBM_GBS, 4),
-                "traffic": traffic_dec,
+                "frac": configs[dcfg.name]["frac_hbm_peak"],
+                "traffic": d_traffic,
             },
         },
+        "configs": configs,
         "cpu_baseline": None,
     }
-    if varlen_ms is not None:
-        # causal pairs counted exactly: S (S + 1) / 2 per sequence and head
-        v_flops = 4 * VL["D"] * VL["Hq"] * sum(L * (L + 1) // 2 for L in vlens)
-        v_tf = v_flops / (varlen_ms * 1e-3) / 1e12
-        result["varlen_prefill"] = {
-            "workload": (f"packed ragged causal prefill: B={VL['B']} sequences, lengths "
-                         f"U[{VL['lmin']},{VL['lmax']}] (total {sum(vlens)} tokens), "
-                         f"Hq={VL['Hq']} Hkv={VL['Hkv']} D={VL['D']}"),
-            "value": round(v_tf, 2),
-            "unit": "TFLOP/s",
-            "us": round(varlen_ms * 1e3, 2),
-            "flops": v_flops,
-            "roofline": {"bound": "mfma", "achieved": round(v_tf, 2), "peak": PEAK_BF16_TFLOPS,
-                         "unit": "TFLOP/s", "frac": round(v_tf / PEAK_BF16_TFLOPS, 4),
-                         "traffic": None},
-        }
-    if paged_ms is not None:
-        p_gbs = dec_bytes / (paged_ms * 1e-3) / 1e9
-        result["paged_decode"] = {
-            "workload": (f"{dcfg.name} with its cache in {args.page_size}-key pages "
-                         "in a seeded random order (block table)"),
-            "value": round(p_gbs, 1),
-            "unit": "GB/s",
-            "us": round(paged_ms * 1e3, 2),
-            "roofline": {"bound": "hbm", "achieved": round(p_gbs, 1), "peak": PEAK_HBM_GBS,
-                         "unit": "GB/s", "frac": round(p_gbs / PEAK_HBM_GBS, 4),
-                         "traffic": None},
-        }
-
-    if bwd_ms is not None:
-        # the usual convention for attention backward: 2.5 times the
-        # forward's FLOPs (five products of the forward's size: S, dP, dV,
-        # dK, dQ); the dQ kernel recomputes S and dP, which is not counted
-        b_flops = 5 * pcfg.flops // 2
-        b_tf = b_flops / (bwd_ms * 1e-3) / 1e12
-        result["backward"] = {
-            "workload": (f"{pcfg.name} backward: dQ, dK, dV from O, LSE and a seeded dO, "
-                         f"{'causal' if pcfg.causal else 'non-causal'} B={pcfg.B} Hq={pcfg.Hq} "
-                         f"Hkv={pcfg.Hkv} S={pcfg.S} D={pcfg.D} bf16"),
-            "value": round(b_tf, 2),
-            "unit": "TFLOP/s",
-            "us": round(bwd_ms * 1e3, 2),
-            "flops": b_flops,
-            "roofline": {"bound": "mfma", "achieved": round(b_tf, 2), "peak": PEAK_BF16_TFLOPS,
-                         "unit": "TFLOP/s", "frac": round(b_tf / PEAK_BF16_TFLOPS, 4),
-                         "traffic": None},
-        }
-
-    if mla_ms is not None:
-        m_gbs = mla_bytes / (mla_ms * 1e-3) / 1e9
-        result["mla_decode"] = {
-            "workload": (f"{MW['name']}: MLA decode B={MW['B']} H={MW['H']} latent {MW['Dc']} + "
-                         f"rotary {MW['Dr']}, lengths U[{MW['lmin']},{MW['lmax']}], shared "
-                         "latent cache, split-KV (equal-work parts) + LSE merge"),
-            "value": round(m_gbs, 1),
-            "unit": "GB/s",
-            "us": round(mla_ms * 1e3, 2),
-            "bytes": mla_bytes,
-            "roofline": {"bound": "hbm", "achieved": round(m_gbs, 1), "peak": PEAK_HBM_GBS,
-                         "unit": "GB/s", "frac": round(m_gbs / PEAK_HBM_GBS, 4),
-                         "traffic": None},
-        }
-
-    if long_ms is not None:
-        l_tf = lcfg.flops / (long_ms * 1e-3) / 1e12
-        result["long_prefill"] = {
-            "workload": (f"{lcfg.name}: causal attention fwd B={lcfg.B} Hq={lcfg.Hq} "
-                         f"Hkv={lcfg.Hkv} S={lcfg.S} D={lcfg.D} bf16"),
-            "value": round(l_tf, 2),
-            "unit": "TFLOP/s",
-            "us": round(long_ms * 1e3, 1),
-            "roofline": {"bound": "mfma", "achieved": round(l_tf, 2), "peak": PEAK_BF16_TFLOPS,
-                         "unit": "TFLOP/s", "frac": round(l_tf / PEAK_BF16_TFLOPS, 4),
-                         "traffic": None},
-        }
-
-    if not args.no_cpu_baseline:
-        from oracle import oracle as orc  # timed CPU baseline only
-        qh, kh, vh = workloads.config_inputs(pcfg)
-        qb, kb, vb = workloads.bits(qh), workloads.bits(kh), workloads.bits(vh)
-        threads = orc.default_threads()
-        if args.cpu_rows and args.cpu_rows < pcfg.S:
-            rows = workloads.sample_rows(pcfg.B, pcfg.Hq, pcfg.S, args.cpu_rows,
-                                         seed=pcfg.seed + 7)
-            pairs = int((rows.long() + 1).sum())  # causal row i sees i+1 keys
-            rows_np, what = rows.numpy(), f"{args.cpu_rows} seeded query rows per head"
-        else:
-            rows_np, what = None, "every query row"
-            pairs = pcfg.B * pcfg.Hq * pcfg.pairs_per_head
-        log(f"[bench] cpu oracle baseline: {what} on {threads} threads")
-        c0 = time.perf_counter()
-        orc.attn_fwd(qb, kb, vb, causal=True, scale=pcfg.scale, rows=rows_np, threads=threads)
-        c1 = time.perf_counter()
-        cpu_tflops = 4 * pcfg.D * pairs / (c1 - c0) / 1e12
-        result["cpu_baseline"] = {
-            "value": cpu_tflops,
-            "unit": "TFLOP/s",
-            "cores": threads,
-            "kind": "oracle",
-            "sample": (f"{what} of {pcfg.name} ({pairs} query-key pairs, fp64, "
-                       f"{c1 - c0:.2f} s)"),
-        }
+    result.update(extra)
+    if args.cpu_baseline != "none":
+        result["cpu_baseline"] = cpu_baselines(args, sum_l)
     print(json.dumps(result), flush=True)
 
 

@@ -134,7 +134,14 @@ int mk_attn_fwd_varlen(const void *q, const void *k, const void *v, void *o, flo
  *   fit in 31 bits (MK_ERR_SHAPE otherwise).
  *   n_parts           waves the key stream is cut into, 1 .. 2^20
  *                     (0 = mk_attn_decode_default_parts(Hq, Hkv, D));
- *                     any value gives the same result up to rounding
+ *                     any value gives the same result up to rounding.
+ *                     There is no "keys per split" argument: the stream's
+ *                     length depends on kv_seqlens, which lives on the
+ *                     device, so keys per part are fixed inside the kernel
+ *                     (about 32 * Hkv * sum_b ceil(L_b / 32) / n_parts).
+ *   Groups wider than 16 query heads per kv head (Hq / Hkv > 16) return
+ *   MK_ERR_UNSUPPORTED: a pair's query heads are the columns of one
+ *   16-wide matrix-core block.
  *   workspace         device buffer, 256-byte aligned, of workspace_bytes >=
  *                     mk_attn_decode_workspace_bytes(Hq, Hkv, D, n_parts);
  *                     its contents need no initialisation and are left

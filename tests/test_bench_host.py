@@ -104,3 +104,41 @@ def test_summarize_trace_splits_one_kernel_by_grid(tmp_path):
     small = [c.strip() for c in rows["mk::fwd_kernel<128, true, false, 1, true, false> "
                                      "[1024 workgroups]"].split("|")]
     assert small[2] == "2" and small[3] == "81.00"
+
+
+def test_summarize_pmc_splits_one_kernel_by_grid(tmp_path):
+    """'name@N' selects the launches of a kernel with N workgroups, so one
+    forward kernel timed on two workloads gets one traffic figure each."""
+    calib = 1 << 30
+
+    def db(path, counter, copy_val, vals):
+        os.makedirs(path)
+        con = sqlite3.connect(os.path.join(path, "x_results.db"))
+        con.execute("create table kernels (dispatch_id integer, name text, duration integer, "
+                    "grid_x integer, workgroup_x integer)")
+        con.execute("create table pmc_events (dispatch_id integer, name text, "
+                    "counter_name text, counter_value real)")
+        con.executemany("insert into kernels values (?, ?, ?, ?, ?)",
+                        [(1, COPY, 1, 4096 * 256, 256), (2, FWD, 1, 1024 * 256, 256),
+                         (3, FWD, 1, 8192 * 256, 256), (4, FWD, 1, 1024 * 256, 256)])
+        con.executemany("insert into pmc_events values (?, ?, ?, ?)",
+                        [(1, COPY, counter, copy_val)] +
+                        [(d, FWD, counter, v) for d, v in zip((2, 3, 4), vals)])
+        con.commit()
+        con.close()
+        return path
+    fetch = db(str(tmp_path / "f"), "FETCH_SIZE", calib / 1024 / 2, (100.0, 9000.0, 300.0))
+    write = db(str(tmp_path / "w"), "WRITE_SIZE", calib / 1024, (50.0, 4000.0, 50.0))
+    small = bench.summarize_pmc(fetch, write, ["fwd_kernel@1024"], calib, ["c"])
+    big = bench.summarize_pmc(fetch, write, ["fwd_kernel@8192"], calib, ["c"])
+    t_small = float(small.split("hbm_bytes_per_launch:")[1].split()[0])
+    t_big = float(big.split("hbm_bytes_per_launch:")[1].split()[0])
+    assert t_small == pytest.approx(200.0 * 1024 * 2 + 50.0 * 1024)
+    assert t_big == pytest.approx(9000.0 * 1024 * 2 + 4000.0 * 1024)
+
+
+def test_unknown_leg_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--legs", "c9"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode != 0
+    assert "unknown legs" in r.stderr
