@@ -52,7 +52,8 @@ typedef enum {
     MK_ERR_ALIGN = 4,       /* a pointer is not aligned as required */
     MK_ERR_WORKSPACE = 5,   /* workspace missing or too small */
     MK_ERR_HIP = 6,         /* the HIP runtime refused a launch */
-    MK_ERR_ARG = 7          /* non-finite scale, bad causal flag or part count */
+    MK_ERR_ARG = 7,         /* non-finite scale, bad causal flag or part count */
+    MK_ERR_SCRATCH = 8      /* more decode scratch needed than the fixed array holds */
 } mk_status;
 
 /*
@@ -152,6 +153,33 @@ int mk_attn_decode(const void *q, const void *k_cache, const void *v_cache, void
                    float *lse, int B, int Hq, int Hkv, int Smax, int D, float scale,
                    const int *kv_seqlens, int n_parts, void *workspace,
                    size_t workspace_bytes, void *stream);
+
+/*
+ * Decode step that allocates nothing, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): mk_attn_decode with the workspace
+ * taken from a fixed device array inside the library (16 MiB, one copy per
+ * GPU, held until the process ends) instead of a caller's buffer.
+ *   Arguments as mk_attn_decode, without workspace and workspace_bytes.
+ *   The stream must belong to the current device (MK_ERR_ARG otherwise).
+ *   The first call on a device looks up that device's copy of the array
+ *   (hipGetSymbolAddress, with the device current); make it outside any
+ *   graph capture.  No call allocates or frees memory.
+ *   Returns MK_ERR_SCRATCH when mk_attn_decode_workspace_bytes(Hq, Hkv, D,
+ *   n_parts) exceeds mk_attn_decode_noalloc_max_bytes(); nothing is
+ *   launched then.
+ * Every call on one GPU shares that GPU's array, and the array keeps the
+ * last call's contents (nothing in it needs clearing: each call writes
+ * every entry it reads).  Calls that may overlap in time on one GPU (on
+ * different streams, or from different threads) race on it: serialise
+ * them.  The result is mk_attn_decode's bit for bit.
+ */
+int mk_attn_decode_noalloc(const void *q, const void *k_cache, const void *v_cache, void *o,
+                           float *lse, int B, int Hq, int Hkv, int Smax, int D, float scale,
+                           const int *kv_seqlens, int n_parts, void *stream);
+
+/* Bytes of the fixed array mk_attn_decode_noalloc uses (16 MiB). */
+size_t mk_attn_decode_noalloc_max_bytes(void);
 
 /*
  * Decode step over a paged key/value cache (the paper's "Paged Attention"

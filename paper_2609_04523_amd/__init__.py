@@ -20,11 +20,13 @@ LIB_PATH = os.path.join(_PKG, "libmk_attn.so")
 DECODE_MAX_PARTS = 1 << 20  # largest n_parts
 
 MK_STATUS = {0: "MK_OK", 1: "MK_ERR_NULL", 2: "MK_ERR_SHAPE", 3: "MK_ERR_UNSUPPORTED",
-             4: "MK_ERR_ALIGN", 5: "MK_ERR_WORKSPACE", 6: "MK_ERR_HIP", 7: "MK_ERR_ARG"}
+             4: "MK_ERR_ALIGN", 5: "MK_ERR_WORKSPACE", 6: "MK_ERR_HIP", 7: "MK_ERR_ARG",
+             8: "MK_ERR_SCRATCH"}
 
 # every symbol include/mk_attn.h declares
 EXPORTS = ("mk_attn_fwd", "mk_attn_fwd_o32", "mk_attn_fwd_varlen",
            "mk_attn_decode_workspace_bytes", "mk_attn_decode", "mk_attn_decode_paged",
+           "mk_attn_decode_noalloc", "mk_attn_decode_noalloc_max_bytes",
            "mk_attn_decode_default_parts", "mk_attn_bwd", "mk_attn_bwd_workspace_bytes",
            "mk_attn_mla_decode", "mk_attn_mla_decode_workspace_bytes",
            "mk_status_str", "mk_attn_version")
@@ -59,6 +61,10 @@ def lib():
         h.mk_attn_decode_workspace_bytes.restype = sz
         h.mk_attn_decode.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, f, vp, i, vp, sz, vp]
         h.mk_attn_decode.restype = i
+        h.mk_attn_decode_noalloc.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, f, vp, i, vp]
+        h.mk_attn_decode_noalloc.restype = i
+        h.mk_attn_decode_noalloc_max_bytes.argtypes = []
+        h.mk_attn_decode_noalloc_max_bytes.restype = sz
         h.mk_attn_decode_paged.argtypes = [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, vp, i,
                                            vp, sz, vp]
         h.mk_attn_decode_paged.restype = i
@@ -155,6 +161,17 @@ def mk_attn_decode(q, k_cache, v_cache, o, lse, B, Hq, Hkv, Smax, D, scale, kv_s
     _check(lib().mk_attn_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(o), _ptr(lse), B,
                                 Hq, Hkv, Smax, D, float(scale), _ptr(kv_seqlens), int(n_parts),
                                 _ptr(workspace), int(workspace_bytes), _stream(stream)))
+
+
+def mk_attn_decode_noalloc(q, k_cache, v_cache, o, lse, B, Hq, Hkv, Smax, D, scale, kv_seqlens,
+                           n_parts, stream=None):
+    _check(lib().mk_attn_decode_noalloc(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(o),
+                                        _ptr(lse), B, Hq, Hkv, Smax, D, float(scale),
+                                        _ptr(kv_seqlens), int(n_parts), _stream(stream)))
+
+
+def mk_attn_decode_noalloc_max_bytes() -> int:
+    return int(lib().mk_attn_decode_noalloc_max_bytes())
 
 
 def mk_attn_decode_paged(q, k_pages, v_pages, block_table, o, lse, B, Hq, Hkv, page_size,

@@ -2,9 +2,12 @@
 //
 // Validates arguments on the host, picks the kernel instantiation
 // (head dim, causal flag, output type) and enqueues on the caller's
-// stream.  No allocation, no synchronisation, no global mutable state.
+// stream.  No allocation and no synchronisation.  The only state is the
+// per-device address of the fixed decode scratch (set once per device).
 #include <math.h>
 #include <stdint.h>
+
+#include <mutex>
 
 #include "../../include/mk_attn.h"
 #include "launch.hpp"
@@ -12,10 +15,23 @@
 
 namespace {
 
-constexpr int kVersion = 6;
+constexpr int kVersion = 7;
 constexpr int kComputeUnits = 256;    // MI355X
 constexpr int kLdsPerCu = 160 * 1024; // gfx950
 constexpr int kMaxParts = 1 << 20;    // decode parts per call
+
+// Scratch of the allocation-free decode entry point: a fixed device array,
+// one copy on every GPU the library runs on, held until the process ends.
+// Host code must never pass `scratch` itself to a kernel (on the host the
+// name stands for a host-side shadow, not a device address): its device
+// address is looked up once per device and kept in scratch_ptr.
+constexpr size_t kScratchBytes = (size_t)16 << 20;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+void* scratch_ptr[kMaxDevices];
+hipError_t scratch_err[kMaxDevices];
+std::once_flag scratch_once[kMaxDevices];
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -289,6 +305,40 @@ int mk_attn_decode(const void* q, const void* k_cache, const void* v_cache, void
   return e == hipSuccess ? MK_OK : MK_ERR_HIP;
 }
 
+int mk_attn_decode_noalloc(const void* q, const void* k_cache, const void* v_cache, void* o,
+                           float* lse, int B, int Hq, int Hkv, int Smax, int D, float scale,
+                           const int* kv_seqlens, int n_parts, void* stream) {
+  // validate as mk_attn_decode would with a workspace of the scratch's size
+  // (a stand-in address: nothing is launched unless every check passes)
+  DecLayout l;
+  int rc = dec_check(q, k_cache, v_cache, o, lse, B, Hq, Hkv, Smax, D, scale, kv_seqlens,
+                     n_parts, reinterpret_cast<void*>(uintptr_t{256}), kScratchBytes, &l);
+  if (rc == MK_ERR_WORKSPACE) return MK_ERR_SCRATCH;
+  if (rc != MK_OK) return rc;
+  // the device the work runs on: the stream's, which must be the current one
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return MK_ERR_HIP;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (st) {
+    int sdev = -1;
+    if (hipStreamGetDevice(st, &sdev) != hipSuccess) return MK_ERR_HIP;
+    if (sdev != dev) return MK_ERR_ARG;
+  }
+  if (dev >= kMaxDevices) return MK_ERR_UNSUPPORTED;
+  std::call_once(scratch_once[dev], [dev] {
+    void* p = nullptr;
+    scratch_err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    scratch_ptr[dev] = p;
+  });
+  if (scratch_err[dev] != hipSuccess || scratch_ptr[dev] == nullptr) return MK_ERR_HIP;
+  const mk::DecArgs a = dec_args(q, k_cache, v_cache, o, lse, B, Hq, Hkv, Smax, scale,
+                                 kv_seqlens, l, scratch_ptr[dev]);
+  const hipError_t e = mk::launch_decode(a, D, dec_qblocks(D, Hq / Hkv), false, st);
+  return e == hipSuccess ? MK_OK : MK_ERR_HIP;
+}
+
+size_t mk_attn_decode_noalloc_max_bytes(void) { return kScratchBytes; }
+
 int mk_attn_decode_paged(const void* q, const void* k_pages, const void* v_pages,
                          const int* block_table, void* o, float* lse, int B, int Hq, int Hkv,
                          int page_size, int max_pages, int n_pages, int D, float scale,
@@ -392,6 +442,9 @@ const char* mk_status_str(int status) {
     case MK_ERR_WORKSPACE: return "MK_ERR_WORKSPACE: workspace missing or too small";
     case MK_ERR_HIP: return "MK_ERR_HIP: the HIP runtime refused a launch";
     case MK_ERR_ARG: return "MK_ERR_ARG: non-finite scale, bad causal flag or part count";
+    case MK_ERR_SCRATCH:
+      return "MK_ERR_SCRATCH: the request needs more decode scratch than the "
+             "allocation-free entry point holds (use mk_attn_decode with a workspace)";
     default: return "MK_ERR_UNKNOWN: not an mk_status value";
   }
 }

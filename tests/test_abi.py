@@ -43,9 +43,9 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert mk.mk_attn_version() == 6
+    assert mk.mk_attn_version() == 7
     names = ["MK_OK", "MK_ERR_NULL", "MK_ERR_SHAPE", "MK_ERR_UNSUPPORTED", "MK_ERR_ALIGN",
-             "MK_ERR_WORKSPACE", "MK_ERR_HIP", "MK_ERR_ARG"]
+             "MK_ERR_WORKSPACE", "MK_ERR_HIP", "MK_ERR_ARG", "MK_ERR_SCRATCH"]
     for code, name in enumerate(names):
         assert mk.mk_status_str(code).startswith(name)
         assert mk.MK_STATUS[code] == name
@@ -137,6 +137,34 @@ def test_decode_validation(lib):
     assert dec_rc(lib, ws_bytes=need - 1) == 5
     assert dec_rc(lib, parts=100, ws_bytes=lib.mk_attn_decode_workspace_bytes(8, 2, 128, 99)) == 5
     assert dec_rc(lib, ws=P + 16) == 4  # workspace must be 256-byte aligned
+
+
+def noalloc_rc(lib, *, q=P, kc=P, vc=P, o=P, lse=None, B=2, Hq=8, Hkv=2, Smax=512, D=128,
+               scale=0.1, seqlens=P, parts=0):
+    return lib.mk_attn_decode_noalloc(q, kc, vc, o, lse, B, Hq, Hkv, Smax, D, scale, seqlens,
+                                      parts, None)
+
+
+def test_decode_noalloc_validation(lib):
+    # every check runs on the host before any HIP call, so nothing here
+    # reaches the device
+    assert lib.mk_attn_decode_noalloc_max_bytes() == 16 << 20
+    for name in ("q", "kc", "vc", "o", "seqlens"):
+        assert noalloc_rc(lib, **{name: None}) == 1
+    for name in ("B", "Hq", "Hkv", "Smax"):
+        assert noalloc_rc(lib, **{name: 0}) == 2
+    assert noalloc_rc(lib, D=96) == 3
+    assert noalloc_rc(lib, Hq=34, Hkv=2) == 3
+    assert noalloc_rc(lib, parts=-1) == 7
+    assert noalloc_rc(lib, scale=math.nan) == 7
+    for name in ("q", "kc", "vc", "o"):
+        assert noalloc_rc(lib, **{name: P_ODD}) == 4
+    # a part count whose workspace passes the fixed array's size
+    cap = lib.mk_attn_decode_noalloc_max_bytes()
+    big = 1
+    while lib.mk_attn_decode_workspace_bytes(32, 2, 128, big) <= cap:
+        big *= 2
+    assert noalloc_rc(lib, Hq=32, Hkv=2, parts=big) == 8
 
 
 def paged_rc(lib, *, q=P, kp=P, vp=P, bt=P, o=P, lse=None, B=2, Hq=8, Hkv=2, ps=16,
