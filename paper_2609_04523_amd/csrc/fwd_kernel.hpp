@@ -64,9 +64,9 @@ __device__ __forceinline__ void fwd_seq_range(const int* cu, int b, int total, i
   len = s1 > s0 ? s1 - s0 : 0;
 }
 
-template <int D, int QB>
+template <int D, int QB, int WAVES_ = 4>
 struct FwdShape {
-  static constexpr int WAVES = 4;
+  static constexpr int WAVES = WAVES_;
   static constexpr int THREADS = WAVES * 64;
   static constexpr int BM = WAVES * 32 * QB;              // query rows per workgroup
   static constexpr int BN = 64;                           // keys per LDS tile
@@ -117,9 +117,9 @@ __device__ __forceinline__ void fwd_map_block(int bid, const FwdArgs& a, int& qt
 // the scale folded into the exponent's FMA.  Otherwise scores are scaled
 // first (scale 0 and negative scales).  VARLEN: a packed ragged batch (see
 // FwdArgs); only where rows live changes, the tile pipeline is the same.
-template <int D, bool CAUSAL, bool OUT_F32, int QB, bool POS_SCALE, bool VARLEN>
-__global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
-  using S = FwdShape<D, QB>;
+template <int D, bool CAUSAL, bool OUT_F32, int QB, bool POS_SCALE, bool VARLEN, int WAVES>
+__global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
+  using S = FwdShape<D, QB, WAVES>;
   constexpr int BN = S::BN;
   constexpr int TILE = BN * D;            // bf16 per tile per tensor
   constexpr int TILE_BYTES = TILE * 2;
@@ -128,8 +128,12 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   constexpr int NV = 8 * S::DBLK;       // transposing V reads per tile
   constexpr int RW = POS_SCALE ? 8 : 4;  // LDS reads in flight (fewer registers otherwise)
   static_assert(RW >= 2 && RW % 2 == 0 && RW <= NK && RW <= NV, "read window");
-  __shared__ __attribute__((aligned(1024))) uint16_t k_lds[2][TILE];
-  __shared__ __attribute__((aligned(1024))) uint16_t v_lds[2][TILE];
+  // K tile buffers 0 and 1, then V tile buffers 0 and 1, contiguous (the
+  // epilogue stages the output rows of all waves through them)
+  __shared__ __attribute__((aligned(1024))) uint16_t kv_lds[4][TILE];
+  uint16_t(*const k_lds)[TILE] = kv_lds;
+  uint16_t(*const v_lds)[TILE] = kv_lds + 2;
+  static_assert(S::WAVES * 32 * QB * D * 2 <= 4 * TILE_BYTES, "output staging fits the tiles");
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -217,20 +221,20 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   const uint32_t v_lds_w = __builtin_amdgcn_readfirstlane(lds_addr(&v_lds[0][0]) + wave * 1024);
   // Block p of tile kt of one tensor (K or V) into LDS buffer BUF.  FULL:
   // the tile lies inside the sequence, so no row needs clamping: the load
-  // goes through a buffer resource on the tile with the precomputed lane
-  // offset full_off[p].
-  uint32_t full_off[S::BLOCKS_PER_WAVE];
-#pragma unroll
-  for (int p = 0; p < S::BLOCKS_PER_WAVE; ++p)
-    full_off[p] = (uint32_t)((dma_row + p * ROW_STEP) * kv_stride + dma_ch);
+  // goes through a buffer resource on the tile with the lane offset
+  // full_off and the block's (wave-uniform) offset p * ROW_STEP rows.
+  const uint32_t full_off = (uint32_t)(dma_row * kv_stride + dma_ch);
   auto issue_rows = [&](const char* g, uint32_t lds_w, int kt, auto buf_tag, auto p_tag,
                         auto full_tag) {
     constexpr int BUF = decltype(buf_tag)::value;
     constexpr int P = decltype(p_tag)::value;
     constexpr uint32_t lds_off = BUF * TILE_BYTES + P * S::WAVES * 1024;
-    const char* tile = g + (size_t)kt * BN * kv_stride;
+    // kt is the same in every lane; saying so keeps the tile address, and so
+    // the load's buffer resource, in scalar registers
+    const char* tile = g + (size_t)__builtin_amdgcn_readfirstlane(kt) * BN * kv_stride;
     if constexpr (decltype(full_tag)::value) {
-      load_lds16_buf(tile, (uint32_t)(BN * kv_stride), full_off[P], lds_w + lds_off);
+      load_lds16_buf(tile, (uint32_t)(BN * kv_stride), full_off, lds_w + lds_off,
+                     (uint32_t)(P * ROW_STEP * kv_stride));
     } else {
       const int lim = L - 1 - kt * BN;  // last valid row of the tile
       const uint32_t goff = (uint32_t)(min(dma_row, lim - P * ROW_STEP) * kv_stride + dma_ch) +
@@ -290,132 +294,305 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
   n_live = (max(n_live, 0) + BN - 1) / BN;
   n_free = max(0, min(n_free, n_live));
 
-  // Scores of even and odd tiles: step t forms those of tile t while it
-  // turns those of tile t - 1 into weights.
+  // Scores (fp32) and weights (bf16 P^T fragments) of even and odd tiles.
+  // Step t forms the scores of tile t, turns those of tile t - 1 into
+  // weights and adds the weights of tile t - 2 times V into O.
   f32x16 s_even[QB][2], s_odd[QB][2];
-  float m_use[QB];  // exponent offset for the weights of the last scored tile
+  u32x4 p_even[QB][4], p_odd[QB][4];  // bf16 bits (carried as integers)
+  float m_use[QB];  // exponent offset of the weights being formed
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) m_use[qb] = 0.f;
 
-  // Step t (t = 0 .. n_kt) of the pipeline, for one wave:
-  //   QK (t < n_live):       S(t) = K(t) Q^T on the matrix cores, with the
-  //                          exponentials of tile t - 1 issued in between
-  //                          (PV), then the softmax head of tile t (MASK:
-  //                          tile t needs the length / causal mask): row
-  //                          max and lazy rescale;
-  //   PV (1 <= t <= n_live): O += P V(t-1), with the head of tile t issued
-  //                          in between (QK).
-  // K(t) sits in K buffer t % 2 and V(t - 1) in V buffer (t - 1) % 2; the
-  // step loads K(t + 1) and V(t) into the other two buffers, spread over
-  // its score products.  STEADY: both loads are due and both tiles are full
-  // (t + 1 < n_full), so they are issued without a branch that would split
-  // the products' schedule and without row clamping (used for unmasked
-  // tiles, the bulk of the work).
-  auto step = [&](int t, auto par_tag, auto qk_tag, auto pv_tag, auto mask_tag, auto steady_tag) {
+  // Step t (t = 0 .. n_kt + 1) of the pipeline, for one wave:
+  //   A  PV (2 <= t <= n_live + 1): O += P(t-2) V(t-2) on the matrix cores,
+  //      with the weights of tile t - 1 (first half of its keys) formed in
+  //      between; HEAD: tile t - 1 first gets its row maximum (MASK: the
+  //      length / causal mask too) and the lazy rescale, whose factor
+  //      reaches O once the products of tile t - 2 are in;
+  //   B  QK (t < n_live): S(t) = K(t) Q^T, with the second half of the
+  //      weights of tile t - 1 formed in between;
+  //   then the check of tile t - 1's weights (EX: 1 <= t <= n_live).
+  // Every product thus has about one exponential and three other vector
+  // operations beside it, so the vector work of a wave runs under its own
+  // matrix work.  K(t) sits in K buffer t % 2 and V(t - 2) in V buffer t % 2;
+  // the step loads K(t + 1) and V(t - 1) into the other two, spread over
+  // its first products.  STEADY: both loads are due, both tiles lie inside
+  // the sequence and the step has both phases without a head, so the loads
+  // go out unconditionally and the products form one schedulable block.
+  auto step = [&](int t, auto par_tag, auto qk_tag, auto ex_tag, auto pv_tag, auto head_tag,
+                  auto mask_tag, auto steady_tag) {
     constexpr int PAR = decltype(par_tag)::value;
     constexpr bool QK = decltype(qk_tag)::value;
+    constexpr bool EX = decltype(ex_tag)::value;
     constexpr bool PV = decltype(pv_tag)::value;
+    constexpr bool HEAD = decltype(head_tag)::value;
     constexpr bool MASK = decltype(mask_tag)::value;
     constexpr bool STEADY = decltype(steady_tag)::value;
-    // MAXP: tile t gets its row maximum (and the lazy rescale) in this step.
-    // Unmasked tiles after the first skip it when scale > 0: their weights
-    // are formed against the running maximum and checked by their sums.
-    constexpr bool MAXP = MASK || !PV || !POS_SCALE;
-    constexpr int KBUF = PAR, VBUF = 1 - PAR;
-    auto& s_new = pick<PAR>(s_even, s_odd);
-    auto& s_old = pick<1 - PAR>(s_even, s_odd);
+    static_assert(EX || !HEAD, "a head belongs to a tile being weighed");
+    auto& s_new = pick<PAR>(s_even, s_odd);      // S(t)
+    auto& s_old = pick<1 - PAR>(s_even, s_odd);  // S(t - 1), turned into weights
+    auto& p_new = pick<1 - PAR>(p_even, p_odd);  // P(t - 1)
+    auto& p_old = pick<PAR>(p_even, p_odd);      // P(t - 2)
+    const int tw = t - 1;                        // the tile being weighed
+    // A step that forms no scores (no weights) still gives the array a
+    // value: otherwise the contents of two steps back would stay live
+    // through every step, since the compiler cannot see that no later step
+    // reads them.
+    if constexpr (!QK) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) s_new[qb][kb][r] = 0.f;
+    }
+    if constexpr (!EX) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) p_new[qb][kc] = u32x4{0u, 0u, 0u, 0u};
+    }
     const bool load_k = t + 1 < n_kt;
-    const bool load_v = t < n_kt;
+    const bool load_v = t >= 1 && t - 1 < n_kt;
     auto load_block = [&](auto p_tag) {
-      using KB_ = std::integral_constant<int, 1 - PAR>;
-      using VB_ = std::integral_constant<int, PAR>;
-      if (STEADY || load_k) issue_rows(kg, k_lds_w, t + 1, KB_(), p_tag, steady_tag);
-      if (STEADY || load_v) issue_rows(vg, v_lds_w, t, VB_(), p_tag, steady_tag);
+      using NB_ = std::integral_constant<int, 1 - PAR>;
+      if (STEADY || load_k) issue_rows(kg, k_lds_w, t + 1, NB_(), p_tag, steady_tag);
+      if (STEADY || load_v) issue_rows(vg, v_lds_w, t - 1, NB_(), p_tag, steady_tag);
     };
 
-    // ---- LDS read stream: the NK K fragments of tile t (key block kb,
-    // then step s: the scores of key block 1 need registers only once the
-    // weights of key block 0 of tile t - 1 are formed), then the NV
-    // transposing V reads of tile t - 1 in the order the products consume
-    // them.  RS reads are kept in flight: consuming one issues the next.  The
-    // first ones go out before the softmax head, ahead of their products. ----
-    constexpr int NKS = QK ? NK : 0;
+    // ---- LDS read stream: the NV transposing V reads of tile t - 2 in the
+    // order the products consume them, then the NK K fragments of tile t
+    // (key block kb, then step s).  RS reads are kept in flight: consuming
+    // one issues the next. ----
     constexpr int NVS = PV ? NV : 0;
-    constexpr int TOT = NKS + NVS;
+    constexpr int NKS = QK ? NK : 0;
+    constexpr int TOT = NVS + NKS;
     constexpr int RS = RW < TOT ? RW : TOT;
-    u32x4 kr[NK];
     u32x2 vr[NV];
+    u32x4 kr[NK];
     auto issue_read = [&](auto j_tag) {
       constexpr int J = decltype(j_tag)::value;
-      if constexpr (J < NKS) {
-        constexpr int OFF = KBUF * TILE_BYTES + (J / S::KSTEPS) * 32 * ROW_BYTES;
-        kr[J] = lds_read_b128_async_off<OFF>(k_addr[J % S::KSTEPS]);
+      if constexpr (J < NVS) {
+        constexpr int OFF = PAR * TILE_BYTES + (J / (2 * S::DBLK)) * 16 * ROW_BYTES;
+        vr[J] = lds_read_tr16_async_off<OFF>(v_addr[(J / 2) % S::DBLK][J % 2]);
       } else if constexpr (J < TOT) {
-        constexpr int V = J - NKS;  // (kc, db, hh) = V / (2 DBLK), V / 2 % DBLK, V % 2
-        constexpr int OFF = VBUF * TILE_BYTES + (V / (2 * S::DBLK)) * 16 * ROW_BYTES;
-        vr[V] = lds_read_tr16_async_off<OFF>(v_addr[(V / 2) % S::DBLK][V % 2]);
+        constexpr int K = J - NVS;
+        constexpr int OFF = PAR * TILE_BYTES + (K / S::KSTEPS) * 32 * ROW_BYTES;
+        kr[K] = lds_read_b128_async_off<OFF>(k_addr[K % S::KSTEPS]);
       }
     };
     static_for<0, RS>(issue_read);
 
-    // Weights of 16-key chunk kc of tile t - 1 (accumulator rows
-    // 8 (kc % 2) .. +7 of key block kc / 2) as the bf16 P^T fragment, and
-    // their sum.
+    // ---- weights of tile t - 1: chunk kc = keys 16 kc .. 16 kc + 15
+    // (accumulator rows 8 (kc % 2) .. +7 of key block kc / 2) ----
     const float cc = POS_SCALE ? c : 1.f;
-    bf16x8 pf[QB][4];
     float l_tile[QB];  // this lane's share of the row sums of tile t - 1
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) l_tile[qb] = 0.f;
-    // The exponentials of chunk kc come in PER_EXP parts (one per score
-    // product they are interleaved with); exp_finish then forms the chunk's
-    // fragment and sum.
-    constexpr int PER_EXP = NK / 4;   // score products per weight chunk
-    constexpr int EPP = 8 / PER_EXP;  // exponentials per part
-    static_assert(NK % 4 == 0 && 8 % PER_EXP == 0, "exponential spacing");
-    auto exp_part = [&](auto kc_tag, auto j_tag) {
+    auto exp_one = [&](auto kc_tag, auto e_tag) {
       constexpr int KC = decltype(kc_tag)::value;
-      constexpr int J = decltype(j_tag)::value;
+      constexpr int R = 8 * (KC % 2) + decltype(e_tag)::value;
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-        for (int e = 0; e < EPP; ++e) {
-          constexpr int R = 8 * (KC % 2) + J * EPP;
-          s_old[qb][KC / 2][R + e] = fast_exp2(fmaf(s_old[qb][KC / 2][R + e], cc, -m_use[qb]));
-        }
+        s_old[qb][KC / 2][R] = fast_exp2(fmaf(s_old[qb][KC / 2][R], cc, -m_use[qb]));
     };
     auto exp_finish = [&](auto kc_tag) {
       constexpr int KC = decltype(kc_tag)::value;
+      constexpr int R = 8 * (KC % 2);
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
         const f32x16& x = s_old[qb][KC / 2];
-        constexpr int R = 8 * (KC % 2);
         l_tile[qb] += ((x[R] + x[R + 1]) + (x[R + 2] + x[R + 3])) +
                       ((x[R + 4] + x[R + 5]) + (x[R + 6] + x[R + 7]));
-        pf[qb][KC] = to_bf16x8(x[R], x[R + 1], x[R + 2], x[R + 3], x[R + 4], x[R + 5], x[R + 6],
-                               x[R + 7]);
+        p_new[qb][KC] = as_u32x4(to_bf16x8(x[R], x[R + 1], x[R + 2], x[R + 3], x[R + 4],
+                                           x[R + 5], x[R + 6], x[R + 7]));
       }
     };
-    auto exp_chunk = [&](auto kc_tag) {
-      static_for<0, PER_EXP>([&](auto j_tag) { exp_part(kc_tag, j_tag); });
-      exp_finish(kc_tag);
+    // exponential i (0 .. 15) of half H (chunks 2H, 2H + 1), and the chunk's
+    // fragment after its last one
+    auto exp_item = [&](auto h_tag, auto i_tag) {
+      constexpr int H = decltype(h_tag)::value;
+      constexpr int I = decltype(i_tag)::value;
+      using KC_ = std::integral_constant<int, 2 * H + I / 8>;
+      exp_one(KC_(), std::integral_constant<int, I % 8>());
+      if constexpr (I % 8 == 7) exp_finish(KC_());
     };
-    // The weights of tile t - 1 are complete.  Rows whose sums overran
+
+    // ---- head of tile t - 1: scale (scale <= 0), mask, row maximum in
+    // eight parts, then the lazy rescale of the running state.  The rescale
+    // factor of O is applied once the products of tile t - 2 are in. ----
+    float mx0[QB], mx1[QB], alpha_o[QB];
+    bool rescale_o = false;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) mx0[qb] = mx1[qb] = kNegInf;
+    auto head_part = [&](auto j_tag) {
+      constexpr int J = decltype(j_tag)::value;
+      constexpr int KB = J / 4, R0 = 4 * (J % 4);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+        for (int r = R0; r < R0 + 4; ++r) {
+          if (!POS_SCALE) s_old[qb][KB][r] *= c;
+          if (MASK) {
+            const int qrow = qw0 + qb * 32 + n;
+            const int lim = min(L - 1, CAUSAL ? qrow + off : L - 1);  // last admissible key
+            const int key = tw * BN + KB * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+            if (key > lim) s_old[qb][KB][r] = kNegInf;
+          }
+        }
+        float& mx = KB == 0 ? mx0[qb] : mx1[qb];
+        mx = fmaxf(fmaxf(mx, s_old[qb][KB][R0]), s_old[qb][KB][R0 + 1]);
+        mx = fmaxf(fmaxf(mx, s_old[qb][KB][R0 + 2]), s_old[qb][KB][R0 + 3]);
+      }
+    };
+    auto head_end = [&]() {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        float mx = max_xor32(fmaxf(mx0[qb], mx1[qb]));
+        if (POS_SCALE) mx *= c;
+        alpha_o[qb] = 1.f;
+        if (__ballot(mx > m_run[qb] + kRescaleSlack)) {
+          const float m_new = fmaxf(m_run[qb], mx);
+          const float alpha = (m_new == kNegInf) ? 1.f : fast_exp2(m_run[qb] - m_new);
+          m_run[qb] = m_new;
+          l_run[qb] *= alpha;
+          alpha_o[qb] = alpha;
+          rescale_o = true;
+        }
+        m_use[qb] = (m_run[qb] == kNegInf) ? 0.f : m_run[qb];
+      }
+    };
+
+    // ---- phase A: O += P(t-2) V(t-2), the head and the first half of the
+    // weights of tile t - 1 in between ----
+    constexpr bool LOADS_A = PV;  // the loads go out during the first products
+    if constexpr (PV) {
+      constexpr int NP = NV / 2;  // products: (kc, db) = (m / DBLK, m % DBLK)
+      static_assert(NP == 16 || NP == 8, "products per phase");
+      constexpr int PER_LOAD = NP / S::BLOCKS_PER_WAVE;
+      static_for<0, NP>([&](auto m_tag) {
+        constexpr int M = decltype(m_tag)::value;
+        constexpr int AHEAD = (RS < TOT - 2 * M ? RS : TOT - 2 * M) - 2;  // reads after 2M+1
+        lds_wait_lgkm<AHEAD>();
+        lds_ready(vr[2 * M]);
+        lds_ready(vr[2 * M + 1]);
+        const u32x4 w = {vr[2 * M][0], vr[2 * M][1], vr[2 * M + 1][0], vr[2 * M + 1][1]};
+        const bf16x8 vf = as_bf16x8(w);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+          o_acc[qb][M % S::DBLK] =
+              mfma32(vf, as_bf16x8(p_old[qb][M / S::DBLK]), o_acc[qb][M % S::DBLK]);
+        issue_read(std::integral_constant<int, 2 * M + RS>());
+        issue_read(std::integral_constant<int, 2 * M + 1 + RS>());
+        if constexpr (M % PER_LOAD == 0) load_block(std::integral_constant<int, M / PER_LOAD>());
+        if constexpr (EX) {
+          if constexpr (HEAD) {
+            // the first half of the products carries the head's eight
+            // parts, the second half the sixteen exponentials
+            constexpr int NH = NP / 2, HPP = 8 / NH, EPP = 16 / (NP - NH);
+            if constexpr (M < NH) {
+              static_for<0, HPP>([&](auto j_tag) {
+                head_part(std::integral_constant<int, HPP * M + decltype(j_tag)::value>());
+              });
+              if constexpr (M == NH - 1) head_end();
+            } else {
+              static_for<0, EPP>([&](auto e_tag) {
+                exp_item(std::integral_constant<int, 0>(),
+                         std::integral_constant<int, EPP * (M - NH) + decltype(e_tag)::value>());
+              });
+            }
+          } else {
+            constexpr int EPP = 16 / NP;
+            static_for<0, EPP>([&](auto e_tag) {
+              exp_item(std::integral_constant<int, 0>(),
+                       std::integral_constant<int, EPP * M + decltype(e_tag)::value>());
+            });
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      if constexpr (HEAD) {
+        if (rescale_o) {
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+            for (int db = 0; db < S::DBLK; ++db)
+#pragma unroll
+              for (int r = 0; r < 16; ++r) o_acc[qb][db][r] *= alpha_o[qb];
+        }
+      }
+    } else if constexpr (EX) {
+      // t = 1: no product has reached O yet, so O needs no rescale
+      if constexpr (HEAD) {
+        static_for<0, 8>(head_part);
+        head_end();
+      }
+      static_for<0, 16>([&](auto i_tag) { exp_item(std::integral_constant<int, 0>(), i_tag); });
+    }
+
+    // ---- phase B: S(t) = K(t) Q^T, the second half of the weights in
+    // between ----
+    if constexpr (QK) {
+      static_assert(NK == 16 || NK == 8, "products per phase");
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) s_new[qb][kb][r] = 0.f;
+      constexpr int PER_LOAD = NK / S::BLOCKS_PER_WAVE;
+      constexpr int EPP = 16 / NK;  // exponentials per product
+      static_for<0, NK>([&](auto i_tag) {
+        constexpr int I = decltype(i_tag)::value;
+        constexpr int KB = I / S::KSTEPS, ST = I % S::KSTEPS;
+        constexpr int J = NVS + I;  // position in the read stream
+        constexpr int AHEAD = (J + RS < TOT ? RS : TOT - J) - 1;
+        lds_wait_lgkm<AHEAD>();
+        lds_ready(kr[I]);
+        const bf16x8 kf = as_bf16x8(kr[I]);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) s_new[qb][KB] = mfma32(kf, qf[qb][ST], s_new[qb][KB]);
+        issue_read(std::integral_constant<int, J + RS>());
+        if constexpr (!LOADS_A && I % PER_LOAD == PER_LOAD - 1)
+          load_block(std::integral_constant<int, I / PER_LOAD>());
+        if constexpr (EX)
+          static_for<0, EPP>([&](auto e_tag) {
+            exp_item(std::integral_constant<int, 1>(),
+                     std::integral_constant<int, EPP * I + decltype(e_tag)::value>());
+          });
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    } else {
+      if constexpr (!LOADS_A) static_for<0, S::BLOCKS_PER_WAVE>(load_block);
+      if constexpr (EX)
+        static_for<0, 16>([&](auto i_tag) { exp_item(std::integral_constant<int, 1>(), i_tag); });
+    }
+
+    // ---- the weights of tile t - 1 are complete.  Rows whose sums overran
     // kSumLimit (a tile weighed without its own maximum whose scores rose
     // well above the running one) get the tile's scores again, from K in
     // global memory (its LDS buffer is being refilled by now), a lazy
-    // rescale to the exact maximum, and new weights.  Then the sums join the
-    // running ones.
-    auto settle = [&]() {
-      if constexpr (POS_SCALE) {
+    // rescale to the exact maximum, and new weights.  O holds tiles up to
+    // t - 2 here, so its rescale is immediate.  Then the sums join the
+    // running ones. ----
+    if constexpr (EX) {
+      if constexpr (POS_SCALE && !HEAD) {
         // only tiles 1 .. n_free - 1 are weighed without their maximum; they
         // lie wholly inside the sequence, so their K rows can be read again
-        const bool check = t >= 2 && t - 1 < n_free;
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
-          if (check && __ballot(l_tile[qb] > kSumLimit)) {
-            // the tile's rows through a buffer resource (32-bit lane
-            // offsets formed here, so no 64-bit address stays live)
+          if (__ballot(l_tile[qb] > kSumLimit)) {
+            // (the base is made wave-uniform explicitly: a resource in vector
+            // registers would need a loop over its distinct values)
+            const uintptr_t base = (uintptr_t)(kg + (size_t)tw * BN * kv_stride);
+            const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)base);
+            const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(base >> 32));
             const __amdgpu_buffer_rsrc_t rows = __builtin_amdgcn_make_buffer_rsrc(
-                const_cast<char*>(kg + (size_t)(t - 1) * BN * kv_stride), 0,
-                (int)(BN * kv_stride), 0x00020000);
+                reinterpret_cast<char*>(((uintptr_t)hi << 32) | lo), 0, (int)(BN * kv_stride),
+                0x00020000);
+            // lane part of the fragment offsets in a vector register, the
+            // rest (wave-uniform) in the scalar offset
+            const uint32_t lane_off = (uint32_t)(n * kv_stride + 16 * h);
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
@@ -423,7 +600,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
 #pragma unroll
               for (int st = 0; st < S::KSTEPS; ++st) {
                 const u32x4 u = __builtin_amdgcn_raw_buffer_load_b128(
-                    rows, (uint32_t)((32 * kb + n) * kv_stride + (16 * st + 8 * h) * 2), 0, 0);
+                    rows, lane_off, (uint32_t)(32 * kb * kv_stride + 32 * st), 0);
                 s_old[qb][kb] = mfma32(as_bf16x8(u), qf[qb][st], s_old[qb][kb]);
                 __builtin_amdgcn_sched_barrier(0);  // one fragment in registers at a time
               }
@@ -452,133 +629,19 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
               for (int e = 0; e < 8; ++e) x[R + e] = fast_exp2(fmaf(x[R + e], c, -m_use[qb]));
               l_tile[qb] += ((x[R] + x[R + 1]) + (x[R + 2] + x[R + 3])) +
                             ((x[R + 4] + x[R + 5]) + (x[R + 6] + x[R + 7]));
-              pf[qb][KC] = to_bf16x8(x[R], x[R + 1], x[R + 2], x[R + 3], x[R + 4], x[R + 5],
-                                     x[R + 6], x[R + 7]);
+              p_new[qb][KC] = as_u32x4(to_bf16x8(x[R], x[R + 1], x[R + 2], x[R + 3], x[R + 4],
+                                                 x[R + 5], x[R + 6], x[R + 7]));
             });
           }
         }
       }
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) l_run[qb] += l_tile[qb];
-    };
-
-
-    if constexpr (QK) {
-      // ---- S^T(t) = K(t) Q^T, exponentials of tile t - 1 in between ----
-      constexpr int PER_LOAD = NK / S::BLOCKS_PER_WAVE;  // products per load block
-      static_assert(NK % S::BLOCKS_PER_WAVE == 0, "load spacing");
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) s_new[qb][kb][r] = 0.f;
-      static_for<0, NK>([&](auto i_tag) {
-        constexpr int I = decltype(i_tag)::value;
-        constexpr int KB = I / S::KSTEPS, ST = I % S::KSTEPS;
-        constexpr int AHEAD = (I + RS < TOT ? I + RS : TOT) - I - 1;  // reads issued after I
-        lds_wait_lgkm<AHEAD>();
-        lds_ready(kr[I]);
-        const bf16x8 kf = as_bf16x8(kr[I]);
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) s_new[qb][KB] = mfma32(kf, qf[qb][ST], s_new[qb][KB]);
-        issue_read(std::integral_constant<int, I + RS>());
-        if constexpr (I % PER_LOAD == PER_LOAD - 1)
-          load_block(std::integral_constant<int, I / PER_LOAD>());
-        if constexpr (PV) {
-          exp_part(std::integral_constant<int, I / PER_EXP>(),
-                   std::integral_constant<int, I % PER_EXP>());
-          if constexpr (I % PER_EXP == PER_EXP - 1)
-            exp_finish(std::integral_constant<int, I / PER_EXP>());
-        }
-        // the source order is the schedule: it keeps each product's
-        // exponentials beside it and bounds the live registers
-        __builtin_amdgcn_sched_barrier(0);
-      });
-    } else {
-      static_for<0, S::BLOCKS_PER_WAVE>(load_block);
-      if constexpr (PV) static_for<0, 4>(exp_chunk);
-    }
-    if constexpr (PV) settle();
-
-    // ---- softmax head of tile t: scale (scale <= 0), mask, row max, in
-    // eight parts interleaved with the P V products of tile t - 1 (key block
-    // 0 first: its scores were formed first) ----
-    float mx0[QB], mx1[QB];
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) mx0[qb] = mx1[qb] = kNegInf;
-    auto head_part = [&](auto j_tag) {
-      constexpr int J = decltype(j_tag)::value;
-      constexpr int KB = J / 4, R0 = 4 * (J % 4);
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-#pragma unroll
-        for (int r = R0; r < R0 + 4; ++r) {
-          if (!POS_SCALE) s_new[qb][KB][r] *= c;
-          if (MASK) {
-            const int qrow = qw0 + qb * 32 + n;
-            const int lim = min(L - 1, CAUSAL ? qrow + off : L - 1);  // last admissible key
-            const int key = t * BN + KB * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-            if (key > lim) s_new[qb][KB][r] = kNegInf;
-          }
-        }
-        float& mx = KB == 0 ? mx0[qb] : mx1[qb];
-        mx = fmaxf(fmaxf(mx, s_new[qb][KB][R0]), s_new[qb][KB][R0 + 1]);
-        mx = fmaxf(fmaxf(mx, s_new[qb][KB][R0 + 2]), s_new[qb][KB][R0 + 3]);
-      }
-    };
-
-    if constexpr (PV) {
-      // ---- O^T += V^T(t-1) P^T(t-1) over 16-key chunks ----
-      // Chunk kc: k-group h holds P for keys 16 kc + {4h..4h+3, 8+4h..8+4h+3};
-      // the two transposing reads fetch V for exactly those keys, column d.
-      // Product m = (kc, db) takes V reads 2m and 2m + 1.
-      constexpr int PER_HEAD = (NV / 2) / 8;  // products per head part
-      static_assert((NV / 2) % 8 == 0, "head spacing");
-      static_for<0, NV / 2>([&](auto m_tag) {
-        constexpr int M = decltype(m_tag)::value;
-        constexpr int AHEAD = (RS < NV - 2 * M ? RS : NV - 2 * M) - 2;  // reads after 2M+1
-        lds_wait_lgkm<AHEAD>();
-        lds_ready(vr[2 * M]);
-        lds_ready(vr[2 * M + 1]);
-        const u32x4 w = {vr[2 * M][0], vr[2 * M][1], vr[2 * M + 1][0], vr[2 * M + 1][1]};
-        const bf16x8 vf = as_bf16x8(w);
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
-          o_acc[qb][M % S::DBLK] = mfma32(vf, pf[qb][M / S::DBLK], o_acc[qb][M % S::DBLK]);
-        issue_read(std::integral_constant<int, NKS + RS + 2 * M>());
-        issue_read(std::integral_constant<int, NKS + RS + 2 * M + 1>());
-        if constexpr (QK && MAXP && M % PER_HEAD == PER_HEAD - 1)
-          head_part(std::integral_constant<int, M / PER_HEAD>());
-        __builtin_amdgcn_sched_barrier(0);
-      });
-    } else if constexpr (QK && MAXP) {
-      static_for<0, 8>(head_part);
-    }
-
-    // ---- softmax head of tile t, end: lazy rescale of the running state ----
-    if constexpr (QK && MAXP) {
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        float mx = max_xor32(fmaxf(mx0[qb], mx1[qb]));
-        if (POS_SCALE) mx *= c;
-        if (__ballot(mx > m_run[qb] + kRescaleSlack)) {
-          const float m_new = fmaxf(m_run[qb], mx);
-          const float alpha = (m_new == kNegInf) ? 1.f : fast_exp2(m_run[qb] - m_new);
-          m_run[qb] = m_new;
-          l_run[qb] *= alpha;
-#pragma unroll
-          for (int db = 0; db < S::DBLK; ++db)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) o_acc[qb][db][r] *= alpha;
-        }
-        m_use[qb] = (m_run[qb] == kNegInf) ? 0.f : m_run[qb];
-      }
     }
   };
 
   // One barrier per step: once every wave has waited for its own loads,
-  // the barrier makes K(t) and V(t - 1) visible and proves that every wave
+  // the barrier makes K(t) and V(t - 2) visible and proves that every wave
   // has finished step t - 1, whose buffers the step's loads overwrite.
   using T1 = std::true_type;
   using F0 = std::false_type;
@@ -586,30 +649,52 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs a) {
     wait_vmcnt<0>();
     __syncthreads();
     const bool qk = t < n_live;
-    const bool pv = t >= 1 && t <= n_live;
-    const bool mask = t >= n_free;
-    if (qk && pv && t + 1 < n_full && !mask) {
-      step(t, par_tag, T1(), T1(), F0(), T1());
-    } else if (qk && pv) {
+    const bool ex = t >= 1 && t <= n_live;
+    const bool pv = t >= 2 && t <= n_live + 1;
+    // tile t - 1 gets its maximum: the first tile, masked tiles, and every
+    // tile when the scale is not positive
+    const bool mask = t - 1 >= n_free;
+    const bool head = !POS_SCALE || t == 1 || mask;
+    if (qk && ex && pv) {
+      if (!head) {
+        if (t + 1 < n_full)
+          step(t, par_tag, T1(), T1(), T1(), F0(), F0(), T1());
+        else
+          step(t, par_tag, T1(), T1(), T1(), F0(), F0(), F0());
+      } else if (mask) {
+        step(t, par_tag, T1(), T1(), T1(), T1(), T1(), F0());
+      } else {
+        step(t, par_tag, T1(), T1(), T1(), T1(), F0(), F0());
+      }
+    } else if (qk && ex) {  // t = 1
       if (mask)
-        step(t, par_tag, T1(), T1(), T1(), F0());
+        step(t, par_tag, T1(), T1(), F0(), T1(), T1(), F0());
       else
-        step(t, par_tag, T1(), T1(), F0(), F0());
-    } else if (qk) {
+        step(t, par_tag, T1(), T1(), F0(), T1(), F0(), F0());
+    } else if (qk) {  // t = 0
+      step(t, par_tag, T1(), F0(), F0(), F0(), F0(), F0());
+    } else if (ex && pv) {  // t = n_live
+      if (!head)
+        step(t, par_tag, F0(), T1(), T1(), F0(), F0(), F0());
+      else if (mask)
+        step(t, par_tag, F0(), T1(), T1(), T1(), T1(), F0());
+      else
+        step(t, par_tag, F0(), T1(), T1(), T1(), F0(), F0());
+    } else if (ex) {  // t = 1 = n_live
       if (mask)
-        step(t, par_tag, T1(), F0(), T1(), F0());
+        step(t, par_tag, F0(), T1(), F0(), T1(), T1(), F0());
       else
-        step(t, par_tag, T1(), F0(), F0(), F0());
-    } else if (pv) {
-      step(t, par_tag, F0(), T1(), F0(), F0());
+        step(t, par_tag, F0(), T1(), F0(), T1(), F0(), F0());
+    } else if (pv) {  // t = n_live + 1
+      step(t, par_tag, F0(), F0(), T1(), F0(), F0(), F0());
     } else {
-      step(t, par_tag, F0(), F0(), F0(), F0());
+      step(t, par_tag, F0(), F0(), F0(), F0(), F0(), F0());
     }
   };
   if (n_kt > 0) {
-    for (int t = 0; t <= n_kt; t += 2) {
+    for (int t = 0; t <= n_kt + 1; t += 2) {
       run_step(t, B0());
-      if (t + 1 <= n_kt) run_step(t + 1, B1());
+      if (t + 1 <= n_kt + 1) run_step(t + 1, B1());
     }
   }
 

@@ -9,7 +9,7 @@ hipError_t launch_fwd_d64(const FwdArgs& a, unsigned nblocks, bool causal, bool 
 
 hipError_t launch_fwd(const FwdArgs& a, unsigned nblocks, int D, bool causal, bool out_f32,
                       bool pos_scale, hipStream_t st) {
-  if (D == 128) return fwd_detail::go_d<128>(a, nblocks, causal, out_f32, pos_scale, st);
+  if (D == 128) return fwd_detail::go_w<128, kFwdWaves>(a, nblocks, causal, out_f32, pos_scale, st);
   return launch_fwd_d64(a, nblocks, causal, out_f32, pos_scale, st);
 }
 

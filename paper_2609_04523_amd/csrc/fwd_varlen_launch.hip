@@ -7,8 +7,8 @@ namespace {
 
 template <int D, bool CAUSAL, bool POS>
 hipError_t go(const FwdArgs& a, unsigned nblocks, hipStream_t st) {
-  hipLaunchKernelGGL((fwd_kernel<D, CAUSAL, false, kFwdQB, POS, true>), dim3(nblocks),
-                     dim3(FwdShape<D, kFwdQB>::THREADS), 0, st, a);
+  hipLaunchKernelGGL((fwd_kernel<D, CAUSAL, false, kFwdQB, POS, true, kFwdWaves>),
+                     dim3(nblocks), dim3(FwdShape<D, kFwdQB, kFwdWaves>::THREADS), 0, st, a);
   return hipGetLastError();
 }
 

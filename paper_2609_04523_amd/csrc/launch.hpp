@@ -13,7 +13,8 @@
 
 namespace mk {
 
-constexpr int kFwdQB = 1;  // 32-query blocks per wave in the forward kernel
+constexpr int kFwdQB = 1;     // 32-query blocks per wave in the forward kernel
+constexpr int kFwdWaves = 4;  // waves per forward workgroup (128 query rows)
 
 // Dense [B, H, S, D] forward: nblocks workgroups of the forward kernel.
 hipError_t launch_fwd(const FwdArgs& a, unsigned nblocks, int D, bool causal, bool out_f32,

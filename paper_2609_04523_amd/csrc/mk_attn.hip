@@ -50,7 +50,7 @@ int fwd_impl(const void* q, const void* k, const void* v, void* o, float* lse, i
     return MK_ERR_ALIGN;
   if (lse && !aligned(lse, 4)) return MK_ERR_ALIGN;
   if (kv_seqlens && !aligned(kv_seqlens, 4)) return MK_ERR_ALIGN;
-  const int BM = mk::FwdShape<128, mk::kFwdQB>::BM;  // same for both head dims
+  const int BM = mk::FwdShape<128, mk::kFwdQB, mk::kFwdWaves>::BM;  // same for both head dims
   const long long n_qtiles = (Sq + BM - 1) / BM;
   const long long nblocks = n_qtiles * B * Hq;
   if (nblocks > 0x7fffffffLL) return MK_ERR_SHAPE;
@@ -215,7 +215,7 @@ int mk_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o, flo
       !aligned(cu_seqlens_q, 4) || !aligned(cu_seqlens_k, 4))
     return MK_ERR_ALIGN;
   if (lse && !aligned(lse, 4)) return MK_ERR_ALIGN;
-  const int BM = mk::FwdShape<128, mk::kFwdQB>::BM;
+  const int BM = mk::FwdShape<128, mk::kFwdQB, mk::kFwdWaves>::BM;
   const long long n_qtiles = (max_seqlen_q + BM - 1) / BM;
   const long long nblocks = n_qtiles * B * Hq;
   // workgroups of one launch; a key tile's rows (64 tokens of Hkv heads)

@@ -107,12 +107,14 @@ __device__ __forceinline__ void load_lds16_at(const void* g, uint32_t lds_addr) 
 // `bytes` (kept in scalar registers) plus a 32-bit lane offset, so no 64-bit
 // address arithmetic runs on the vector unit.  Offsets at or past `bytes`
 // read zeros instead of leaving the range.
+// `soff` is a wave-uniform byte offset added to every lane's (it lives in a
+// scalar register, so per-block offsets need no vector register each).
 __device__ __forceinline__ void load_lds16_buf(const char* base, uint32_t bytes, uint32_t voff,
-                                               uint32_t lds_addr) {
+                                               uint32_t lds_addr, uint32_t soff = 0) {
   const __amdgpu_buffer_rsrc_t rs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), 0, (int)bytes, 0x00020000);
   __builtin_amdgcn_raw_ptr_buffer_load_lds(
-      rs, (__attribute__((address_space(3))) void*)(uintptr_t)lds_addr, 16, voff, 0, 0, 0);
+      rs, (__attribute__((address_space(3))) void*)(uintptr_t)lds_addr, 16, voff, soff, 0, 0);
 }
 
 // s_waitcnt vmcnt(N): wait until at most N vector-memory operations of this
