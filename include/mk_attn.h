@@ -123,7 +123,9 @@ int mk_attn_fwd_varlen(const void *q, const void *k, const void *v, void *o, flo
  * b * Hkv + g - 1) and this stream is cut into n_parts equal parts, one
  * wave each.  A pair that lies inside one part is attended and written by
  * that wave alone; a pair cut by part boundaries is attended piecewise and
- * its pieces are merged by a second kernel.  Two kernels on `stream`.
+ * its pieces are merged by a second kernel, one wave per part, in which
+ * the part holding the pair's last piece merges it.  Two kernels on
+ * `stream`.
  *   q                 [B, Hq, D] bf16
  *   k_cache, v_cache  [B, Hkv, Smax, D] bf16; positions >= L_b are never read
  *   o                 [B, Hq, D] bf16 (written)
@@ -213,9 +215,10 @@ int mk_attn_decode_paged(const void *q, const void *k_pages, const void *v_pages
 
 /*
  * Bytes of decode workspace for these sizes: per part, two partial outputs
- * [2, G, D] fp32 (the part's first and last piece, G = Hq / Hkv) and their
- * LSEs [2, G] fp32, the two regions 256-byte aligned.  n_parts = 0 selects
- * the default.  Independent of B and Smax.  Returns 0 for invalid sizes.
+ * [2, G, D] fp32 (the part's first and last piece, G = Hq / Hkv), their
+ * LSEs [2, G] fp32, and an int32 [4] record of the cut pair the part
+ * closes, the three regions 256-byte aligned.  n_parts = 0 selects the
+ * default.  Independent of B and Smax.  Returns 0 for invalid sizes.
  */
 size_t mk_attn_decode_workspace_bytes(int Hq, int Hkv, int D, int n_parts);
 

@@ -30,11 +30,11 @@ hipError_t launch_decode(const DecArgs& a, int D, int qblocks, bool paged, hipSt
     parts<false>(a, D, qblocks, st);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const unsigned mblocks = (unsigned)(((long long)a.B * a.Hq + 3) / 4);  // one wave per row
+  const unsigned mblocks = (unsigned)((a.P + 3) / 4);  // one wave per part
   if (D == 128)
-    hipLaunchKernelGGL(dec_merge_kernel<128>, dim3(mblocks), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(dec_close_kernel<128>, dim3(mblocks), dim3(256), 0, st, a);
   else
-    hipLaunchKernelGGL(dec_merge_kernel<64>, dim3(mblocks), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(dec_close_kernel<64>, dim3(mblocks), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

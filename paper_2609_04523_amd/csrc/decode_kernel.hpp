@@ -32,11 +32,12 @@
 // each lane's 16-byte row chunk is addressed in its half's page.  The
 // stream, the pieces and the merge are those of the contiguous cache.
 //
-// Kernel 2 (dec_merge_kernel), one wave per (batch, query head) row: rows
-// of pairs cut by part boundaries are merged from their pieces by
-// log-sum-exp, LSE = log sum_i exp(LSE_i), O = sum_i exp(LSE_i - LSE) O_i;
-// sequences without keys get O = 0, LSE = -inf; every other row is left
-// alone.
+// Kernel 2 (dec_close_kernel), one wave per part: the part that closes a
+// cut pair (holds its last piece) recorded where the pair's pieces lie, and
+// its wave merges them by log-sum-exp, LSE = log sum_i exp(LSE_i),
+// O = sum_i exp(LSE_i - LSE) O_i, into the pair's G rows; sequences without
+// keys get O = 0, LSE = -inf; every other row is left alone.  (The MLA
+// decode merges with dec_merge_kernel, one wave per row.)
 #pragma once
 
 #include "mk_common.hpp"
@@ -54,6 +55,7 @@ struct DecArgs {
   float* lse;               // [B, Hq] or null
   float* o_part;            // [P, 2, G, D]
   float* lse_part;          // [P, 2, G]
+  int* close_desc;          // [P, 4]: the cut pair a part closes (see dec_part_kernel)
   const int* kv_seqlens;    // [B]
   int B, Hq, Hkv, Smax, P;  // paged: Smax = max_pages * page_size
   float scale_log2;
@@ -83,6 +85,16 @@ __device__ __forceinline__ int wave_incl_scan(int x) {
 // (<= 2^-22), so the floor of the rounded quotient is the exact floor.
 __device__ __forceinline__ int part_start(int w, int T, int P) {
   return (int)floor((double)w * (double)T / (double)P);
+}
+
+// Owner of stage s (0 <= s < T): the largest part w with
+// floor(w T / P) <= s, i.e. w T < (s + 1) P, which is
+// ceil((s + 1) P / T) - 1 (in [0, P - 1] since s + 1 <= T).  The ceiling is
+// exact by the argument of part_start: (s + 1) P is exact in double, and a
+// non-integer quotient lies >= 1/T >= 2^-31 from an integer while half an
+// ulp of a value <= P <= 2^20 is <= 2^-33.
+__device__ __forceinline__ int part_of(int s, int T, int P) {
+  return (int)ceil((double)(s + 1) * (double)P / (double)T) - 1;
 }
 
 // Stage counts of sequences b0 + lane (0 past B) and their inclusive scan.
@@ -212,8 +224,28 @@ __global__ __launch_bounds__(64) void dec_part_kernel(DecArgs a) {
   const int T = dec_total(a, first);
   const int s0 = part_start(w, T, a.P);
   const int n_stages = part_start(w + 1, T, a.P) - s0;
+  // A part whose first piece ends a pair that began in an earlier part
+  // closes that cut pair: it records the pair's first output row, the part
+  // holding the pair's first stage and that piece's slot there, and T, so
+  // that the merge kernel needs no stream geometry.  Every part writes its
+  // record (flag bit 1 clear when it closes nothing).
+  DecCursor cur = {0, 0, 0, 0, 0};
+  int rec[4] = {0, 0, 0, T};
+  if (n_stages > 0) {
+    cur = dec_locate(a, first, s0);
+    if (cur.t > 0 && cur.nt - cur.t <= n_stages) {
+      const int A = s0 - cur.t;  // the pair's first stage
+      const int w0 = part_of(A, T, a.P);
+      rec[0] = cur.b * a.Hq + cur.g * G;
+      rec[1] = w0;
+      rec[2] = 2 | (A > part_start(w0, T, a.P) ? 1 : 0);
+    }
+  }
+  if (lane == 0) {
+    const u32x4 r = {(uint32_t)rec[0], (uint32_t)rec[1], (uint32_t)rec[2], (uint32_t)rec[3]};
+    *reinterpret_cast<u32x4*>(a.close_desc + 4 * w) = r;
+  }
   if (n_stages <= 0) return;
-  DecCursor cur = dec_locate(a, first, s0);
 
   // ---- stage loads: slot <- K rows, V rows, then the pair's Q rows, each
   // row's 16-byte chunks XOR-swizzled.  K/V rows past the sequence end
@@ -467,16 +499,6 @@ __global__ __launch_bounds__(64) void dec_part_kernel(DecArgs a) {
   }
 }
 
-// Owner of stage s (0 <= s < T): the largest part w with
-// floor(w T / P) <= s, i.e. w T < (s + 1) P, which is
-// ceil((s + 1) P / T) - 1 (in [0, P - 1] since s + 1 <= T).  The ceiling is
-// exact by the argument of part_start: (s + 1) P is exact in double, and a
-// non-integer quotient lies >= 1/T >= 2^-31 from an integer while half an
-// ulp of a value <= P <= 2^20 is <= 2^-33.
-__device__ __forceinline__ int part_of(int s, int T, int P) {
-  return (int)ceil((double)(s + 1) * (double)P / (double)T) - 1;
-}
-
 __device__ __forceinline__ float wave_max(float x) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
@@ -602,6 +624,89 @@ __global__ __launch_bounds__(256) void dec_merge_kernel(DecArgs a) {
 #pragma unroll
   for (int k = 0; k < PER_LANE; ++k) o[k] = to_bf16_bits(out[k]);
   if (lane == 0 && a.lse) a.lse[row] = lse;
+}
+
+
+// One wave per part w (see kernel 2 above).  Each lane takes 16-byte
+// chunks of the pair's G x D block of outputs (chunk c: head 4c / D, head
+// dims 4c % D .. +3) and merges the pieces online, in order, eight at a
+// time with all their loads issued before any is used:
+//   M' = max(M, LSE_i),  S = S 2^.. + exp(LSE_i - M'),  acc likewise,
+// then O = acc / S and LSE = M' + log S.
+template <int D>
+__global__ __launch_bounds__(256) void dec_close_kernel(DecArgs a) {
+  constexpr int BATCH = 8;  // pieces whose loads are issued together
+  const int lane = threadIdx.x & 63;
+  const int w = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (w >= a.P) return;
+  const int G = a.Hq / a.Hkv;
+  // the record, through the scalar cache
+  const __attribute__((address_space(4))) int* rp =
+      (const __attribute__((address_space(4))) int*)(a.close_desc + 4 * w);
+  const int row0 = rp[0], w0 = rp[1], flags = rp[2], T = rp[3];
+
+  // sequences without keys: b = w, w + P, ...
+  for (int b = w; b < a.B; b += a.P) {
+    if (seq_len_uniform(a, b) != 0) continue;
+    uint16_t* o = a.o + (size_t)b * a.Hq * D;
+    for (int i = lane; i < a.Hq * D / 8; i += 64)
+      *reinterpret_cast<u32x4*>(o + 8 * i) = u32x4{0u, 0u, 0u, 0u};
+    if (a.lse)
+      for (int i = lane; i < a.Hq; i += 64) a.lse[(size_t)b * a.Hq + i] = kNegInf;
+  }
+  if (!(flags & 2)) return;
+
+  // pieces: i = 0 in part w0 (slot flags & 1), i >= 1 in part w0 + i
+  // (slot 0); with fewer stages than parts some parts hold none
+  const int n_pc = w - w0 + 1;
+  const int slot_a = flags & 1;
+  const bool all_hold = T >= a.P;
+  auto entry = [&](int i) {  // (part, slot) row of piece i in the workspace
+    return (size_t)(w0 + i) * 2 + (i == 0 ? slot_a : 0);
+  };
+  auto holds = [&](int i) {
+    const int p = w0 + i;
+    return all_hold || part_start(p, T, a.P) < part_start(p + 1, T, a.P);
+  };
+  const int n_chunks = G * D / 4;
+  for (int c = lane; c < n_chunks; c += 64) {
+    const int h = (4 * c) / D;
+    const int d0 = 4 * c - h * D;
+    float M = kNegInf, S = 0.f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int i0 = 0; i0 < n_pc; i0 += BATCH) {
+      float ls[BATCH];
+      f32x4 ov[BATCH];
+#pragma unroll
+      for (int j = 0; j < BATCH; ++j) {
+        // a piece past the pair or in an empty part reads piece 0 and
+        // weighs nothing
+        const bool use = i0 + j < n_pc && holds(i0 + j);
+        const size_t e = entry(use ? i0 + j : 0) * G + h;
+        ls[j] = a.lse_part[e];
+        ov[j] = *reinterpret_cast<const f32x4*>(a.o_part + e * D + d0);
+        if (!use) ls[j] = kNegInf;
+      }
+#pragma unroll
+      for (int j = 0; j < BATCH; ++j) {
+        const float m_new = fmaxf(M, ls[j]);
+        if (m_new == kNegInf) continue;  // nothing weighed yet
+        const float f_old = __expf(M - m_new);
+        const float f_new = __expf(ls[j] - m_new);
+        S = S * f_old + f_new;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) acc[k] = acc[k] * f_old + f_new * ov[j][k];
+        M = m_new;
+      }
+    }
+    const float inv = S > 0.f ? 1.f / S : 0.f;
+    const u32x2 wv = {(uint32_t)to_bf16_bits(acc[0] * inv) |
+                          ((uint32_t)to_bf16_bits(acc[1] * inv) << 16),
+                      (uint32_t)to_bf16_bits(acc[2] * inv) |
+                          ((uint32_t)to_bf16_bits(acc[3] * inv) << 16)};
+    *reinterpret_cast<u32x2*>(a.o + (size_t)(row0 + h) * D + d0) = wv;
+    if (d0 == 0 && a.lse) a.lse[row0 + h] = S > 0.f ? M + logf(S) : kNegInf;
+  }
 }
 
 }  // namespace mk

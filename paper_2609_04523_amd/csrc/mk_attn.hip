@@ -79,10 +79,11 @@ int fwd_impl(const void* q, const void* k, const void* v, void* o, float* lse, i
 }
 
 // Decode workspace: o_part [P, 2, G, D] fp32, then lse_part [P, 2, G]
-// fp32 at a 256-byte aligned offset.
+// fp32, then the parts' records of the cut pairs they close, int32 [P, 4],
+// each region at a 256-byte aligned offset.
 struct DecLayout {
   int parts;
-  size_t o_bytes, lse_off, total;
+  size_t o_bytes, lse_off, desc_off, total;
 };
 
 // ring-slot variant (16-byte Q chunks per 1 KB load) of a head dim and group
@@ -110,7 +111,8 @@ bool dec_layout(int Hq, int Hkv, int D, int n_parts, DecLayout* out) {
   l.parts = n_parts == 0 ? dec_default_parts(D, G) : n_parts;
   l.o_bytes = (size_t)l.parts * 2 * G * D * sizeof(float);
   l.lse_off = round_up(l.o_bytes, 256);
-  l.total = l.lse_off + round_up((size_t)l.parts * 2 * G * sizeof(float), 256);
+  l.desc_off = l.lse_off + round_up((size_t)l.parts * 2 * G * sizeof(float), 256);
+  l.total = l.desc_off + round_up((size_t)l.parts * 4 * sizeof(int), 256);
   *out = l;
   return true;
 }
@@ -125,6 +127,7 @@ bool mla_layout(int H, int Dc, int n_parts, DecLayout* out) {
   l.parts = n_parts == 0 ? kComputeUnits : n_parts;
   l.o_bytes = (size_t)l.parts * 2 * H * Dc * sizeof(float);
   l.lse_off = round_up(l.o_bytes, 256);
+  l.desc_off = 0;  // the MLA merge needs no records
   l.total = l.lse_off + round_up((size_t)l.parts * 2 * H * sizeof(float), 256);
   *out = l;
   return true;
@@ -170,6 +173,7 @@ mk::DecArgs dec_args(const void* q, const void* kc, const void* vc, void* o, flo
   a.lse = lse;
   a.o_part = reinterpret_cast<float*>(ws);
   a.lse_part = reinterpret_cast<float*>(ws + l.lse_off);
+  a.close_desc = l.desc_off ? reinterpret_cast<int*>(ws + l.desc_off) : nullptr;
   a.kv_seqlens = kv_seqlens;
   a.B = B;
   a.Hq = Hq;

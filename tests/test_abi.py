@@ -223,7 +223,8 @@ def test_decode_workspace_size(lib):
     rnd = lambda x: -(-x // 256) * 256
     for Hq, Hkv, D, P in ((32, 8, 128, 768), (16, 1, 64, 3), (4, 4, 128, 1)):
         G = Hq // Hkv
-        want = rnd(P * 2 * G * D * 4) + rnd(P * 2 * G * 4)
+        # partial outputs, their LSEs, then one int32 [4] record per part
+        want = rnd(P * 2 * G * D * 4) + rnd(P * 2 * G * 4) + rnd(P * 4 * 4)
         assert lib.mk_attn_decode_workspace_bytes(Hq, Hkv, D, P) == want
     assert lib.mk_attn_decode_workspace_bytes(32, 8, 128, 0) == \
         lib.mk_attn_decode_workspace_bytes(32, 8, 128, 768)
