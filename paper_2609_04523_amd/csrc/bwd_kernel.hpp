@@ -48,6 +48,7 @@ struct BwdArgs {
   int B, Hq, Hkv, Sq, Skv;
   int sq_pad;            // Sq rounded up to a multiple of 128
   int n_qtiles;          // dQ kernel: ceil(Sq / 128)
+  int xcd_gp;            // dQ kernel: > 0 xcd_pair_map order (groups of xcd_gp pairs)
   int n_kblocks;         // dK/dV kernel: ceil(Skv / 128)
   float scale;
   float scale_log2;      // scale * log2(e)
@@ -114,12 +115,18 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 31, h = lane >> 5;
-  // longest query tiles first
-  const int per = a.B * a.Hq;
-  const int t_ = blockIdx.x / per;
-  const int rem = blockIdx.x - t_ * per;
-  const int qt = a.n_qtiles - 1 - t_;
-  const int b = rem / a.Hq, hq = rem - (rem / a.Hq) * a.Hq;
+  // longest query tiles first; pairs placed on the XCDs when possible
+  int qt, b, hq;
+  if (a.xcd_gp > 0) {
+    xcd_pair_map(blockIdx.x, a.n_qtiles, a.B, a.Hkv, a.Hq / a.Hkv, a.xcd_gp, qt, b, hq);
+  } else {
+    const int per = a.B * a.Hq;
+    const int t_ = blockIdx.x / per;
+    const int rem = blockIdx.x - t_ * per;
+    qt = a.n_qtiles - 1 - t_;
+    b = rem / a.Hq;
+    hq = rem - b * a.Hq;
+  }
   const int g = hq / (a.Hq / a.Hkv);
   const int L = a.kv_seqlens ? clamp_len(a.kv_seqlens[b], a.Skv) : a.Skv;
   const int off = L - a.Sq;

@@ -44,7 +44,7 @@ struct FwdArgs {
   const int* kv_seqlens;
   int B, Hq, Hkv, Sq, Skv;
   int n_qtiles;
-  int xcd_groups;     // 1: (batch, kv head) groups spread over the 8 XCDs
+  int xcd_gp;         // > 0: xcd_pair_map order with groups of xcd_gp pairs; 0: plain order
   float scale_log2;   // scale * log2(e)
   // packed ragged batches only: q, o [total_q, Hq, D], k, v [total_k, Hkv, D],
   // sequence b = query tokens [cu_q[b], cu_q[b+1]), keys [cu_k[b], cu_k[b+1]),
@@ -86,23 +86,13 @@ constexpr float kRescaleSlack = 8.0f;
 constexpr float kSumLimit = 256.0f;
 
 // Work-item order.  Longest causal q-tiles are issued first.  When the
-// number of (batch, kv head) groups is a multiple of 8, consecutive
-// workgroups on one XCD (dispatch is round-robin over the 8 XCDs) belong
-// to the same group, so the query heads and q-tiles that re-read one K/V
-// head share that XCD's L2.
+// number of (batch, kv head) pairs is a multiple of 8, the pairs are placed
+// on the XCDs (xcd_pair_map), so the query heads and q-tiles that re-read
+// one K/V head share that XCD's L2.
 __device__ __forceinline__ void fwd_map_block(int bid, const FwdArgs& a, int& qt, int& hq,
                                               int& b) {
-  const int G = a.Hq / a.Hkv;
-  if (a.xcd_groups) {
-    const int x = bid & 7;
-    const int j = bid >> 3;
-    const int per = ((a.B * a.Hkv) >> 3) * G;  // items per XCD per q-tile
-    const int t = j / per;
-    const int rem = j - t * per;
-    qt = a.n_qtiles - 1 - t;
-    const int grp = x + 8 * (rem / G);
-    b = grp / a.Hkv;
-    hq = (grp - b * a.Hkv) * G + (rem % G);
+  if (a.xcd_gp > 0) {
+    xcd_pair_map(bid, a.n_qtiles, a.B, a.Hkv, a.Hq / a.Hkv, a.xcd_gp, qt, b, hq);
   } else {
     const int per = a.B * a.Hq;
     const int t = bid / per;

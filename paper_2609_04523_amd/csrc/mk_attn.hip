@@ -68,7 +68,7 @@ int fwd_impl(const void* q, const void* k, const void* v, void* o, float* lse, i
   a.Sq = Sq;
   a.Skv = Skv;
   a.n_qtiles = (int)n_qtiles;
-  a.xcd_groups = ((B * Hkv) % 8 == 0) ? 1 : 0;
+  a.xcd_gp = ((B * Hkv) % 8 == 0) ? mk::xcd_group_pairs(Hq / Hkv, (int)n_qtiles) : 0;
   a.scale_log2 = scale * mk::kLog2e;
   a.cu_q = a.cu_k = nullptr;
   a.total_q = a.total_k = 0;
@@ -240,7 +240,7 @@ int mk_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o, flo
   a.Sq = max_seqlen_q;
   a.Skv = 0;
   a.n_qtiles = (int)n_qtiles;
-  a.xcd_groups = 0;
+  a.xcd_gp = 0;
   a.scale_log2 = scale * mk::kLog2e;
   a.cu_q = cu_seqlens_q;
   a.cu_k = cu_seqlens_k;
@@ -427,6 +427,7 @@ int mk_attn_bwd(const void* q, const void* k, const void* v, const void* o, cons
   a.Sq = Sq;
   a.Skv = Skv;
   a.n_qtiles = (Sq + 127) / 128;
+  a.xcd_gp = ((B * Hkv) % 8 == 0) ? mk::xcd_group_pairs(Hq / Hkv, a.n_qtiles) : 0;
   a.n_kblocks = (Skv + 127) / 128;
   a.scale = scale;
   a.scale_log2 = scale * mk::kLog2e;

@@ -254,6 +254,38 @@ __device__ __forceinline__ T& pick(T& a, T& b) {
     return b;
 }
 
+// Work order of q-tile workgroups over (batch, kv head) pairs, for B * Hkv
+// a multiple of 8.  Workgroup i runs on XCD i % 8 (the hardware deals
+// workgroups to the XCDs in turn); XCD x takes pairs x, x + 8, ..., in
+// groups of gp pairs, and within a group issues the q-tiles of all the
+// group's query heads longest first.  A group is about as many q-tiles as
+// one XCD holds at once, so the K/V rows of few pairs are live in that
+// XCD's L2 at a time.  (gp at least the pairs per XCD: every pair of the
+// XCD at once, q-tiles longest first.)
+__device__ __forceinline__ void xcd_pair_map(int bid, int n_qtiles, int B, int Hkv, int G,
+                                             int gp, int& qt, int& b, int& hq) {
+  const int x = bid & 7, j = bid >> 3;
+  const int n_pairs = (B * Hkv) >> 3;  // pairs on this XCD
+  const int grp_items = gp * G * n_qtiles;
+  const int grp = j / grp_items;
+  const int gsz = min(gp, n_pairs - grp * gp);  // pairs in this group (the last may be short)
+  int r = j - grp * grp_items;
+  const int t = r / (gsz * G);  // q-tile rank, longest first
+  r -= t * gsz * G;
+  const int pl = r / G;
+  const int p = x + 8 * (grp * gp + pl);
+  qt = n_qtiles - 1 - t;
+  b = p / Hkv;
+  hq = (p - b * Hkv) * G + (r - pl * G);
+}
+
+// Pairs per group for xcd_pair_map: the q-tiles one XCD holds at once (32
+// compute units, two workgroups each) over the q-tiles of one pair.
+inline int xcd_group_pairs(int G, int n_qtiles) {
+  const int gp = 64 / (G * n_qtiles);
+  return gp < 1 ? 1 : gp;
+}
+
 __device__ __forceinline__ int clamp_len(int len, int hi) {
   return len < 0 ? 0 : (len > hi ? hi : len);
 }
