@@ -69,6 +69,9 @@ def _declare(lib):
     lib.oracle_attn_fwd_varlen.argtypes = [_u16p, _u16p, _u16p, _i32p, _i32p, i, i, i, i, i, i,
                                            i, d, _f64p, _f64p]
     lib.oracle_attn_fwd_varlen.restype = i
+    lib.oracle_attn_fwd_ragged_paged.argtypes = [_u16p, _u16p, _u16p, _i32p, _i32p, _i32p, i, i,
+                                                 i, i, i, i, i, i, i, d, _f64p, _f64p]
+    lib.oracle_attn_fwd_ragged_paged.restype = i
     lib.oracle_attn_bwd.argtypes = [_u16p, _u16p, _u16p, _u16p, i, i, i, i, i, i, i, d, _i32p,
                                     _f64p, _f64p, _f64p]
     lib.oracle_attn_bwd.restype = i
@@ -215,6 +218,37 @@ def attn_fwd_varlen(q, k, v, cu_seqlens_q, cu_seqlens_k, *, causal: bool, scale:
                                     _ptr(lse, _f64p))
     if rc != 0:
         raise ValueError(f"oracle_attn_fwd_varlen failed ({rc})")
+    return o, lse
+
+
+def attn_fwd_ragged_paged(q, k_pages, v_pages, cu_seqlens_q, kv_seqlens, block_table, *,
+                          causal: bool, scale: float, lib=None):
+    """Ragged paged forward.  q [total_q,Hq,D] packed, pages [n_pages,Hkv,page_size,D],
+    cu_seqlens_q int32 [B+1], kv_seqlens int32 [B], block_table int32 [B,max_pages]
+    -> (o [total_q,Hq,D], lse [Hq,total_q]); rows no sequence owns stay NaN."""
+    lib = lib or load()
+    q, kp, vp = _u16(q), _u16(k_pages), _u16(v_pages)
+    total_q, Hq, D = q.shape
+    n_pages, Hkv, page_size, _ = kp.shape
+    cq = np.ascontiguousarray(cu_seqlens_q, dtype=np.int32)
+    if cq.ndim != 1 or cq.shape[0] < 2:
+        raise ValueError("cu_seqlens_q must be [B+1]")
+    B = cq.shape[0] - 1
+    sl = _seqlens(kv_seqlens, B)
+    if sl is None:
+        raise ValueError("kv_seqlens is required")
+    bt = np.ascontiguousarray(block_table, dtype=np.int32)
+    if bt.ndim != 2 or bt.shape[0] != B:
+        raise ValueError("block_table must be [B, max_pages]")
+    o = np.full((total_q, Hq, D), np.nan, np.float64)
+    lse = np.full((Hq, total_q), np.nan, np.float64)
+    rc = lib.oracle_attn_fwd_ragged_paged(_ptr(q, _u16p), _ptr(kp, _u16p), _ptr(vp, _u16p),
+                                          _ptr(cq, _i32p), _ptr(sl, _i32p), _ptr(bt, _i32p), B,
+                                          Hq, Hkv, total_q, page_size, bt.shape[1], n_pages, D,
+                                          int(bool(causal)), float(scale), _ptr(o, _f64p),
+                                          _ptr(lse, _f64p))
+    if rc != 0:
+        raise ValueError(f"oracle_attn_fwd_ragged_paged failed ({rc})")
     return o, lse
 
 

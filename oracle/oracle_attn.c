@@ -2,8 +2,8 @@
  * oracle_attn.c -- plain fp64 CPU oracle for causal grouped-query
  * scaled-dot-product attention (forward), its split-KV decode form,
  * decode over a paged cache (the "Paged Attention" workload of Table 2),
- * the forward over packed variable-length sequences (the ragged batches of
- * the "Ragged Paged Attention" workload of Table 2), the backward
+ * the forward over packed variable-length sequences, the same over a paged
+ * cache (the "Ragged Paged Attention" workload of Table 2), the backward
  * (gradients of the output with respect to q, k and v), and the decode
  * step of multi-head latent attention (the "MLA Attention" workload).
  *
@@ -44,7 +44,9 @@
  * repeated K/V heads, decode equals the last prefill row, split-combine
  * equals unsplit, paged decode equals decode on the cache gathered through
  * the block table, a packed ragged batch equals each of its sequences run
- * alone, the backward equals central finite differences of an independent
+ * alone, the ragged paged forward equals the packed forward over keys
+ * gathered from the pages and the paged decode for one-token sequences,
+ * the backward equals central finite differences of an independent
  * forward, MLA decode equals a decode over the same rows used as K and as
  * zero-padded V) and hand-derived values stored under tests/golden/.
  *
@@ -553,6 +555,93 @@ int oracle_attn_fwd_varlen(const uint16_t *q, const uint16_t *k, const uint16_t 
 }
 
 /* ------------------------------------------------------------------ */
+/* Ragged paged forward: packed queries over a paged key/value cache    */
+/* ------------------------------------------------------------------ */
+
+/*
+ * The "Ragged Paged Attention" workload of Table 2 (prefill chunks and
+ * decode tokens of many sequences in one call, the keys in a paged cache),
+ * with the length clamps of Section 3.4.  Sequence b owns query tokens
+ * [cu_q[b], cu_q[b+1]) of the packed q [total_q, Hq, D] (offsets clamped
+ * into [0, total_q] and made non-decreasing) and L_b = clamp(kv_seqlens[b],
+ * 0, max_pages * page_size) keys; key j of sequence b, kv head g, is row
+ * j % page_size of page block_table[b][j / page_size] of the pools
+ * k_pages / v_pages [n_pages, Hkv, page_size, D] (an entry outside
+ * [0, n_pages) read as the nearest valid page).  The Sq_b queries are the
+ * sequence's last positions: query row i attends to keys j < L_b, and when
+ * causal only to j <= i + L_b - Sq_b.  The plain definition per row,
+ * written out with its own loops:
+ *   s_j = scale * q . k_j,  O = sum_j softmax(s)_j v_j,  LSE = log sum exp s,
+ * no valid key -> O = 0, LSE = -inf.  o [total_q, Hq, D] double, lse
+ * [Hq, total_q] double; rows no sequence owns are not written.
+ */
+int oracle_attn_fwd_ragged_paged(const uint16_t *q, const uint16_t *k_pages,
+                                 const uint16_t *v_pages, const int32_t *cu_q,
+                                 const int32_t *kv_seqlens, const int32_t *block_table,
+                                 int B, int Hq, int Hkv, int total_q, int page_size,
+                                 int max_pages, int n_pages, int D, int causal,
+                                 double scale, double *o, double *lse)
+{
+    if (!q || !k_pages || !v_pages || !cu_q || !kv_seqlens || !block_table || !o || !lse)
+        return -1;
+    if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || total_q < 0 || page_size < 1 ||
+        max_pages < 1 || n_pages < 1 || D < 1 || (causal != 0 && causal != 1))
+        return -2;
+    const int G = Hq / Hkv;
+    const int max_keys = max_pages * page_size;
+    double *s = malloc((size_t)max_keys * sizeof *s);
+    if (!s) return -3;
+    for (int b = 0; b < B; ++b) {
+        int q0, q1;
+        seq_range(cu_q, b, total_q, &q0, &q1);
+        const int Sq = q1 - q0;
+        const int L = clamp_len(kv_seqlens[b], max_keys);
+        for (int hq = 0; hq < Hq; ++hq) {
+            const int g = hq / G;
+            for (int i = 0; i < Sq; ++i) {
+                const uint16_t *q_row = q + ((size_t)(q0 + i) * Hq + hq) * D;
+                double *o_row = o + ((size_t)(q0 + i) * Hq + hq) * D;
+                double *lse_row = &lse[(size_t)hq * total_q + q0 + i];
+                int n_valid = L;
+                if (causal && i + L - Sq + 1 < n_valid) n_valid = i + L - Sq + 1;
+                if (n_valid <= 0) {
+                    for (int d = 0; d < D; ++d) o_row[d] = 0.0;
+                    *lse_row = -INFINITY;
+                    continue;
+                }
+                double m = -INFINITY;
+                for (int j = 0; j < n_valid; ++j) {
+                    const size_t krow = paged_row(block_table, b, max_pages, n_pages,
+                                                  page_size, Hkv, g, j);
+                    double dot = 0.0;
+                    for (int d = 0; d < D; ++d)
+                        dot += bf16_bits_to_double(q_row[d]) *
+                               bf16_bits_to_double(k_pages[krow * D + d]);
+                    s[j] = scale * dot;
+                    if (s[j] > m) m = s[j];
+                }
+                double l = 0.0;
+                for (int j = 0; j < n_valid; ++j) {
+                    s[j] = exp(s[j] - m);
+                    l += s[j];
+                }
+                for (int d = 0; d < D; ++d) o_row[d] = 0.0;
+                for (int j = 0; j < n_valid; ++j) {
+                    const size_t vrow = paged_row(block_table, b, max_pages, n_pages,
+                                                  page_size, Hkv, g, j);
+                    const double p = s[j] / l;
+                    for (int d = 0; d < D; ++d)
+                        o_row[d] += p * bf16_bits_to_double(v_pages[vrow * D + d]);
+                }
+                *lse_row = m + log(l);
+            }
+        }
+    }
+    free(s);
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
 /* Backward: gradients of the output with respect to q, k, v            */
 /* ------------------------------------------------------------------ */
 
@@ -695,4 +784,4 @@ int oracle_mla_decode(const uint16_t *q, const uint16_t *ckv, int B, int H,
     return 0;
 }
 
-int oracle_version(void) { return 5; }
+int oracle_version(void) { return 6; }

@@ -437,6 +437,66 @@ def pin_varlen_gaps_and_clamped_offsets(lib):
         "offsets not clamped"
 
 
+RAGGED_PAGED_CASES = [
+    # Hq, Hkv, D, page_size, max_pages, n_pages, [(Sq_b, L_b), ...]
+    (4, 2, 8, 16, 4, 20, [(5, 37), (1, 64), (0, 10), (7, 3), (16, 16), (3, 0)]),
+    (2, 1, 4, 3, 6, 9, [(4, 17), (2, 2), (6, 5)]),       # odd page size, Sq > L
+    (3, 3, 8, 8, 2, 7, [(2, 100), (1, -4), (4, 16)]),    # lengths clamp to [0, 16]
+]
+
+
+def _ragged_paged_inputs(n, Hq, Hkv, D, ps, mp, npg, seqs):
+    cq = np.concatenate([[0], np.cumsum([a for a, _ in seqs])]).astype(np.int32)
+    q = _rand((max(int(cq[-1]), 1), Hq, D), 240 + n, -2.5, 2.5)
+    kp = _rand((npg, Hkv, ps, D), 250 + n, -2.5, 2.5)
+    vp = _rand((npg, Hkv, ps, D), 260 + n)
+    bt = np.random.default_rng(270 + n).integers(-2, npg + 2, size=(len(seqs), mp),
+                                                  dtype=np.int32)  # some entries out of range
+    lens = np.array([b for _, b in seqs], np.int32)
+    return q, kp, vp, cq, lens, bt
+
+
+def _gather_keys(pages, bt, lens):
+    """Packed [sum L, Hkv, D] rows of every sequence's valid keys, read
+    through the table by numpy indexing (entries clamped into the pool)."""
+    n_pages, Hkv, ps, D = pages.shape
+    rows = []
+    for b, L in enumerate(lens):
+        L = min(max(int(L), 0), bt.shape[1] * ps)
+        j = np.arange(L)
+        rows.append(pages[np.clip(bt[b, j // ps], 0, n_pages - 1), :, j % ps, :])
+    out = np.concatenate(rows) if rows else np.zeros((0, Hkv, D), pages.dtype)
+    return np.ascontiguousarray(out if out.shape[0] else np.zeros((1, Hkv, D), pages.dtype))
+
+
+def pin_ragged_paged_equals_gathered_varlen(lib):
+    for causal in (True, False):
+        for n, (Hq, Hkv, D, ps, mp, npg, seqs) in enumerate(RAGGED_PAGED_CASES):
+            q, kp, vp, cq, lens, bt = _ragged_paged_inputs(n, Hq, Hkv, D, ps, mp, npg, seqs)
+            o, lse = orc.attn_fwd_ragged_paged(q, kp, vp, cq, lens, bt, causal=causal, scale=0.4,
+                                               lib=lib)
+            lc = np.clip(lens, 0, mp * ps)
+            ck = np.concatenate([[0], np.cumsum(lc)]).astype(np.int32)
+            og, lg = orc.attn_fwd_varlen(q, _gather_keys(kp, bt, lens), _gather_keys(vp, bt, lens),
+                                         cq, ck, causal=causal, scale=0.4, lib=lib)
+            tq = int(cq[-1])
+            _close(o[:tq], og[:tq], 1e-13, f"ragged paged case {n} causal={causal} O")
+            _close(lse[:, :tq], lg[:, :tq], 1e-13, f"ragged paged case {n} causal={causal} LSE")
+
+
+def pin_ragged_paged_decode_tokens(lib):
+    # one query token per sequence: the paged decode step
+    Hq, Hkv, D, ps, mp, npg = 4, 2, 8, 4, 6, 11
+    seqs = [(1, 21), (1, 1), (1, 24), (1, 0), (1, 9)]
+    q, kp, vp, cq, lens, bt = _ragged_paged_inputs(7, Hq, Hkv, D, ps, mp, npg, seqs)
+    for causal in (True, False):
+        o, lse = orc.attn_fwd_ragged_paged(q, kp, vp, cq, lens, bt, causal=causal, scale=0.35,
+                                           lib=lib)
+        od, ld = orc.decode_paged(q, kp, vp, bt, lens, scale=0.35, lib=lib)
+        _close(o, od, 1e-13, f"ragged paged decode tokens causal={causal} O")
+        _close(lse.T, ld, 1e-13, f"ragged paged decode tokens causal={causal} LSE")
+
+
 BWD_FD_CASES = [
     # B, Hq, Hkv, Sq, Skv, D, causal, seqlens
     (1, 2, 1, 4, 4, 3, True, None),
@@ -558,5 +618,6 @@ ALL_PINS = [pin_golden, pin_brute_force, pin_rows_sum_to_one, pin_probs_brute_fo
             pin_decode_equals_last_prefill_row, pin_split_combine, pin_row_subset,
             pin_paged_equals_gathered, pin_paged_table_clamp_and_unused_pages,
             pin_varlen_equals_each_sequence, pin_varlen_gaps_and_clamped_offsets,
+            pin_ragged_paged_equals_gathered_varlen, pin_ragged_paged_decode_tokens,
             pin_bwd_finite_differences, pin_bwd_gqa_sums_repeated_heads,
             pin_mla_brute_force, pin_mla_equals_padded_decode, pin_mla_single_key_and_rope]

@@ -67,6 +67,14 @@ MUTANTS = {
                             "s[j] = dot;\n                }\n                double m = s[0];", 1),
     "probs_gqa_interleaved_heads": ("int g = hq / G;\n                int L = clamp_len(",
                                     "int g = hq % Hkv;\n                int L = clamp_len(", 1),
+    "ragged_paged_causal_top_left": ("if (causal && i + L - Sq + 1 < n_valid) n_valid = i + L - Sq + 1;",
+                                     "if (causal && i + 1 < n_valid) n_valid = i + 1;", 1),
+    "ragged_paged_value_head_zero": ("page_size, Hkv, g, j);\n                    const double p = s[j] / l;",
+                                     "page_size, Hkv, 0, j);\n                    const double p = s[j] / l;", 1),
+    "ragged_paged_last_key_dropped": ("int n_valid = L;\n                if (causal && i + L - Sq",
+                                      "int n_valid = L > 1 ? L - 1 : L;\n                if (causal && i + L - Sq", 1),
+    "ragged_paged_lse_token_major": ("double *lse_row = &lse[(size_t)hq * total_q + q0 + i];",
+                                     "double *lse_row = &lse[(size_t)(q0 + i) * Hq + hq];", 1),
     "varlen_key_start_ignored": ("const uint16_t *k_row = k + ((size_t)(k0 + j) * Hkv + g) * D;",
                                  "const uint16_t *k_row = k + ((size_t)(j) * Hkv + g) * D;", 1),
 }
