@@ -114,6 +114,51 @@ int mk_attn_fwd_varlen(const void *q, const void *k, const void *v, void *o, flo
                        int causal, float scale, void *stream);
 
 /*
+ * Ragged paged attention (the paper's "Ragged Paged Attention" workload,
+ * Table 2; length clamps as in Section 3.4): a packed batch of query
+ * chunks of many sequences -- decode tokens, prefill chunks and whole
+ * prompts in one call -- attending to their sequences' keys and values in
+ * a paged cache.  Sequence b's Sq_b query tokens are its last positions,
+ * and its keys (including the new tokens', already written to the cache)
+ * are the first L_b rows its block table lists.
+ *   q, o            [total_q, Hq, D] bf16, token-major; o written only at
+ *                   rows some sequence owns
+ *   k_pages, v_pages  [n_pages, Hkv, page_size, D] bf16 page pools; key j
+ *                   of sequence b, kv head g, is row j % page_size of page
+ *                   block_table[b][j / page_size], head g
+ *   block_table     device int32 [B, max_pages]; an entry outside
+ *                   [0, n_pages) is read as the nearest valid page;
+ *                   entries at or past ceil(L_b / page_size) are not read
+ *   lse             [Hq, total_q] fp32 natural-log LSE (written at owned
+ *                   rows), or NULL to skip
+ *   cu_seqlens_q    device int32 [B + 1]: sequence b owns query tokens
+ *                   [cu_seqlens_q[b], cu_seqlens_q[b + 1]) (offsets clamped
+ *                   into [0, total_q], a decreasing pair is empty);
+ *                   sequences must not share query rows
+ *   kv_seqlens      device int32 [B]: L_b, clamped into
+ *                   [0, max_pages * page_size]
+ *   max_seqlen_q    at least every sequence's query count (rows past it are
+ *                   not computed)
+ *   causal          0 or 1; causal is bottom-right per sequence: query i
+ *                   sees keys j <= i + L_b - Sq_b
+ *   page_size       keys per page, a positive multiple of 16
+ *                   (MK_ERR_UNSUPPORTED otherwise)
+ *   B, Hq, Hkv, max_seqlen_q, total_q, max_pages, n_pages >= 1,
+ *   Hq % Hkv == 0, D in {64, 128}; max_pages * page_size and
+ *   B * max_pages must fit in 31 bits (MK_ERR_SHAPE); scale, stream as
+ *   mk_attn_fwd.
+ * The result is mk_attn_fwd_varlen's on the keys and values gathered from
+ * the pages (bitwise the same).  Returns MK_OK or an mk_status;
+ * asynchronous on `stream`.
+ */
+int mk_attn_fwd_ragged_paged(const void *q, const void *k_pages, const void *v_pages,
+                             const int *block_table, void *o, float *lse,
+                             const int *cu_seqlens_q, const int *kv_seqlens, int B, int Hq,
+                             int Hkv, int max_seqlen_q, int total_q, int page_size,
+                             int max_pages, int n_pages, int D, int causal, float scale,
+                             void *stream);
+
+/*
  * Decode step: one query token per sequence against a key/value cache
  * (the decode step of the paper's paged-attention workloads, Table 2),
  * computed as split-KV attention whose per-split results are merged by

@@ -24,7 +24,7 @@ MK_STATUS = {0: "MK_OK", 1: "MK_ERR_NULL", 2: "MK_ERR_SHAPE", 3: "MK_ERR_UNSUPPO
              8: "MK_ERR_SCRATCH"}
 
 # every symbol include/mk_attn.h declares
-EXPORTS = ("mk_attn_fwd", "mk_attn_fwd_o32", "mk_attn_fwd_varlen",
+EXPORTS = ("mk_attn_fwd", "mk_attn_fwd_o32", "mk_attn_fwd_varlen", "mk_attn_fwd_ragged_paged",
            "mk_attn_decode_workspace_bytes", "mk_attn_decode", "mk_attn_decode_paged",
            "mk_attn_decode_noalloc", "mk_attn_decode_noalloc_max_bytes",
            "mk_attn_decode_default_parts", "mk_attn_bwd", "mk_attn_bwd_workspace_bytes",
@@ -57,6 +57,9 @@ def lib():
         h.mk_attn_fwd_o32.restype = i
         h.mk_attn_fwd_varlen.argtypes = [vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, i, f, vp]
         h.mk_attn_fwd_varlen.restype = i
+        h.mk_attn_fwd_ragged_paged.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i,
+                                               i, i, i, i, f, vp]
+        h.mk_attn_fwd_ragged_paged.restype = i
         h.mk_attn_decode_workspace_bytes.argtypes = [i, i, i, i]
         h.mk_attn_decode_workspace_bytes.restype = sz
         h.mk_attn_decode.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, f, vp, i, vp, sz, vp]
@@ -154,6 +157,16 @@ def mk_attn_fwd_varlen(q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, B, Hq, Hkv, 
                                     _ptr(cu_seqlens_q), _ptr(cu_seqlens_k), B, Hq, Hkv,
                                     max_seqlen_q, total_q, total_k, D, int(causal), float(scale),
                                     _stream(stream)))
+
+
+def mk_attn_fwd_ragged_paged(q, k_pages, v_pages, block_table, o, lse, cu_seqlens_q, kv_seqlens,
+                             B, Hq, Hkv, max_seqlen_q, total_q, page_size, max_pages, n_pages, D,
+                             causal, scale, stream=None):
+    _check(lib().mk_attn_fwd_ragged_paged(_ptr(q), _ptr(k_pages), _ptr(v_pages),
+                                          _ptr(block_table), _ptr(o), _ptr(lse),
+                                          _ptr(cu_seqlens_q), _ptr(kv_seqlens), B, Hq, Hkv,
+                                          max_seqlen_q, total_q, page_size, max_pages, n_pages,
+                                          D, int(causal), float(scale), _stream(stream)))
 
 
 def mk_attn_decode(q, k_cache, v_cache, o, lse, B, Hq, Hkv, Smax, D, scale, kv_seqlens,
@@ -302,6 +315,36 @@ def fwd_varlen(q, k, v, cu_seqlens_q, cu_seqlens_k, max_seqlen_q: int, *, causal
     lse = torch.empty((Hq, total_q), device=q.device, dtype=torch.float32) if with_lse else None
     mk_attn_fwd_varlen(q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, B, Hq, Hkv, max_seqlen_q,
                        total_q, total_k, D, causal, scale, stream)
+    return o, lse
+
+
+def fwd_ragged_paged(q, k_pages, v_pages, block_table, cu_seqlens_q, kv_seqlens,
+                     max_seqlen_q: int, *, causal: bool = True, scale: float | None = None,
+                     with_lse: bool = True, stream=None):
+    """Ragged paged forward.  q [total_q,Hq,D] bf16 packed, page pools
+    [n_pages,Hkv,page_size,D] bf16, block_table int32 [B,max_pages],
+    cu_seqlens_q int32 [B+1], kv_seqlens int32 [B] (device)
+    -> (o [total_q,Hq,D], lse [Hq,total_q] or None).  Rows no sequence owns
+    are left as allocated (uninitialised)."""
+    import torch
+    _require(q, "q", torch.bfloat16, 3)
+    _require(k_pages, "k_pages", torch.bfloat16, 4)
+    _require(v_pages, "v_pages", torch.bfloat16, 4)
+    _require(block_table, "block_table", torch.int32, 2)
+    _require(cu_seqlens_q, "cu_seqlens_q", torch.int32, 1)
+    _require(kv_seqlens, "kv_seqlens", torch.int32, 1)
+    total_q, Hq, D = q.shape
+    n_pages, Hkv, page_size, _ = k_pages.shape
+    B, max_pages = block_table.shape
+    if cu_seqlens_q.shape[0] != B + 1 or kv_seqlens.shape[0] != B:
+        raise ValueError("cu_seqlens_q must be [B+1] and kv_seqlens [B]")
+    if scale is None:
+        scale = D ** -0.5
+    o = torch.empty((total_q, Hq, D), device=q.device, dtype=torch.bfloat16)
+    lse = torch.empty((Hq, total_q), device=q.device, dtype=torch.float32) if with_lse else None
+    mk_attn_fwd_ragged_paged(q, k_pages, v_pages, block_table, o, lse, cu_seqlens_q, kv_seqlens,
+                             B, Hq, Hkv, max_seqlen_q, total_q, page_size, max_pages, n_pages, D,
+                             causal, scale, stream)
     return o, lse
 
 

@@ -52,6 +52,16 @@ struct FwdArgs {
   const int* cu_q;
   const int* cu_k;
   int total_q, total_k;
+  // packed queries over a paged cache (PAGED) only: k, v are page pools
+  // [n_pages, Hkv, page_size, D]; key j of sequence b is row j % page_size
+  // of page block_table[b][j / page_size]; sequence b has kv_seqlens[b] keys
+  const int* block_table;
+  int page_size, max_pages, n_pages;
+  // r / page_size = (r * ps_magic) >> ps_shift for 0 <= r < 2^31
+  // (ps_magic = floor(2^ps_shift / page_size) + 1, ps_shift = 31 +
+  // ceil(log2 page_size): exact for 31-bit dividends)
+  uint64_t ps_magic;
+  int ps_shift;
 };
 
 // Tokens [start, end) of sequence b from cumulative offsets, clamped into
@@ -107,8 +117,15 @@ __device__ __forceinline__ void fwd_map_block(int bid, const FwdArgs& a, int& qt
 // the scale folded into the exponent's FMA.  Otherwise scores are scaled
 // first (scale 0 and negative scales).  VARLEN: a packed ragged batch (see
 // FwdArgs); only where rows live changes, the tile pipeline is the same.
-template <int D, bool CAUSAL, bool OUT_F32, int QB, bool POS_SCALE, bool VARLEN, int WAVES>
+// PAGED (with VARLEN): the keys and values of the packed queries' sequences
+// come from a paged cache; each wave's 1 KB block of a tile is 4 (D = 128)
+// or 8 (D = 64) consecutive key rows, which lie in one page since pages
+// hold a multiple of 16 keys, so the page of every block is one table
+// entry, read through the scalar cache at the start of the step.
+template <int D, bool CAUSAL, bool OUT_F32, int QB, bool POS_SCALE, bool VARLEN, int WAVES,
+          bool PAGED = false>
 __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
+  static_assert(VARLEN || !PAGED, "the paged cache is read by the packed forward");
   using S = FwdShape<D, QB, WAVES>;
   constexpr int BN = S::BN;
   constexpr int TILE = BN * D;            // bf16 per tile per tensor
@@ -145,17 +162,29 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
   const char* kg;
   const char* vg;
   if constexpr (VARLEN) {
-    int qs, ks;
+    int qs, ks = 0;
     fwd_seq_range(a.cu_q, b, a.total_q, qs, Sq);
-    fwd_seq_range(a.cu_k, b, a.total_k, ks, L);
+    if constexpr (PAGED)
+      L = clamp_len(a.kv_seqlens[b], a.max_pages * a.page_size);
+    else
+      fwd_seq_range(a.cu_k, b, a.total_k, ks, L);
     if (qt * S::BM >= Sq) return;  // past this sequence's queries (whole workgroup)
     o_base = ((size_t)qs * a.Hq + hq) * D;
     q_stride = (size_t)a.Hq * D;
-    kv_stride = (size_t)a.Hkv * ROW_BYTES;
     if (lse_base) lse_base += (size_t)hq * a.total_q + qs;
-    const size_t kv_off = ((size_t)ks * a.Hkv + g) * D;
-    kg = reinterpret_cast<const char*>(a.k + kv_off);
-    vg = reinterpret_cast<const char*>(a.v + kv_off);
+    if constexpr (PAGED) {
+      // rows of one head inside a page are consecutive; kg / vg point at
+      // head g of page 0 (page p adds p * Hkv * page_size rows)
+      kv_stride = ROW_BYTES;
+      const size_t kv_off = (size_t)g * a.page_size * D;
+      kg = reinterpret_cast<const char*>(a.k + kv_off);
+      vg = reinterpret_cast<const char*>(a.v + kv_off);
+    } else {
+      kv_stride = (size_t)a.Hkv * ROW_BYTES;
+      const size_t kv_off = ((size_t)ks * a.Hkv + g) * D;
+      kg = reinterpret_cast<const char*>(a.k + kv_off);
+      vg = reinterpret_cast<const char*>(a.v + kv_off);
+    }
   } else {
     Sq = a.Sq;
     L = a.kv_seqlens ? clamp_len(a.kv_seqlens[b], a.Skv) : a.Skv;
@@ -214,11 +243,46 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
   // goes through a buffer resource on the tile with the lane offset
   // full_off and the block's (wave-uniform) offset p * ROW_STEP rows.
   const uint32_t full_off = (uint32_t)(dma_row * kv_stride + dma_ch);
+  // PAGED: byte offset, from kg / vg, of key row r (the same in every lane)
+  // of this sequence: row r % page_size of its page, the table entry read
+  // through the scalar cache and clamped into the pool.
+  auto page_row = [&](int r) -> size_t {
+    const uint32_t ru = (uint32_t)__builtin_amdgcn_readfirstlane(r);
+    const uint32_t pi = (uint32_t)(((uint64_t)ru * a.ps_magic) >> a.ps_shift);  // ru / page_size
+    const __attribute__((address_space(4))) int* bt =
+        (const __attribute__((address_space(4))) int*)(a.block_table + (size_t)b * a.max_pages);
+    int pg = bt[pi];
+    pg = pg < 0 ? 0 : (pg >= a.n_pages ? a.n_pages - 1 : pg);
+    return ((size_t)pg * a.Hkv * a.page_size + (ru - pi * (uint32_t)a.page_size)) * ROW_BYTES;
+  };
+  // PAGED: a lane's byte offset within its wave's block (row, then chunk)
+  const uint32_t paged_lane_off = (uint32_t)((lane / S::CHUNKS) * ROW_BYTES + dma_ch);
+  // PAGED: first row this wave reads for block p of tile kt (its own block,
+  // or the sequence's last row when the block lies wholly past it)
+  auto block_row = [&](int kt, int p) {
+    const int r0 = kt * BN + (p * S::WAVES + wave) * S::ROWS_PER_KB;
+    return r0 < L ? r0 : L - 1;
+  };
   auto issue_rows = [&](const char* g, uint32_t lds_w, int kt, auto buf_tag, auto p_tag,
-                        auto full_tag) {
+                        auto full_tag, size_t page_off = 0) {
     constexpr int BUF = decltype(buf_tag)::value;
     constexpr int P = decltype(p_tag)::value;
     constexpr uint32_t lds_off = BUF * TILE_BYTES + P * S::WAVES * 1024;
+    if constexpr (PAGED) {
+      // page_off = page_row(block_row(kt, P)): the wave's block through a
+      // buffer resource on its rows in the page; a lane's row within the
+      // block is clamped to the sequence's last row
+      const char* blk = g + page_off;
+      if constexpr (decltype(full_tag)::value) {
+        load_lds16_buf(blk, S::ROWS_PER_KB * ROW_BYTES, paged_lane_off, lds_w + lds_off);
+      } else {
+        const int r0 = kt * BN + (P * S::WAVES + wave) * S::ROWS_PER_KB;
+        const int lr = r0 < L ? min(lane / S::CHUNKS, L - 1 - r0) : 0;
+        load_lds16_buf(blk, S::ROWS_PER_KB * ROW_BYTES, (uint32_t)(lr * ROW_BYTES + dma_ch),
+                       lds_w + lds_off);
+      }
+      return;
+    }
     // kt is the same in every lane; saying so keeps the tile address, and so
     // the load's buffer resource, in scalar registers
     const char* tile = g + (size_t)__builtin_amdgcn_readfirstlane(kt) * BN * kv_stride;
@@ -248,8 +312,10 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
   using B0 = std::integral_constant<int, 0>;
   using B1 = std::integral_constant<int, 1>;
   if (n_kt > 0)
-    static_for<0, S::BLOCKS_PER_WAVE>(
-        [&](auto p_tag) { issue_rows(kg, k_lds_w, 0, B0(), p_tag, std::false_type()); });
+    static_for<0, S::BLOCKS_PER_WAVE>([&](auto p_tag) {
+      issue_rows(kg, k_lds_w, 0, B0(), p_tag, std::false_type(),
+                 PAGED ? page_row(block_row(0, decltype(p_tag)::value)) : 0);
+    });
 
   // Lane parts of the LDS read addresses (bytes within a tile).  K row
   // 32 kb + n: the swizzle of n + 32 kb equals that of n.  Transposing V
@@ -344,10 +410,24 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
     }
     const bool load_k = t + 1 < n_kt;
     const bool load_v = t >= 1 && t - 1 < n_kt;
+    // PAGED: the pages of this step's blocks, looked up before any LDS read
+    // is in flight (so the wait for them waits for nothing else)
+    size_t pk_off[S::BLOCKS_PER_WAVE], pv_off[S::BLOCKS_PER_WAVE];
+    if constexpr (PAGED) {
+#pragma unroll
+      for (int p = 0; p < S::BLOCKS_PER_WAVE; ++p) {
+        pk_off[p] = (STEADY || load_k) ? page_row(block_row(t + 1, p)) : 0;
+        pv_off[p] = (STEADY || load_v) ? page_row(block_row(t - 1, p)) : 0;
+      }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    }
     auto load_block = [&](auto p_tag) {
       using NB_ = std::integral_constant<int, 1 - PAR>;
-      if (STEADY || load_k) issue_rows(kg, k_lds_w, t + 1, NB_(), p_tag, steady_tag);
-      if (STEADY || load_v) issue_rows(vg, v_lds_w, t - 1, NB_(), p_tag, steady_tag);
+      constexpr int P_ = decltype(p_tag)::value;
+      if (STEADY || load_k)
+        issue_rows(kg, k_lds_w, t + 1, NB_(), p_tag, steady_tag, PAGED ? pk_off[P_] : 0);
+      if (STEADY || load_v)
+        issue_rows(vg, v_lds_w, t - 1, NB_(), p_tag, steady_tag, PAGED ? pv_off[P_] : 0);
     };
 
     // ---- LDS read stream: the NV transposing V reads of tile t - 2 in the
@@ -565,13 +645,69 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
     // rescale to the exact maximum, and new weights.  O holds tiles up to
     // t - 2 here, so its rescale is immediate.  Then the sums join the
     // running ones. ----
+    // the rescale to the exact maximum of re-formed scores S(t - 1) (in
+    // s_old) and the tile's new weights
+    auto settle_tail = [&](int qb) {
+      float mx = kNegInf;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s_old[qb][kb][r]);
+      mx = max_xor32(mx) * c;
+      const float m_new = fmaxf(m_run[qb], mx);
+      const float alpha = (m_new == kNegInf) ? 1.f : fast_exp2(m_run[qb] - m_new);
+      m_run[qb] = m_new;
+      l_run[qb] *= alpha;
+#pragma unroll
+      for (int db = 0; db < S::DBLK; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o_acc[qb][db][r] *= alpha;
+      m_use[qb] = (m_new == kNegInf) ? 0.f : m_new;
+      l_tile[qb] = 0.f;
+      static_for<0, 4>([&](auto kc_tag) {
+        constexpr int KC = decltype(kc_tag)::value;
+        constexpr int R = 8 * (KC % 2);
+        f32x16& x = s_old[qb][KC / 2];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[R + e] = fast_exp2(fmaf(x[R + e], c, -m_use[qb]));
+        l_tile[qb] += ((x[R] + x[R + 1]) + (x[R + 2] + x[R + 3])) +
+                      ((x[R + 4] + x[R + 5]) + (x[R + 6] + x[R + 7]));
+        p_new[qb][KC] = as_u32x4(to_bf16x8(x[R], x[R + 1], x[R + 2], x[R + 3], x[R + 4],
+                                           x[R + 5], x[R + 6], x[R + 7]));
+      });
+    };
     if constexpr (EX) {
       if constexpr (POS_SCALE && !HEAD) {
         // only tiles 1 .. n_free - 1 are weighed without their maximum; they
         // lie wholly inside the sequence, so their K rows can be read again
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
-          if (__ballot(l_tile[qb] > kSumLimit)) {
+          if (PAGED && __ballot(l_tile[qb] > kSumLimit)) {
+            // the tile's key rows through the block table: each 16-row half
+            // of a 32-key block lies in one page, read through a resource of
+            // its own, and a lane keeps the half its row is in
+            const uint32_t lane_off = (uint32_t)((n & 15) * ROW_BYTES + 16 * h);
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+              const __amdgpu_buffer_rsrc_t lo = __builtin_amdgcn_make_buffer_rsrc(
+                  const_cast<char*>(kg + page_row(tw * BN + 32 * kb)), 0, 16 * ROW_BYTES,
+                  0x00020000);
+              const __amdgpu_buffer_rsrc_t hi = __builtin_amdgcn_make_buffer_rsrc(
+                  const_cast<char*>(kg + page_row(tw * BN + 32 * kb + 16)), 0, 16 * ROW_BYTES,
+                  0x00020000);
+#pragma unroll
+              for (int r2 = 0; r2 < 16; ++r2) s_old[qb][kb][r2] = 0.f;
+#pragma unroll
+              for (int st = 0; st < S::KSTEPS; ++st) {
+                const u32x4 ul = __builtin_amdgcn_raw_buffer_load_b128(lo, lane_off, 32 * st, 0);
+                const u32x4 uh = __builtin_amdgcn_raw_buffer_load_b128(hi, lane_off, 32 * st, 0);
+                const u32x4 u = n < 16 ? ul : uh;
+                s_old[qb][kb] = mfma32(as_bf16x8(u), qf[qb][st], s_old[qb][kb]);
+                __builtin_amdgcn_sched_barrier(0);
+              }
+            }
+            settle_tail(qb);
+          } else if (!PAGED && __ballot(l_tile[qb] > kSumLimit)) {
             // (the base is made wave-uniform explicitly: a resource in vector
             // registers would need a loop over its distinct values)
             const uintptr_t base = (uintptr_t)(kg + (size_t)tw * BN * kv_stride);
@@ -595,33 +731,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
                 __builtin_amdgcn_sched_barrier(0);  // one fragment in registers at a time
               }
             }
-            float mx = kNegInf;
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-              for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s_old[qb][kb][r]);
-            mx = max_xor32(mx) * c;
-            const float m_new = fmaxf(m_run[qb], mx);
-            const float alpha = (m_new == kNegInf) ? 1.f : fast_exp2(m_run[qb] - m_new);
-            m_run[qb] = m_new;
-            l_run[qb] *= alpha;
-#pragma unroll
-            for (int db = 0; db < S::DBLK; ++db)
-#pragma unroll
-              for (int r = 0; r < 16; ++r) o_acc[qb][db][r] *= alpha;
-            m_use[qb] = (m_new == kNegInf) ? 0.f : m_new;
-            l_tile[qb] = 0.f;
-            static_for<0, 4>([&](auto kc_tag) {
-              constexpr int KC = decltype(kc_tag)::value;
-              constexpr int R = 8 * (KC % 2);
-              f32x16& x = s_old[qb][KC / 2];
-#pragma unroll
-              for (int e = 0; e < 8; ++e) x[R + e] = fast_exp2(fmaf(x[R + e], c, -m_use[qb]));
-              l_tile[qb] += ((x[R] + x[R + 1]) + (x[R + 2] + x[R + 3])) +
-                            ((x[R + 4] + x[R + 5]) + (x[R + 6] + x[R + 7]));
-              p_new[qb][KC] = as_u32x4(to_bf16x8(x[R], x[R + 1], x[R + 2], x[R + 3], x[R + 4],
-                                                 x[R + 5], x[R + 6], x[R + 7]));
-            });
+            settle_tail(qb);
           }
         }
       }

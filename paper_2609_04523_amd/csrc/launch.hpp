@@ -24,6 +24,10 @@ hipError_t launch_fwd(const FwdArgs& a, unsigned nblocks, int D, bool causal, bo
 hipError_t launch_fwd_varlen(const FwdArgs& a, unsigned nblocks, int D, bool causal,
                              bool pos_scale, hipStream_t st);
 
+// Packed queries over a paged cache (bf16 O).
+hipError_t launch_fwd_ragged_paged(const FwdArgs& a, unsigned nblocks, int D, bool causal,
+                                   bool pos_scale, hipStream_t st);
+
 // Decode: the part kernel (contiguous or paged cache) then the merge kernel.
 hipError_t launch_decode(const DecArgs& a, int D, int qblocks, bool paged, hipStream_t st);
 

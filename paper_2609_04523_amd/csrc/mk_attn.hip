@@ -15,7 +15,7 @@
 
 namespace {
 
-constexpr int kVersion = 7;
+constexpr int kVersion = 8;
 constexpr int kComputeUnits = 256;    // MI355X
 constexpr int kLdsPerCu = 160 * 1024; // gfx950
 constexpr int kMaxParts = 1 << 20;    // decode parts per call
@@ -72,6 +72,10 @@ int fwd_impl(const void* q, const void* k, const void* v, void* o, float* lse, i
   a.scale_log2 = scale * mk::kLog2e;
   a.cu_q = a.cu_k = nullptr;
   a.total_q = a.total_k = 0;
+  a.block_table = nullptr;
+  a.page_size = a.max_pages = a.n_pages = 0;
+  a.ps_magic = 0;
+  a.ps_shift = 0;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool pos = scale > 0.f;
   const hipError_t e = mk::launch_fwd(a, (unsigned)nblocks, D, causal, out_f32, pos, st);
@@ -246,9 +250,77 @@ int mk_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o, flo
   a.cu_k = cu_seqlens_k;
   a.total_q = total_q;
   a.total_k = total_k;
+  a.block_table = nullptr;
+  a.page_size = a.max_pages = a.n_pages = 0;
+  a.ps_magic = 0;
+  a.ps_shift = 0;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool pos = scale > 0.f;
   const hipError_t e = mk::launch_fwd_varlen(a, (unsigned)nblocks, D, causal, pos, st);
+  return e == hipSuccess ? MK_OK : MK_ERR_HIP;
+}
+
+int mk_attn_fwd_ragged_paged(const void* q, const void* k_pages, const void* v_pages,
+                             const int* block_table, void* o, float* lse,
+                             const int* cu_seqlens_q, const int* kv_seqlens, int B, int Hq,
+                             int Hkv, int max_seqlen_q, int total_q, int page_size,
+                             int max_pages, int n_pages, int D, int causal, float scale,
+                             void* stream) {
+  if (!q || !k_pages || !v_pages || !block_table || !o || !cu_seqlens_q || !kv_seqlens)
+    return MK_ERR_NULL;
+  if (B < 1 || Hq < 1 || Hkv < 1 || max_seqlen_q < 1 || total_q < 1 || D < 1 ||
+      page_size < 1 || max_pages < 1 || n_pages < 1)
+    return MK_ERR_SHAPE;
+  if (Hq % Hkv != 0) return MK_ERR_SHAPE;
+  if (D != 64 && D != 128) return MK_ERR_UNSUPPORTED;
+  // a wave's 1 KB block of a tile (4 or 8 key rows) must lie in one page
+  if (page_size % 16 != 0) return MK_ERR_UNSUPPORTED;
+  if (causal != 0 && causal != 1) return MK_ERR_ARG;
+  if (!isfinite(scale)) return MK_ERR_ARG;
+  if (!aligned(q, 16) || !aligned(k_pages, 16) || !aligned(v_pages, 16) || !aligned(o, 16) ||
+      !aligned(cu_seqlens_q, 4) || !aligned(kv_seqlens, 4) || !aligned(block_table, 4))
+    return MK_ERR_ALIGN;
+  if (lse && !aligned(lse, 4)) return MK_ERR_ALIGN;
+  const int BM = mk::FwdShape<128, mk::kFwdQB, mk::kFwdWaves>::BM;
+  const long long n_qtiles = (max_seqlen_q + BM - 1) / BM;
+  const long long nblocks = n_qtiles * B * Hq;
+  // workgroups of one launch, key positions and table indices are 32-bit
+  if (nblocks > 0x7fffffffLL || (long long)max_pages * page_size > 0x7fffffffLL ||
+      (long long)B * max_pages > 0x7fffffffLL || B > 0x7ffffffe)
+    return MK_ERR_SHAPE;
+
+  mk::FwdArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k_pages);
+  a.v = static_cast<const uint16_t*>(v_pages);
+  a.o = o;
+  a.lse = lse;
+  a.kv_seqlens = kv_seqlens;
+  a.B = B;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.Sq = max_seqlen_q;
+  a.Skv = 0;
+  a.n_qtiles = (int)n_qtiles;
+  a.xcd_gp = 0;
+  a.scale_log2 = scale * mk::kLog2e;
+  a.cu_q = cu_seqlens_q;
+  a.cu_k = nullptr;
+  a.total_q = total_q;
+  a.total_k = 0;
+  a.block_table = block_table;
+  a.page_size = page_size;
+  a.max_pages = max_pages;
+  a.n_pages = n_pages;
+  {
+    int l = 0;  // ceil(log2 page_size)
+    while ((1LL << l) < page_size) ++l;
+    a.ps_shift = 31 + l;
+    a.ps_magic = ((uint64_t)1 << a.ps_shift) / (uint64_t)page_size + 1;
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const bool pos = scale > 0.f;
+  const hipError_t e = mk::launch_fwd_ragged_paged(a, (unsigned)nblocks, D, causal, pos, st);
   return e == hipSuccess ? MK_OK : MK_ERR_HIP;
 }
 

@@ -43,7 +43,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert mk.mk_attn_version() == 7
+    assert mk.mk_attn_version() == 8
     names = ["MK_OK", "MK_ERR_NULL", "MK_ERR_SHAPE", "MK_ERR_UNSUPPORTED", "MK_ERR_ALIGN",
              "MK_ERR_WORKSPACE", "MK_ERR_HIP", "MK_ERR_ARG", "MK_ERR_SCRATCH"]
     for code, name in enumerate(names):
@@ -87,6 +87,32 @@ def varlen_rc(lib, *, q=P, k=P, v=P, o=P, lse=None, cq=P, ck=P, B=3, Hq=8, Hkv=2
               total_q=300, total_k=400, D=128, causal=1, scale=0.125):
     return lib.mk_attn_fwd_varlen(q, k, v, o, lse, cq, ck, B, Hq, Hkv, max_sq, total_q, total_k,
                                   D, causal, scale, None)
+
+
+def rpa_rc(lib, *, q=P, kp=P, vp=P, bt=P, o=P, lse=None, cq=P, sl=P, B=3, Hq=8, Hkv=2,
+           max_sq=100, total_q=300, ps=16, mp=64, npg=200, D=128, causal=1, scale=0.125):
+    return lib.mk_attn_fwd_ragged_paged(q, kp, vp, bt, o, lse, cq, sl, B, Hq, Hkv, max_sq,
+                                        total_q, ps, mp, npg, D, causal, scale, None)
+
+
+def test_fwd_ragged_paged_validation(lib):
+    for name in ("q", "kp", "vp", "bt", "o", "cq", "sl"):
+        assert rpa_rc(lib, **{name: None}) == 1
+    for name in ("B", "Hq", "Hkv", "max_sq", "total_q", "ps", "mp", "npg"):
+        assert rpa_rc(lib, **{name: 0}) == 2
+    assert rpa_rc(lib, Hq=6, Hkv=4) == 2
+    assert rpa_rc(lib, mp=1 << 20, ps=4096) == 2           # key positions past 31 bits
+    assert rpa_rc(lib, B=1 << 16, mp=1 << 16) == 2          # table entries past 31 bits
+    assert rpa_rc(lib, D=96) == 3
+    for ps in (8, 24, 40):
+        assert rpa_rc(lib, ps=ps) == 3                      # pages of a multiple of 16 keys
+    assert rpa_rc(lib, causal=2) == 7
+    assert rpa_rc(lib, scale=math.inf) == 7
+    for name in ("q", "kp", "vp", "o"):
+        assert rpa_rc(lib, **{name: P_ODD}) == 4
+    for name in ("cq", "sl", "bt"):
+        assert rpa_rc(lib, **{name: P + 2}) == 4
+    assert rpa_rc(lib, lse=P + 2) == 4
 
 
 def test_fwd_varlen_validation(lib):

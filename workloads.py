@@ -194,6 +194,27 @@ def paged_layout(k_cache: torch.Tensor, v_cache: torch.Tensor, page_size: int, s
     return kp, vp, bt
 
 
+def ragged_paged_inputs(seqs, Hq: int, Hkv: int, D: int, page_size: int, seed: int,
+                        extra_pages: int = 0, k_mult: float = 1.0):
+    """Seeded inputs of a ragged paged batch, sequences [(Sq_b, L_b), ...]:
+    Sq_b packed query tokens and L_b keys each (L_b may be 0, negative or past
+    the table, exercising the clamps).  q [total_q,Hq,D] randn in fp32 (then
+    bf16); contiguous caches [B,Hkv,max_pages*page_size,D] randn (K times
+    k_mult) scattered into NaN-poisoned page pools by paged_layout.  Returns
+    (q, k_pages, v_pages, block_table, cu_q int32 [B+1], lens int32 [B],
+    k_cache, v_cache)."""
+    g = _gen(seed)
+    cu = torch.zeros(len(seqs) + 1, dtype=torch.int32)
+    cu[1:] = torch.cumsum(torch.tensor([a for a, _ in seqs], dtype=torch.int32), 0)
+    lens = torch.tensor([b for _, b in seqs], dtype=torch.int32)
+    mp = max(1, max(-(-max(0, b) // page_size) for _, b in seqs))
+    q = torch.randn((max(int(cu[-1]), 1), Hq, D), generator=g).to(torch.bfloat16)
+    kc = (torch.randn((len(seqs), Hkv, mp * page_size, D), generator=g) * k_mult).to(torch.bfloat16)
+    vc = torch.randn((len(seqs), Hkv, mp * page_size, D), generator=g).to(torch.bfloat16)
+    kp, vp, bt = paged_layout(kc, vc, page_size, seed + 1, extra_pages=extra_pages, lens=lens)
+    return q, kp, vp, bt, cu, lens, kc, vc
+
+
 def sample_rows(B: int, Hq: int, S: int, nrows: int, seed: int) -> torch.Tensor:
     """int32 [B,Hq,nrows] of query rows: 0 and S-1 plus nrows-2 distinct
     rows drawn from a per-(b, hq) seeded permutation."""
