@@ -264,7 +264,7 @@ def _pmc_all(path: str):
     return out
 
 
-LEGS_ALL = "c3,c2,c1,decode,varlen,paged,bwd,mla"
+LEGS_ALL = "c3,c2,c1,decode,varlen,rpa,paged,bwd,mla"
 
 
 def prefill_alg_bytes(cfg) -> int:
@@ -621,6 +621,55 @@ def main():
         }
         log(f"[bench] varlen prefill: {ms * 1e3:.1f} us")
         del vb, vq, vk, vv
+    if "rpa" in legs:
+        # prefill chunks and decode tokens over a paged cache in one call,
+        # against the packed forward on the same keys gathered contiguously
+        RP = workloads.RPA
+        rseqs = workloads.ragged_paged_mix(RP["n_prefill"], RP["n_decode"], RP["seed"])
+        rq, rkp, rvp, rbt, rcu, rlens, rkc, rvc = workloads.ragged_paged_inputs(
+            rseqs, RP["Hq"], RP["Hkv"], RP["D"], RP["page_size"], RP["seed"], extra_pages=64)
+        rk = torch.cat([rkc[b, :, :L].permute(1, 0, 2) for b, (_, L) in enumerate(rseqs)])
+        rv = torch.cat([rvc[b, :, :L].permute(1, 0, 2) for b, (_, L) in enumerate(rseqs)])
+        rck = torch.zeros(len(rseqs) + 1, dtype=torch.int32)
+        rck[1:] = torch.cumsum(rlens, 0)
+        del rkc, rvc
+        max_sq = max(a for a, _ in rseqs)
+        tq = int(rcu[-1])
+        rb = [(rq.to(dev), rkp.to(dev), rvp.to(dev), rbt.to(dev), rcu.to(dev), rlens.to(dev),
+               rk.contiguous().to(dev), rv.contiguous().to(dev), rck.to(dev),
+               torch.empty(rq.shape, device=dev, dtype=torch.bfloat16),
+               torch.empty((RP["Hq"], tq), device=dev, dtype=torch.float32)) for _ in range(2)]
+        del rq, rkp, rvp, rk, rv
+
+        def rpa(i):
+            q_, kp_, vp_, bt_, cu_, ln_, _, _, _, o_, l_ = rb[i & 1]
+            mk.mk_attn_fwd_ragged_paged(q_, kp_, vp_, bt_, o_, l_, cu_, ln_, len(rseqs), RP["Hq"],
+                                        RP["Hkv"], max_sq, tq, RP["page_size"], bt_.shape[1],
+                                        kp_.shape[0], RP["D"], 1, RP["D"] ** -0.5, stream)
+
+        def rpa_gathered(i):
+            q_, _, _, _, cu_, _, k_, v_, ck_, o_, l_ = rb[i & 1]
+            mk.mk_attn_fwd_varlen(q_, k_, v_, o_, l_, cu_, ck_, len(rseqs), RP["Hq"], RP["Hkv"],
+                                  max_sq, tq, k_.shape[0], RP["D"], 1, RP["D"] ** -0.5, stream)
+        ms = time_block(stream, rpa, 5, 20)
+        ms_g = time_block(stream, rpa_gathered, 5, 20)
+        r_pairs = sum(sq * (L - sq) + sq * (sq + 1) // 2 for sq, L in rseqs)
+        r_flops = 4 * RP["D"] * RP["Hq"] * r_pairs
+        r_tf = r_flops / (ms * 1e-3) / 1e12
+        extra["ragged_paged"] = {
+            "workload": (f"{RP['name']}: {RP['n_prefill']} prefill chunks U[512,2048] after "
+                         f"U[0,4096] context keys + {RP['n_decode']} decode tokens over U[512,4096] "
+                         f"keys, {tq} query tokens, Hq={RP['Hq']} Hkv={RP['Hkv']} D={RP['D']}, "
+                         f"{RP['page_size']}-key pages in a seeded random order, causal"),
+            "value": round(r_tf, 2), "unit": "TFLOP/s", "us": round(ms * 1e3, 2),
+            "us_packed_contiguous": round(ms_g * 1e3, 2), "flops": r_flops,
+            "roofline": {"bound": "mfma", "achieved": round(r_tf, 2), "peak": PEAK_BF16_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(r_tf / PEAK_BF16_TFLOPS, 4),
+                         "traffic": None},
+        }
+        log(f"[bench] ragged paged: {ms * 1e3:.1f} us (packed contiguous {ms_g * 1e3:.1f} us)")
+        del rb
+        torch.cuda.empty_cache()
     if "paged" in legs:
         # the decode's keys scattered over pages in a seeded random order
         kp, vp, bt = workloads.paged_layout(kc, vc, args.page_size, seed=dcfg.seed + 7,

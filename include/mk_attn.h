@@ -148,8 +148,10 @@ int mk_attn_fwd_varlen(const void *q, const void *k, const void *v, void *o, flo
  *   B * max_pages must fit in 31 bits (MK_ERR_SHAPE); scale, stream as
  *   mk_attn_fwd.
  * The result is mk_attn_fwd_varlen's on the keys and values gathered from
- * the pages (bitwise the same).  Returns MK_OK or an mk_status;
- * asynchronous on `stream`.
+ * the pages, up to rounding (every tile here takes its own row maximum;
+ * the results are bitwise equal unless a tile's scaled scores rise more
+ * than 8 (log2 units) above the earlier tiles' maximum).  Returns MK_OK or
+ * an mk_status; asynchronous on `stream`.
  */
 int mk_attn_fwd_ragged_paged(const void *q, const void *k_pages, const void *v_pages,
                              const int *block_table, void *o, float *lse,

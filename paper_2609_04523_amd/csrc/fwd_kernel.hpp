@@ -62,6 +62,7 @@ struct FwdArgs {
   // ceil(log2 page_size): exact for 31-bit dividends)
   uint64_t ps_magic;
   int ps_shift;
+  int tile_in_page;  // page_size % 64 == 0: a 64-key tile lies in one page
 };
 
 // Tokens [start, end) of sequence b from cumulative offsets, clamped into
@@ -133,7 +134,8 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
   constexpr int ROW_BYTES = D * 2;
   constexpr int NK = 2 * S::KSTEPS;     // K fragment reads per tile
   constexpr int NV = 8 * S::DBLK;       // transposing V reads per tile
-  constexpr int RW = POS_SCALE ? 8 : 4;  // LDS reads in flight (fewer registers otherwise)
+  // LDS reads in flight (fewer where the registers are needed elsewhere)
+  constexpr int RW = POS_SCALE && !PAGED ? 8 : 4;
   static_assert(RW >= 2 && RW % 2 == 0 && RW <= NK && RW <= NV, "read window");
   // K tile buffers 0 and 1, then V tile buffers 0 and 1, contiguous (the
   // epilogue stages the output rows of all waves through them)
@@ -259,8 +261,9 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
   const uint32_t paged_lane_off = (uint32_t)((lane / S::CHUNKS) * ROW_BYTES + dma_ch);
   // PAGED: first row this wave reads for block p of tile kt (its own block,
   // or the sequence's last row when the block lies wholly past it)
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);  // the same in every lane
   auto block_row = [&](int kt, int p) {
-    const int r0 = kt * BN + (p * S::WAVES + wave) * S::ROWS_PER_KB;
+    const int r0 = kt * BN + (p * S::WAVES + wave_u) * S::ROWS_PER_KB;
     return r0 < L ? r0 : L - 1;
   };
   auto issue_rows = [&](const char* g, uint32_t lds_w, int kt, auto buf_tag, auto p_tag,
@@ -414,10 +417,21 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
     // is in flight (so the wait for them waits for nothing else)
     size_t pk_off[S::BLOCKS_PER_WAVE], pv_off[S::BLOCKS_PER_WAVE];
     if constexpr (PAGED) {
+      if (a.tile_in_page) {
+        // one entry per tile: a block's rows follow the tile's first row
+        const size_t k0 = (STEADY || load_k) ? page_row((t + 1) * BN) : 0;
+        const size_t v0 = (STEADY || load_v) ? page_row((t - 1) * BN) : 0;
 #pragma unroll
-      for (int p = 0; p < S::BLOCKS_PER_WAVE; ++p) {
-        pk_off[p] = (STEADY || load_k) ? page_row(block_row(t + 1, p)) : 0;
-        pv_off[p] = (STEADY || load_v) ? page_row(block_row(t - 1, p)) : 0;
+        for (int p = 0; p < S::BLOCKS_PER_WAVE; ++p) {
+          pk_off[p] = k0 + (size_t)(block_row(t + 1, p) - (t + 1) * BN) * ROW_BYTES;
+          pv_off[p] = v0 + (size_t)(block_row(t - 1, p) - (t - 1) * BN) * ROW_BYTES;
+        }
+      } else {
+#pragma unroll
+        for (int p = 0; p < S::BLOCKS_PER_WAVE; ++p) {
+          pk_off[p] = (STEADY || load_k) ? page_row(block_row(t + 1, p)) : 0;
+          pv_off[p] = (STEADY || load_v) ? page_row(block_row(t - 1, p)) : 0;
+        }
       }
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     }
@@ -682,32 +696,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
         // lie wholly inside the sequence, so their K rows can be read again
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
-          if (PAGED && __ballot(l_tile[qb] > kSumLimit)) {
-            // the tile's key rows through the block table: each 16-row half
-            // of a 32-key block lies in one page, read through a resource of
-            // its own, and a lane keeps the half its row is in
-            const uint32_t lane_off = (uint32_t)((n & 15) * ROW_BYTES + 16 * h);
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-              const __amdgpu_buffer_rsrc_t lo = __builtin_amdgcn_make_buffer_rsrc(
-                  const_cast<char*>(kg + page_row(tw * BN + 32 * kb)), 0, 16 * ROW_BYTES,
-                  0x00020000);
-              const __amdgpu_buffer_rsrc_t hi = __builtin_amdgcn_make_buffer_rsrc(
-                  const_cast<char*>(kg + page_row(tw * BN + 32 * kb + 16)), 0, 16 * ROW_BYTES,
-                  0x00020000);
-#pragma unroll
-              for (int r2 = 0; r2 < 16; ++r2) s_old[qb][kb][r2] = 0.f;
-#pragma unroll
-              for (int st = 0; st < S::KSTEPS; ++st) {
-                const u32x4 ul = __builtin_amdgcn_raw_buffer_load_b128(lo, lane_off, 32 * st, 0);
-                const u32x4 uh = __builtin_amdgcn_raw_buffer_load_b128(hi, lane_off, 32 * st, 0);
-                const u32x4 u = n < 16 ? ul : uh;
-                s_old[qb][kb] = mfma32(as_bf16x8(u), qf[qb][st], s_old[qb][kb]);
-                __builtin_amdgcn_sched_barrier(0);
-              }
-            }
-            settle_tail(qb);
-          } else if (!PAGED && __ballot(l_tile[qb] > kSumLimit)) {
+          if (__ballot(l_tile[qb] > kSumLimit)) {
             // (the base is made wave-uniform explicitly: a resource in vector
             // registers would need a loop over its distinct values)
             const uintptr_t base = (uintptr_t)(kg + (size_t)tw * BN * kv_stride);
@@ -752,9 +741,11 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
     const bool ex = t >= 1 && t <= n_live;
     const bool pv = t >= 2 && t <= n_live + 1;
     // tile t - 1 gets its maximum: the first tile, masked tiles, and every
-    // tile when the scale is not positive
+    // tile when the scale is not positive or the keys come from pages (a
+    // tile weighed against the running maximum may have to be formed again
+    // from K, which the paged path does not do)
     const bool mask = t - 1 >= n_free;
-    const bool head = !POS_SCALE || t == 1 || mask;
+    const bool head = !POS_SCALE || PAGED || t == 1 || mask;
     if (qk && ex && pv) {
       if (!head) {
         if (t + 1 < n_full)
@@ -763,6 +754,8 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
           step(t, par_tag, T1(), T1(), T1(), F0(), F0(), F0());
       } else if (mask) {
         step(t, par_tag, T1(), T1(), T1(), T1(), T1(), F0());
+      } else if (PAGED && t + 1 < n_full) {
+        step(t, par_tag, T1(), T1(), T1(), T1(), F0(), T1());
       } else {
         step(t, par_tag, T1(), T1(), T1(), T1(), F0(), F0());
       }

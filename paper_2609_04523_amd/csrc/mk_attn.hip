@@ -76,6 +76,7 @@ int fwd_impl(const void* q, const void* k, const void* v, void* o, float* lse, i
   a.page_size = a.max_pages = a.n_pages = 0;
   a.ps_magic = 0;
   a.ps_shift = 0;
+  a.tile_in_page = 0;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool pos = scale > 0.f;
   const hipError_t e = mk::launch_fwd(a, (unsigned)nblocks, D, causal, out_f32, pos, st);
@@ -254,6 +255,7 @@ int mk_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o, flo
   a.page_size = a.max_pages = a.n_pages = 0;
   a.ps_magic = 0;
   a.ps_shift = 0;
+  a.tile_in_page = 0;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool pos = scale > 0.f;
   const hipError_t e = mk::launch_fwd_varlen(a, (unsigned)nblocks, D, causal, pos, st);
@@ -318,6 +320,7 @@ int mk_attn_fwd_ragged_paged(const void* q, const void* k_pages, const void* v_p
     a.ps_shift = 31 + l;
     a.ps_magic = ((uint64_t)1 << a.ps_shift) / (uint64_t)page_size + 1;
   }
+  a.tile_in_page = page_size % 64 == 0 ? 1 : 0;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool pos = scale > 0.f;
   const hipError_t e = mk::launch_fwd_ragged_paged(a, (unsigned)nblocks, D, causal, pos, st);

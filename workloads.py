@@ -215,6 +215,27 @@ def ragged_paged_inputs(seqs, Hq: int, Hkv: int, D: int, page_size: int, seed: i
     return q, kp, vp, bt, cu, lens, kc, vc
 
 
+# The ragged paged bench batch: prefill chunks over earlier context and decode
+# tokens in one call, Hq = 32, Hkv = 8, D = 128, 64-key pages.
+RPA = dict(name="rpa_mixed_b64", n_prefill=8, n_decode=56, Hq=32, Hkv=8, D=128, page_size=64,
+           seed=1008)
+
+
+def ragged_paged_mix(n_prefill: int, n_decode: int, seed: int):
+    """Seeded (Sq, L) list of a serving step: n_prefill chunks of U{512..2048}
+    queries after U{0..4096} keys of earlier context (L = context + chunk),
+    then n_decode single tokens over U{512..4096} keys."""
+    g = _gen(seed)
+    seqs = []
+    for _ in range(n_prefill):
+        sq = int(torch.randint(512, 2049, (1,), generator=g))
+        ctx = int(torch.randint(0, 4097, (1,), generator=g))
+        seqs.append((sq, ctx + sq))
+    for _ in range(n_decode):
+        seqs.append((1, int(torch.randint(512, 4097, (1,), generator=g))))
+    return seqs
+
+
 def sample_rows(B: int, Hq: int, S: int, nrows: int, seed: int) -> torch.Tensor:
     """int32 [B,Hq,nrows] of query rows: 0 and S-1 plus nrows-2 distinct
     rows drawn from a per-(b, hq) seeded permutation."""
