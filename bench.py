@@ -410,6 +410,9 @@ def main():
     ap.add_argument("--cpu-baseline", choices=("all", "headline", "none"), default="all",
                     help="oracle timing: every workload, the headline sample only, or none")
     ap.add_argument("--page-size", type=int, default=16, help="page size of the paged leg")
+    ap.add_argument("--ws-min-seq", type=int, default=16384,
+                    help="prefill workloads with at least this many keys run through "
+                         "mk_attn_fwd_ws (0: all bf16 ones; a huge value: none)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this size (counter calibration)")
     ap.add_argument("--summarize-trace", metavar="DIR",
@@ -477,8 +480,26 @@ def main():
             out.append((q.to(dev), k.to(dev), v.to(dev), o, lse))
         return out
 
+    def prefill_entry(cfg):
+        """The entry point a workload runs through: mk_attn_fwd_ws (V^T tiles
+        written by the call, then the forward) where the copy pays for itself
+        (keys re-read by many query tiles: S >= --ws-min-seq), else mk_attn_fwd."""
+        if cfg.out_fp32:
+            return "mk_attn_fwd_o32"
+        return "mk_attn_fwd_ws" if cfg.S >= args.ws_min_seq else "mk_attn_fwd"
+
     def prefill_fn(cfg, bufs):
-        entry = mk.mk_attn_fwd_o32 if cfg.out_fp32 else mk.mk_attn_fwd
+        name = prefill_entry(cfg)
+        if name == "mk_attn_fwd_ws":
+            wsb = mk.mk_attn_fwd_workspace_bytes(cfg.B, cfg.Hkv, cfg.S, cfg.D)
+            wsp = torch.empty(wsb, device=dev, dtype=torch.uint8)
+
+            def run(i):
+                q, k, v, o, lse = bufs[i & 1]
+                mk.mk_attn_fwd_ws(q, k, v, o, lse, cfg.B, cfg.Hq, cfg.Hkv, cfg.S, cfg.S, cfg.D,
+                                  1, cfg.scale, None, wsp, wsb, stream)
+            return run
+        entry = getattr(mk, name)
 
         def run(i):
             q, k, v, o, lse = bufs[i & 1]
@@ -554,6 +575,7 @@ def main():
         return read_traffic(f"{kernel}_{cfg_name}_counters.md", digest)
 
     configs = {pcfg.name: prefill_record(pcfg, pre_ms * 1e3, traffic_of(pcfg.name))}
+    configs[pcfg.name]["entry"] = prefill_entry(pcfg)
 
     # ---- legs ----
     dec_ms = None
@@ -570,6 +592,7 @@ def main():
         bufs = prefill_inputs_on_device(cfg)
         ms = time_block(stream, prefill_fn(cfg, bufs), warm, n)
         configs[cname] = prefill_record(cfg, ms * 1e3, traffic_of(cname))
+        configs[cname]["entry"] = prefill_entry(cfg)
         log(f"[bench] {cname}: {ms * 1e3:.1f} us ({configs[cname]['tflops']} TFLOP/s)")
         del bufs
         torch.cuda.empty_cache()
@@ -782,6 +805,7 @@ def main():
         "data": "synthetic (seeded N(0,1) bf16, generated on the host, resident in HBM)",
         "config": {
             "workload": (f"{head['workload']} + fp32 LSE; then {configs[dcfg.name]['workload']}"),
+            "prefill_entry": configs[pcfg.name]["entry"],
             "prefill_flops_per_step": pcfg.flops,
             "decode_bytes_per_step": dec_bytes,
             "decode_sum_kv_len": sum_l,

@@ -83,6 +83,37 @@ int mk_attn_fwd_o32(const void *q, const void *k, const void *v, float *o, float
                     int causal, float scale, const int *kv_seqlens, void *stream);
 
 /*
+ * Same computation and result as mk_attn_fwd (bitwise: the same products
+ * in the same order), with V read through a copy that the call first
+ * writes into `workspace`: V^T in 64-key tiles laid out as the matrix
+ * cores take it, so the forward reads its V operand from LDS with plain
+ * 16-byte reads instead of transposing ones.  The copy costs one read and
+ * one write of V (4 * B * Hkv * Skv * D bytes of HBM traffic), which pays
+ * where each key tile is used by many query tiles (long causal sequences,
+ * grouped query heads).
+ *   workspace        device memory of at least
+ *                    mk_attn_fwd_workspace_bytes(B, Hkv, Skv, D) bytes,
+ *                    16-byte aligned, owned by the caller; overwritten by
+ *                    the call (calls that share it on different streams
+ *                    race)
+ *   other arguments  as mk_attn_fwd (bf16 O)
+ * Returns MK_OK or an mk_status (MK_ERR_NULL for a null workspace,
+ * MK_ERR_ARG when it is smaller than required, MK_ERR_ALIGN when it is not
+ * 16-byte aligned); asynchronous on `stream`.
+ */
+int mk_attn_fwd_ws(const void *q, const void *k, const void *v, void *o, float *lse,
+                   int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                   int causal, float scale, const int *kv_seqlens,
+                   void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Workspace bytes mk_attn_fwd_ws needs: B * Hkv * ceil(Skv / 64) * 64 * D
+ * * 2.  Returns 0 for arguments mk_attn_fwd_ws would reject as a shape
+ * (B, Hkv, Skv < 1, D not 64 or 128).
+ */
+size_t mk_attn_fwd_workspace_bytes(int B, int Hkv, int Skv, int D);
+
+/*
  * Forward over a packed batch of variable-length sequences (the ragged
  * batches of the paper's "Ragged Paged Attention" workload, Table 2): each
  * sequence is attended on its own, with the same computation as

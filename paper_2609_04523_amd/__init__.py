@@ -24,7 +24,8 @@ MK_STATUS = {0: "MK_OK", 1: "MK_ERR_NULL", 2: "MK_ERR_SHAPE", 3: "MK_ERR_UNSUPPO
              8: "MK_ERR_SCRATCH"}
 
 # every symbol include/mk_attn.h declares
-EXPORTS = ("mk_attn_fwd", "mk_attn_fwd_o32", "mk_attn_fwd_varlen", "mk_attn_fwd_ragged_paged",
+EXPORTS = ("mk_attn_fwd", "mk_attn_fwd_ws", "mk_attn_fwd_workspace_bytes", "mk_attn_fwd_o32",
+           "mk_attn_fwd_varlen", "mk_attn_fwd_ragged_paged",
            "mk_attn_decode_workspace_bytes", "mk_attn_decode", "mk_attn_decode_paged",
            "mk_attn_decode_noalloc", "mk_attn_decode_noalloc_max_bytes",
            "mk_attn_decode_default_parts", "mk_attn_bwd", "mk_attn_bwd_workspace_bytes",
@@ -53,6 +54,10 @@ def lib():
         vp, i, f, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
         h.mk_attn_fwd.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, vp, vp]
         h.mk_attn_fwd.restype = i
+        h.mk_attn_fwd_ws.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, vp, vp, sz, vp]
+        h.mk_attn_fwd_ws.restype = i
+        h.mk_attn_fwd_workspace_bytes.argtypes = [i, i, i, i]
+        h.mk_attn_fwd_workspace_bytes.restype = sz
         h.mk_attn_fwd_o32.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, vp, vp]
         h.mk_attn_fwd_o32.restype = i
         h.mk_attn_fwd_varlen.argtypes = [vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, i, f, vp]
@@ -106,6 +111,10 @@ def mk_attn_decode_workspace_bytes(Hq: int, Hkv: int, D: int, n_parts: int = 0) 
     return lib().mk_attn_decode_workspace_bytes(Hq, Hkv, D, n_parts)
 
 
+def mk_attn_fwd_workspace_bytes(B: int, Hkv: int, Skv: int, D: int) -> int:
+    return int(lib().mk_attn_fwd_workspace_bytes(B, Hkv, Skv, D))
+
+
 def mk_attn_bwd_workspace_bytes(B: int, Hq: int, Sq: int) -> int:
     return int(lib().mk_attn_bwd_workspace_bytes(B, Hq, Sq))
 
@@ -142,6 +151,13 @@ def mk_attn_fwd(q, k, v, o, lse, B, Hq, Hkv, Sq, Skv, D, causal, scale, kv_seqle
     _check(lib().mk_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, Hq, Hkv, Sq,
                              Skv, D, int(causal), float(scale), _ptr(kv_seqlens),
                              _stream(stream)))
+
+
+def mk_attn_fwd_ws(q, k, v, o, lse, B, Hq, Hkv, Sq, Skv, D, causal, scale, kv_seqlens,
+                   workspace, workspace_bytes, stream=None):
+    _check(lib().mk_attn_fwd_ws(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, Hq, Hkv, Sq,
+                                Skv, D, int(causal), float(scale), _ptr(kv_seqlens),
+                                _ptr(workspace), int(workspace_bytes), _stream(stream)))
 
 
 def mk_attn_fwd_o32(q, k, v, o, lse, B, Hq, Hkv, Sq, Skv, D, causal, scale, kv_seqlens=None,
@@ -223,8 +239,11 @@ def _require(t, name, dtype, ndim):
 
 
 def fwd(q, k, v, *, causal: bool = True, scale: float | None = None, kv_seqlens=None,
-        out_fp32: bool = False, with_lse: bool = True, stream=None):
-    """q [B,Hq,Sq,D], k/v [B,Hkv,Skv,D] bf16 -> (o [B,Hq,Sq,D], lse [B,Hq,Sq] or None)."""
+        out_fp32: bool = False, with_lse: bool = True, workspace=None, stream=None):
+    """q [B,Hq,Sq,D], k/v [B,Hkv,Skv,D] bf16 -> (o [B,Hq,Sq,D], lse [B,Hq,Sq] or None).
+    With a workspace (a uint8 tensor of at least mk_attn_fwd_workspace_bytes)
+    the bf16 forward goes through mk_attn_fwd_ws (V^T tiles in the
+    workspace; the same result)."""
     import torch
     _require(q, "q", torch.bfloat16, 4)
     _require(k, "k", torch.bfloat16, 4)
@@ -238,6 +257,12 @@ def fwd(q, k, v, *, causal: bool = True, scale: float | None = None, kv_seqlens=
     o = torch.empty((B, Hq, Sq, D), device=q.device,
                     dtype=torch.float32 if out_fp32 else torch.bfloat16)
     lse = torch.empty((B, Hq, Sq), device=q.device, dtype=torch.float32) if with_lse else None
+    if workspace is not None:
+        if out_fp32:
+            raise ValueError("the workspace forward writes bf16 O")
+        mk_attn_fwd_ws(q, k, v, o, lse, B, Hq, Hkv, Sq, Skv, D, causal, scale, kv_seqlens,
+                       workspace, workspace.numel() * workspace.element_size(), stream)
+        return o, lse
     entry = mk_attn_fwd_o32 if out_fp32 else mk_attn_fwd
     entry(q, k, v, o, lse, B, Hq, Hkv, Sq, Skv, D, causal, scale, kv_seqlens, stream)
     return o, lse

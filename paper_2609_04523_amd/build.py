@@ -11,7 +11,7 @@ LIB = os.path.join(PKG, "libmk_attn.so")
 # one translation unit per kernel family, compiled in parallel, then linked
 SOURCES = [os.path.join(CSRC, f) for f in
            ("mk_attn.hip", "fwd_launch_d128.hip", "fwd_launch_d64.hip",
-            "fwd_varlen_launch.hip", "fwd_rpa_launch.hip", "dec_launch.hip", "bwd_launch.hip",
+            "fwd_varlen_launch.hip", "fwd_rpa_launch.hip", "fwd_vt_launch.hip", "dec_launch.hip", "bwd_launch.hip",
             "mla_launch.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

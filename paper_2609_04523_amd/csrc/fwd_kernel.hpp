@@ -14,7 +14,10 @@
 // reductions are in-lane plus one exchange with lane l^32.  The output is
 // O^T = V^T P^T: P^T is the score accumulator converted to bf16 in place
 // (its key order is the accumulator's own row order), and the V^T operand
-// is read from the row-major V tile with the transposing LDS read.
+// is read from the row-major V tile with the transposing LDS read -- or,
+// with VT, from a copy of V that a pre-pass wrote tile by tile in the
+// operand's own layout, with plain 16-byte LDS reads (which the LDS serves
+// at twice the rate of the transposing ones).
 //
 // Softmax bookkeeping (exp2 domain, c = scale * log2 e):
 //   m    running row maximum of c*s, raised only when a tile's maximum
@@ -63,6 +66,10 @@ struct FwdArgs {
   uint64_t ps_magic;
   int ps_shift;
   int tile_in_page;  // page_size % 64 == 0: a 64-key tile lies in one page
+  // VT only: the V^T tiles of vt_pack_kernel, [B, Hkv, vt_tiles, 4, D, 16]
+  // bf16 (vt_tiles = ceil(Skv / 64))
+  const uint16_t* vt;
+  int vt_tiles;
 };
 
 // Tokens [start, end) of sequence b from cumulative offsets, clamped into
@@ -123,19 +130,25 @@ __device__ __forceinline__ void fwd_map_block(int bid, const FwdArgs& a, int& qt
 // or 8 (D = 64) consecutive key rows, which lie in one page since pages
 // hold a multiple of 16 keys, so the page of every block is one table
 // entry, read through the scalar cache at the start of the step.
+// VT (dense batches only): the V tiles come from the pre-pass's V^T tiles
+// (contiguous 64-key blocks of D * 128 bytes, copied to LDS as they are) and
+// the products read them with ds_read_b128.
 template <int D, bool CAUSAL, bool OUT_F32, int QB, bool POS_SCALE, bool VARLEN, int WAVES,
-          bool PAGED = false>
+          bool PAGED = false, bool VT = false>
 __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
   static_assert(VARLEN || !PAGED, "the paged cache is read by the packed forward");
+  static_assert(!(VT && VARLEN), "the V^T copy is made for dense batches");
   using S = FwdShape<D, QB, WAVES>;
   constexpr int BN = S::BN;
   constexpr int TILE = BN * D;            // bf16 per tile per tensor
   constexpr int TILE_BYTES = TILE * 2;
   constexpr int ROW_BYTES = D * 2;
   constexpr int NK = 2 * S::KSTEPS;     // K fragment reads per tile
-  constexpr int NV = 8 * S::DBLK;       // transposing V reads per tile
-  // LDS reads in flight (fewer where the registers are needed elsewhere)
-  constexpr int RW = POS_SCALE && !PAGED ? 8 : 4;
+  constexpr int RPP = VT ? 1 : 2;       // LDS reads per V^T operand
+  constexpr int NV = 4 * RPP * S::DBLK;  // V reads per tile
+  // LDS reads in flight (fewer where the registers are needed elsewhere;
+  // the V^T path's 16-byte V reads need half as many for the same bytes)
+  constexpr int RW = POS_SCALE && !PAGED && !VT ? 8 : 4;
   static_assert(RW >= 2 && RW % 2 == 0 && RW <= NK && RW <= NV, "read window");
   // K tile buffers 0 and 1, then V tile buffers 0 and 1, contiguous (the
   // epilogue stages the output rows of all waves through them)
@@ -197,7 +210,8 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
     if (lse_base) lse_base += q_row0;
     const size_t kv_off = ((size_t)b * a.Hkv + g) * (size_t)a.Skv * D;
     kg = reinterpret_cast<const char*>(a.k + kv_off);
-    vg = reinterpret_cast<const char*>(a.v + kv_off);
+    vg = reinterpret_cast<const char*>(
+        VT ? a.vt + ((size_t)b * a.Hkv + g) * a.vt_tiles * (size_t)TILE : a.v + kv_off);
   }
   q_base = a.q + o_base;
   const int off = L - Sq;  // bottom-right causal alignment
@@ -300,6 +314,18 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
     }
   };
 
+  // VT: block p (1 KB at byte 1024 (4 p + wave)) of V^T tile kt into V
+  // buffer BUF: the tile is contiguous and padded in the copy, so the
+  // block is a plain 1 KB copy with no clamping.
+  auto issue_vt = [&](int kt, auto buf_tag, auto p_tag) {
+    constexpr int BUF = decltype(buf_tag)::value;
+    constexpr int P = decltype(p_tag)::value;
+    constexpr uint32_t lds_off = BUF * TILE_BYTES + P * S::WAVES * 1024;
+    const char* tile = vg + (size_t)__builtin_amdgcn_readfirstlane(kt) * TILE_BYTES;
+    load_lds16_buf(tile, TILE_BYTES, (uint32_t)(wave * 1024 + lane * 16), v_lds_w + lds_off,
+                   (uint32_t)(P * S::WAVES * 1024));
+  };
+
   float m_run[QB], l_run[QB];
   f32x16 o_acc[QB][S::DBLK];
 #pragma unroll
@@ -328,8 +354,13 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
 #pragma unroll
   for (int s = 0; s < S::KSTEPS; ++s)
     k_addr[s] = lds_addr(&k_lds[0][0]) + n * ROW_BYTES + (((2 * s + h) ^ fwd_swz<D>(n)) << 4);
+  // VT: a V^T tile is [4 key chunks][D head dims][16 keys]; the operand of
+  // key chunk kc and head dims 32 db + n is the 16-byte half h ^ ((n / 8) % 2)
+  // of row (kc, 32 db + n) (the halves of rows 8..15 of every 16 swapped, so
+  // 16 lanes of one k-group hit 64 distinct banks).
+  const uint32_t vt_addr = lds_addr(&v_lds[0][0]) + n * 32 + ((h ^ ((n >> 3) & 1)) << 4);
   uint32_t v_addr[S::DBLK][2];
-  {
+  if constexpr (!VT) {
     const int tr_i = lane & 15;
     const int tr_row = 4 * h + (tr_i >> 2);
     const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (tr_i & 3);
@@ -440,23 +471,31 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
       constexpr int P_ = decltype(p_tag)::value;
       if (STEADY || load_k)
         issue_rows(kg, k_lds_w, t + 1, NB_(), p_tag, steady_tag, PAGED ? pk_off[P_] : 0);
-      if (STEADY || load_v)
-        issue_rows(vg, v_lds_w, t - 1, NB_(), p_tag, steady_tag, PAGED ? pv_off[P_] : 0);
+      if constexpr (VT) {
+        if (STEADY || load_v) issue_vt(t - 1, NB_(), p_tag);
+      } else {
+        if (STEADY || load_v)
+          issue_rows(vg, v_lds_w, t - 1, NB_(), p_tag, steady_tag, PAGED ? pv_off[P_] : 0);
+      }
     };
 
-    // ---- LDS read stream: the NV transposing V reads of tile t - 2 in the
-    // order the products consume them, then the NK K fragments of tile t
-    // (key block kb, then step s).  RS reads are kept in flight: consuming
-    // one issues the next. ----
+    // ---- LDS read stream: the NV V reads of tile t - 2 in the order the
+    // products consume them (RPP per product), then the NK K fragments of
+    // tile t (key block kb, then step s).  RS reads are kept in flight:
+    // consuming one issues the next. ----
     constexpr int NVS = PV ? NV : 0;
     constexpr int NKS = QK ? NK : 0;
     constexpr int TOT = NVS + NKS;
     constexpr int RS = RW < TOT ? RW : TOT;
-    u32x2 vr[NV];
+    std::conditional_t<VT, u32x4, u32x2> vr[NV];
     u32x4 kr[NK];
     auto issue_read = [&](auto j_tag) {
       constexpr int J = decltype(j_tag)::value;
-      if constexpr (J < NVS) {
+      if constexpr (J < NVS && VT) {
+        // product J: key chunk J / DBLK, head dims 32 (J % DBLK) ..
+        constexpr int OFF = PAR * TILE_BYTES + (J / S::DBLK) * D * 32 + (J % S::DBLK) * 32 * 32;
+        vr[J] = lds_read_b128_async_off<OFF>(vt_addr);
+      } else if constexpr (J < NVS) {
         constexpr int OFF = PAR * TILE_BYTES + (J / (2 * S::DBLK)) * 16 * ROW_BYTES;
         vr[J] = lds_read_tr16_async_off<OFF>(v_addr[(J / 2) % S::DBLK][J % 2]);
       } else if constexpr (J < TOT) {
@@ -520,8 +559,18 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
           if (MASK) {
             const int qrow = qw0 + qb * 32 + n;
             const int lim = min(L - 1, CAUSAL ? qrow + off : L - 1);  // last admissible key
-            const int key = tw * BN + KB * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-            if (key > lim) s_old[qb][KB][r] = kNegInf;
+            // The lane's key tw BN + 4 h + o, o = 32 KB + 8 (r / 4) + r % 4.
+            // Two spellings of the same test: comparing o (an inline
+            // constant) with lim - tw BN - 4 h keeps no per-register key
+            // offsets, which the register allocator needs on the VT path
+            // and does worse with on the other.
+            if constexpr (VT) {
+              if (KB * 32 + 8 * (r >> 2) + (r & 3) > lim - tw * BN - 4 * h)
+                s_old[qb][KB][r] = kNegInf;
+            } else {
+              const int key = tw * BN + KB * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+              if (key > lim) s_old[qb][KB][r] = kNegInf;
+            }
           }
         }
         float& mx = KB == 0 ? mx0[qb] : mx1[qb];
@@ -551,23 +600,31 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
     // weights of tile t - 1 in between ----
     constexpr bool LOADS_A = PV;  // the loads go out during the first products
     if constexpr (PV) {
-      constexpr int NP = NV / 2;  // products: (kc, db) = (m / DBLK, m % DBLK)
+      constexpr int NP = NV / RPP;  // products: (kc, db) = (m / DBLK, m % DBLK)
       static_assert(NP == 16 || NP == 8, "products per phase");
       constexpr int PER_LOAD = NP / S::BLOCKS_PER_WAVE;
       static_for<0, NP>([&](auto m_tag) {
         constexpr int M = decltype(m_tag)::value;
-        constexpr int AHEAD = (RS < TOT - 2 * M ? RS : TOT - 2 * M) - 2;  // reads after 2M+1
+        // reads still in flight once those of product M are in
+        constexpr int AHEAD = (RS < TOT - RPP * M ? RS : TOT - RPP * M) - RPP;
         lds_wait_lgkm<AHEAD>();
-        lds_ready(vr[2 * M]);
-        lds_ready(vr[2 * M + 1]);
-        const u32x4 w = {vr[2 * M][0], vr[2 * M][1], vr[2 * M + 1][0], vr[2 * M + 1][1]};
-        const bf16x8 vf = as_bf16x8(w);
+        bf16x8 vf;
+        if constexpr (VT) {
+          lds_ready(vr[M]);
+          vf = as_bf16x8(vr[M]);
+        } else {
+          lds_ready(vr[2 * M]);
+          lds_ready(vr[2 * M + 1]);
+          const u32x4 w = {vr[2 * M][0], vr[2 * M][1], vr[2 * M + 1][0], vr[2 * M + 1][1]};
+          vf = as_bf16x8(w);
+        }
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb)
           o_acc[qb][M % S::DBLK] =
               mfma32(vf, as_bf16x8(p_old[qb][M / S::DBLK]), o_acc[qb][M % S::DBLK]);
-        issue_read(std::integral_constant<int, 2 * M + RS>());
-        issue_read(std::integral_constant<int, 2 * M + 1 + RS>());
+        static_for<0, RPP>([&](auto i_tag) {
+          issue_read(std::integral_constant<int, RPP * M + decltype(i_tag)::value + RS>());
+        });
         if constexpr (M % PER_LOAD == 0) load_block(std::integral_constant<int, M / PER_LOAD>());
         if constexpr (EX) {
           if constexpr (HEAD) {

@@ -1,6 +1,6 @@
 // launch.hpp -- host launchers of the kernel families, each in translation
 // units of its own (fwd_launch_d128.hip, fwd_launch_d64.hip,
-// fwd_varlen_launch.hip, dec_launch.hip, bwd_launch.hip, mla_launch.hip) so that the library compiles in
+// fwd_varlen_launch.hip, fwd_vt_launch.hip, dec_launch.hip, bwd_launch.hip, mla_launch.hip) so that the library compiles in
 // parallel.  Arguments are validated by the callers in mk_attn.hip; these
 // only pick the instantiation and enqueue.
 #pragma once
@@ -19,6 +19,12 @@ constexpr int kFwdWaves = 4;  // waves per forward workgroup (128 query rows)
 // Dense [B, H, S, D] forward: nblocks workgroups of the forward kernel.
 hipError_t launch_fwd(const FwdArgs& a, unsigned nblocks, int D, bool causal, bool out_f32,
                       bool pos_scale, hipStream_t st);
+
+// Dense forward through a V^T copy (bf16 O): the pack kernel writes
+// a.vt (pack_blocks = B * Hkv * vt_tiles workgroups), then the forward
+// reads V from it.
+hipError_t launch_fwd_vt(const FwdArgs& a, unsigned nblocks, int D, bool causal, bool pos_scale,
+                         unsigned pack_blocks, hipStream_t st);
 
 // Packed ragged forward (bf16 O).
 hipError_t launch_fwd_varlen(const FwdArgs& a, unsigned nblocks, int D, bool causal,

@@ -15,7 +15,7 @@
 
 namespace {
 
-constexpr int kVersion = 8;
+constexpr int kVersion = 9;
 constexpr int kComputeUnits = 256;    // MI355X
 constexpr int kLdsPerCu = 160 * 1024; // gfx950
 constexpr int kMaxParts = 1 << 20;    // decode parts per call
@@ -37,9 +37,16 @@ bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// V^T tiles of mk_attn_fwd_ws: ceil(Skv / 64) tiles of 64 * D bf16 per (b, kv head)
+size_t fwd_vt_bytes(int B, int Hkv, int Skv, int D) {
+  if (B < 1 || Hkv < 1 || Skv < 1 || (D != 64 && D != 128)) return 0;
+  return (size_t)B * Hkv * (size_t)((Skv + 63) / 64) * 64 * D * 2;
+}
+
+// vt: V^T workspace of mk_attn_fwd_ws (bf16 O), or null for the transposing path
 int fwd_impl(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq,
              int Hkv, int Sq, int Skv, int D, int causal, float scale, const int* kv_seqlens,
-             void* stream, bool out_f32) {
+             void* stream, bool out_f32, void* vt = nullptr) {
   if (!q || !k || !v || !o) return MK_ERR_NULL;
   if (B < 1 || Hq < 1 || Hkv < 1 || Sq < 1 || Skv < 1 || D < 1) return MK_ERR_SHAPE;
   if (Hq % Hkv != 0) return MK_ERR_SHAPE;
@@ -77,8 +84,17 @@ int fwd_impl(const void* q, const void* k, const void* v, void* o, float* lse, i
   a.ps_magic = 0;
   a.ps_shift = 0;
   a.tile_in_page = 0;
+  a.vt = static_cast<const uint16_t*>(vt);
+  a.vt_tiles = (Skv + 63) / 64;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool pos = scale > 0.f;
+  if (vt) {
+    const long long pack_blocks = (long long)B * Hkv * a.vt_tiles;
+    if (pack_blocks > 0x7fffffffLL) return MK_ERR_SHAPE;
+    const hipError_t e = mk::launch_fwd_vt(a, (unsigned)nblocks, D, causal, pos,
+                                           (unsigned)pack_blocks, st);
+    return e == hipSuccess ? MK_OK : MK_ERR_HIP;
+  }
   const hipError_t e = mk::launch_fwd(a, (unsigned)nblocks, D, causal, out_f32, pos, st);
   return e == hipSuccess ? MK_OK : MK_ERR_HIP;
 }
@@ -202,6 +218,22 @@ int mk_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse
                   false);
 }
 
+int mk_attn_fwd_ws(const void* q, const void* k, const void* v, void* o, float* lse, int B,
+                   int Hq, int Hkv, int Sq, int Skv, int D, int causal, float scale,
+                   const int* kv_seqlens, void* workspace, size_t workspace_bytes,
+                   void* stream) {
+  if (!workspace) return MK_ERR_NULL;
+  if (!aligned(workspace, 16)) return MK_ERR_ALIGN;
+  const size_t need = fwd_vt_bytes(B, Hkv, Skv, D);
+  if (need != 0 && workspace_bytes < need) return MK_ERR_ARG;
+  return fwd_impl(q, k, v, o, lse, B, Hq, Hkv, Sq, Skv, D, causal, scale, kv_seqlens, stream,
+                  false, workspace);
+}
+
+size_t mk_attn_fwd_workspace_bytes(int B, int Hkv, int Skv, int D) {
+  return fwd_vt_bytes(B, Hkv, Skv, D);
+}
+
 int mk_attn_fwd_o32(const void* q, const void* k, const void* v, float* o, float* lse, int B,
                     int Hq, int Hkv, int Sq, int Skv, int D, int causal, float scale,
                     const int* kv_seqlens, void* stream) {
@@ -256,6 +288,8 @@ int mk_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o, flo
   a.ps_magic = 0;
   a.ps_shift = 0;
   a.tile_in_page = 0;
+  a.vt = nullptr;
+  a.vt_tiles = 0;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool pos = scale > 0.f;
   const hipError_t e = mk::launch_fwd_varlen(a, (unsigned)nblocks, D, causal, pos, st);
@@ -321,6 +355,8 @@ int mk_attn_fwd_ragged_paged(const void* q, const void* k_pages, const void* v_p
     a.ps_magic = ((uint64_t)1 << a.ps_shift) / (uint64_t)page_size + 1;
   }
   a.tile_in_page = page_size % 64 == 0 ? 1 : 0;
+  a.vt = nullptr;
+  a.vt_tiles = 0;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool pos = scale > 0.f;
   const hipError_t e = mk::launch_fwd_ragged_paged(a, (unsigned)nblocks, D, causal, pos, st);

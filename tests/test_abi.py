@@ -43,7 +43,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert mk.mk_attn_version() == 8
+    assert mk.mk_attn_version() == 9
     names = ["MK_OK", "MK_ERR_NULL", "MK_ERR_SHAPE", "MK_ERR_UNSUPPORTED", "MK_ERR_ALIGN",
              "MK_ERR_WORKSPACE", "MK_ERR_HIP", "MK_ERR_ARG", "MK_ERR_SCRATCH"]
     for code, name in enumerate(names):
@@ -81,6 +81,42 @@ def test_fwd_validation(lib, o32):
         assert r(scale=s) == 7
     # too many workgroups for one launch
     assert r(B=65536, Hq=65536, Hkv=1, Sq=1) == 2
+
+
+def fwd_ws_rc(lib, *, q=P, k=P, v=P, o=P, lse=None, B=1, Hq=2, Hkv=1, Sq=8, Skv=8, D=128,
+              causal=1, scale=0.125, seqlens=None, ws=P, ws_bytes=1 << 30):
+    return lib.mk_attn_fwd_ws(q, k, v, o, lse, B, Hq, Hkv, Sq, Skv, D, causal, scale, seqlens, ws,
+                              ws_bytes, None)
+
+
+def test_fwd_ws_workspace_bytes(lib):
+    # B * Hkv * ceil(Skv / 64) tiles of 64 keys x D bf16
+    assert mk.mk_attn_fwd_workspace_bytes(1, 8, 32768, 128) == 8 * 512 * 64 * 128 * 2
+    assert mk.mk_attn_fwd_workspace_bytes(2, 3, 65, 64) == 2 * 3 * 2 * 64 * 64 * 2
+    assert mk.mk_attn_fwd_workspace_bytes(4, 16, 1, 128) == 4 * 16 * 64 * 128 * 2
+    for args in ((0, 1, 8, 128), (1, 0, 8, 128), (1, 1, 0, 128), (1, 1, 8, 96), (1, 1, 8, 0)):
+        assert mk.mk_attn_fwd_workspace_bytes(*args) == 0
+
+
+def test_fwd_ws_validation(lib):
+    r = lambda **kw: fwd_ws_rc(lib, **kw)
+    assert r(ws=None) == 1
+    assert r(ws=P + 8) == 4
+    need = mk.mk_attn_fwd_workspace_bytes(1, 1, 8, 128)
+    assert r(ws_bytes=need - 1) == 7
+    assert r(ws_bytes=0) == 7
+    # everything mk_attn_fwd rejects, with a large enough workspace
+    for name in ("q", "k", "v", "o"):
+        assert r(**{name: None}) == 1
+        assert r(**{name: P_ODD}) == 4
+    for name in ("B", "Hq", "Hkv", "Sq", "Skv"):
+        assert r(**{name: 0}) == 2
+    assert r(Hq=3, Hkv=2) == 2
+    assert r(D=96) == 3
+    assert r(causal=2) == 7
+    assert r(scale=math.nan) == 7
+    assert r(lse=P + 2) == 4
+    assert r(seqlens=P + 1) == 4
 
 
 def varlen_rc(lib, *, q=P, k=P, v=P, o=P, lse=None, cq=P, ck=P, B=3, Hq=8, Hkv=2, max_sq=100,
