@@ -117,6 +117,17 @@ __device__ __forceinline__ void load_lds16_buf(const char* base, uint32_t bytes,
       rs, (__attribute__((address_space(3))) void*)(uintptr_t)lds_addr, 16, voff, soff, 0, 0);
 }
 
+// Workgroup barrier without the memory fence of __syncthreads() (which
+// waits for every load of the wave, LDS-DMA loads of later stages
+// included).  For callers that have already waited for what other waves
+// will read -- their own LDS-DMA loads by vmcnt, their LDS reads by lgkmcnt
+// -- so that loads issued for later stages stay in flight across it.
+__device__ __forceinline__ void barrier_no_fence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // s_waitcnt vmcnt(N): wait until at most N vector-memory operations of this
 // wave are outstanding (expcnt and lgkmcnt untouched).
 template <int N>

@@ -161,10 +161,11 @@ __global__ __launch_bounds__(256, 1) void mla_part_kernel(DecArgs a) {
     }
   };
 
-  // One stage.  The LDS reads form one stream -- the 36 K fragments (key
-  // block kb, step s), then the 16 transposing V reads (block d, low /
-  // high keys) -- kept RW reads ahead of their use and waited for by count,
-  // so the V reads are in flight during the softmax.
+  // One stage.  The LDS reads form one stream -- the 36 K fragments (step
+  // s, then key block kb, so the two blocks' accumulation chains
+  // interleave), then the 16 transposing V reads (block d, low / high
+  // keys) -- kept RW reads ahead of their use and waited for by count, so
+  // the V reads are in flight during the softmax.
   constexpr int NK = 2 * S::KSTEPS, NV = 2 * S::DBLK_W, TOT = NK + NV, RW = 8;
   auto consume = [&](const DecCursor& cc, uint32_t slot) {
     const int key0 = cc.t * S::BN;
@@ -175,7 +176,7 @@ __global__ __launch_bounds__(256, 1) void mla_part_kernel(DecArgs a) {
     auto issue_read = [&](auto j_tag) {
       constexpr int J = decltype(j_tag)::value;
       if constexpr (J < NK) {
-        constexpr int KB = J / S::KSTEPS, ST = J % S::KSTEPS;
+        constexpr int KB = J % 2, ST = J / 2;
         kr[J] = lds_read_b128_async_off<128 * (ST / 2)>(KB == 0 ? kb0[ST % 2] : kb1[ST % 2]);
       } else if constexpr (J < TOT) {
         constexpr int V = J - NK, D = V / 2, HH = V % 2;
@@ -194,7 +195,7 @@ __global__ __launch_bounds__(256, 1) void mla_part_kernel(DecArgs a) {
       constexpr int AHEAD = (I + RW < TOT ? I + RW : TOT) - I - 1;
       lds_wait_lgkm<AHEAD>();
       lds_ready(kr[I]);
-      sacc[I / S::KSTEPS] = mfma16(as_bf16x8(kr[I]), qf[I % S::KSTEPS], sacc[I / S::KSTEPS]);
+      sacc[I % 2] = mfma16(as_bf16x8(kr[I]), qf[I / 2], sacc[I % 2]);
       issue_read(std::integral_constant<int, I + RW>());
     });
     // online softmax over the keys of head c16 (every wave the same)
@@ -283,29 +284,32 @@ __global__ __launch_bounds__(256, 1) void mla_part_kernel(DecArgs a) {
       for (int r = 0; r < 4; ++r) o_acc[db][r] = 0.f;
   };
 
-  // ---- pipeline.  Stage j sits in slot j % 3; piece k's Q rows in Q
-  // buffer k % 2, loaded with the piece's first stage.  Iteration j waits
-  // for stage j (only stage j + 1 may still be loading); after a barrier
-  // (every wave is done with stage j - 1, whose slot takes stage j + 2) the
-  // waves copy a new piece's Q rows to registers; after a second barrier
-  // (every wave has copied them, so the other Q buffer, which held piece
-  // k - 1's predecessor, is free) stage j + 2 is issued; then stage j is
-  // consumed while j + 1 and j + 2 load. ----
+  // ---- pipeline.  Stage j sits in slot j % 3, piece k's Q rows in Q
+  // buffer k % 2.  Iteration j first issues stage j + 2 into the slot of
+  // stage j - 1 (every wave left it at the barrier that ended iteration
+  // j - 1), so three stages are in flight while the wave waits for stage j;
+  // after a barrier (every wave's part of stage j has landed) a new piece's
+  // Q rows are copied to registers and stage j is consumed; a barrier then
+  // marks slot j % 3 and the Q copy done, and the Q rows of the piece that
+  // stage j + 2 starts, if any, go out into the Q buffer of two pieces back.
+  // Issue order: Q(0), DMA(0), DMA(1), Q(1), then per iteration DMA(j + 2),
+  // Q(j + 2): the loads after stage j's (and its Q's) are DMA(j + 1),
+  // Q(j + 1) and DMA(j + 2). ----
   constexpr int LKV = S::KV_PER_WAVE, LQ = S::Q_PER_WAVE;
+  auto starts_piece = [](const DecCursor& c) { return c.t == 0; };
   DecCursor iss = cur;  // cursor of the last issued stage
   int iss_piece = 0;    // piece index of the last issued stage
-  bool nxt_new = false; // stage j + 1 starts a piece (so it loads Q rows)
   issue_q(cur.b, q_lds0);
   issue_stage(iss, slot_addr(0));
+  bool q1 = false;  // stage j + 1 brought Q rows
   if (n_stages > 1) {
-    const bool new_pair = iss.t + 1 == iss.nt;
     dec_advance(iss, a);
-    if (new_pair) {
+    issue_stage(iss, slot_addr(1));
+    if (starts_piece(iss)) {
       ++iss_piece;
       issue_q(iss.b, q_lds0 + (uint32_t)(iss_piece & 1) * S::Q_BYTES);
+      q1 = true;
     }
-    issue_stage(iss, slot_addr(1));
-    nxt_new = new_pair;
   }
   bool piece_from_pair_start = cur.t == 0;
   bool first_piece = true;
@@ -313,29 +317,24 @@ __global__ __launch_bounds__(256, 1) void mla_part_kernel(DecArgs a) {
   int slot_c = 0;
   bool new_piece = true;  // stage j starts a piece
   for (int j = 0; j < n_stages; ++j) {
-    if (j + 1 < n_stages) {
-      if (nxt_new)
+    const bool more2 = j + 2 < n_stages;
+    if (more2) {
+      dec_advance(iss, a);
+      issue_stage(iss, slot_addr(slot_c == 0 ? 2 : slot_c - 1));
+      if (q1)
+        wait_vmcnt<2 * LKV + LQ>();
+      else
+        wait_vmcnt<2 * LKV>();
+    } else if (j + 1 < n_stages) {
+      if (q1)
         wait_vmcnt<LKV + LQ>();
       else
         wait_vmcnt<LKV>();
     } else {
       wait_vmcnt<0>();
     }
-    __syncthreads();
+    barrier_no_fence();
     if (new_piece) load_q(q_lds0 + (uint32_t)(piece & 1) * S::Q_BYTES);
-    __syncthreads();
-    // issue stage j + 2 into the slot stage j - 1 used
-    bool issued_new = false;
-    if (j + 2 < n_stages) {
-      const bool new_pair = iss.t + 1 == iss.nt;
-      dec_advance(iss, a);
-      if (new_pair) {
-        ++iss_piece;
-        issue_q(iss.b, q_lds0 + (uint32_t)(iss_piece & 1) * S::Q_BYTES);
-      }
-      issue_stage(iss, slot_addr(slot_c == 0 ? 2 : slot_c - 1));
-      issued_new = new_pair;
-    }
     consume(cur, slot_addr(slot_c));
     const bool pair_end = cur.t + 1 == cur.nt;
     if (pair_end || j + 1 == n_stages) {
@@ -343,10 +342,20 @@ __global__ __launch_bounds__(256, 1) void mla_part_kernel(DecArgs a) {
       first_piece = false;
       piece_from_pair_start = true;
     }
+    lds_wait_lgkm<0>();
+    barrier_no_fence();
+    // Q rows of the piece stage j + 2 starts, into the buffer of piece
+    // iss_piece - 2, whose rows every wave copied before the barrier
+    bool q2 = false;
+    if (more2 && starts_piece(iss)) {
+      ++iss_piece;
+      issue_q(iss.b, q_lds0 + (uint32_t)(iss_piece & 1) * S::Q_BYTES);
+      q2 = true;
+    }
     slot_c = slot_c == 2 ? 0 : slot_c + 1;
-    new_piece = nxt_new;
-    nxt_new = issued_new;
+    new_piece = j + 1 < n_stages && pair_end;
     if (pair_end) ++piece;
+    q1 = q2;
     if (j + 1 < n_stages) dec_advance(cur, a);
   }
 }
