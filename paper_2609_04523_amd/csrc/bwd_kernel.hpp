@@ -533,6 +533,11 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdArgs a) {
           sacc[AC][0] = mfma32(as_bf16x8(ar[I]), kf[I / 2], sacc[AC][0]);  // S
         else
           sacc[AC][1] = mfma32(as_bf16x8(ar[I]), vf[I / 2], sacc[AC][1]);  // dP
+        // The product's result passes through an empty volatile statement,
+        // which keeps the product in this group: otherwise the compiler
+        // sinks all of A's products below B's vector work, and the two no
+        // longer overlap.
+        asm volatile("" : "+a"(sacc[AC][I % 2]));
         issue(std::integral_constant<int, I + RS>());
         static_for<0, EPM>([&](auto e_tag) {
           b_elem(std::integral_constant<int, I * EPM + decltype(e_tag)::value>());
