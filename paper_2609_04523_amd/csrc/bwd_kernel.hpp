@@ -236,40 +236,54 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
       }
     };
     static_for<0, RW>(issue);
-    // S^T = K Q^T and dP^T = V dO^T for the tile's two 32-key blocks
+    // S^T = K Q^T and dP^T = V dO^T for the tile's two 32-key blocks, then
+    // dQ^T += K^T dS^T over its four 16-key chunks.  The elements of dS^T =
+    // P^T (dP^T - D) (bf16; chunk kc = rows 8 (kc % 2) .. +7 of key block
+    // kc / 2) of key block 0 are formed beside the products of key block 1,
+    // those of key block 1 beside the dQ^T products of chunks 0 and 1, so
+    // the vector work runs under the matrix work.  Each product's result
+    // passes through an empty volatile statement, which keeps the product
+    // in its scheduling group (the compiler would otherwise gather the
+    // products into one block).
     f32x16 st[2], dpt[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) st[kb][r] = dpt[kb][r] = 0.f;
+    float e[4][8];
+    bf16x8 dsf[4];
+    auto elem = [&](auto i_tag) {  // element I: chunk I / 8, its row I % 8
+      constexpr int I = decltype(i_tag)::value;
+      constexpr int KC = I / 8, J = I % 8, R = 8 * (KC % 2) + J;
+      const int key = key0 + (KC / 2) * 32 + 8 * (R >> 2) + 4 * h + (R & 3);
+      const float p = bwd_prob(st[KC / 2][R], c, lse2, key <= lim);
+      e[KC][J] = p * (dpt[KC / 2][R] - dl);
+      if constexpr (J == 7)
+        dsf[KC] = to_bf16x8(e[KC][0], e[KC][1], e[KC][2], e[KC][3], e[KC][4], e[KC][5],
+                            e[KC][6], e[KC][7]);
+    };
+    constexpr int EPA = 32 / NA;  // elements of key block 0 per product of key block 1
     static_for<0, NA>([&](auto i_tag) {
       constexpr int I = decltype(i_tag)::value;
       constexpr int KB = I / (2 * KSTEPS), ST = (I / 2) % KSTEPS;
       constexpr int AHEAD = (I + RW < TOT ? I + RW : TOT) - I - 1;
       lds_wait_lgkm<AHEAD>();
       lds_ready(ar[I]);
-      if constexpr (I % 2 == 0)
+      if constexpr (I % 2 == 0) {
         st[KB] = mfma32(as_bf16x8(ar[I]), qf[ST], st[KB]);
-      else
+        asm volatile("" : "+v"(st[KB]));
+      } else {
         dpt[KB] = mfma32(as_bf16x8(ar[I]), df[ST], dpt[KB]);
-      issue(std::integral_constant<int, I + RW>());
-    });
-    // dS^T = P^T (dP^T - D) as bf16, 16-key chunk kc = rows 8 (kc % 2) .. +7
-    // of key block kc / 2
-    bf16x8 dsf[4];
-#pragma unroll
-    for (int kc = 0; kc < 4; ++kc) {
-      float e[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int r = 8 * (kc % 2) + j;
-        const int key = key0 + (kc / 2) * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-        const float p = bwd_prob(st[kc / 2][r], c, lse2, key <= lim);
-        e[j] = p * (dpt[kc / 2][r] - dl);
+        asm volatile("" : "+v"(dpt[KB]));
       }
-      dsf[kc] = to_bf16x8(e[0], e[1], e[2], e[3], e[4], e[5], e[6], e[7]);
-    }
-    // dQ^T += K^T dS^T over the four 16-key chunks
+      issue(std::integral_constant<int, I + RW>());
+      if constexpr (I >= NA / 2)
+        static_for<0, EPA>([&](auto e_tag) {
+          elem(std::integral_constant<int, EPA * (I - NA / 2) + decltype(e_tag)::value>());
+        });
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    constexpr int EPC = 16 / (2 * DBLK);  // elements of key block 1 per dQ^T product
     static_for<0, 4 * DBLK>([&](auto m_tag) {
       constexpr int M = decltype(m_tag)::value;  // (kc, db) = (M / DBLK, M % DBLK)
       constexpr int BASE = NA + 2 * M;
@@ -279,8 +293,14 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
       lds_ready(cr[2 * M + 1]);
       const u32x4 w = {cr[2 * M][0], cr[2 * M][1], cr[2 * M + 1][0], cr[2 * M + 1][1]};
       acc[M % DBLK] = mfma32(as_bf16x8(w), dsf[M / DBLK], acc[M % DBLK]);
+      asm volatile("" : "+v"(acc[M % DBLK]));
       issue(std::integral_constant<int, BASE + RW>());
       issue(std::integral_constant<int, BASE + RW + 1>());
+      if constexpr (M < 2 * DBLK)
+        static_for<0, EPC>([&](auto e_tag) {
+          elem(std::integral_constant<int, 16 + EPC * M + decltype(e_tag)::value>());
+        });
+      __builtin_amdgcn_sched_barrier(0);
     });
     __syncthreads();
     if (kt + 2 < n_kt) issue_tile(kt + 2, BUF);
