@@ -1,6 +1,7 @@
 """Seeded random sweeps on the GPU against the fp64 oracle, through the C ABI:
 dense forward (mixed head groups, head dims, causal or not, ragged and
-clamped lengths, scales of either sign or zero, sharpened keys), packed
+clamped lengths, scales of either sign or zero, sharpened keys; its V^T
+workspace path bitwise against it), packed
 ragged forward, decode with random lengths and part counts (contiguous and
 paged caches), MLA decode, and the backward (gradients against the
 oracle's backward).  Every
@@ -53,6 +54,14 @@ def test_fwd_random(i):
     o_ref, lse_ref = orc.attn_fwd(workloads.bits(q), workloads.bits(k), workloads.bits(v),
                                   causal=c["causal"], scale=c["scale"], kv_seqlens=c["lens"])
     assert_parity(f"fwd_random_{i}", o, lse, o_ref, lse_ref)
+    # the V^T workspace path forms the same products in the same order
+    ws = torch.empty(mk.mk_attn_fwd_workspace_bytes(c["B"], c["Hkv"], c["Skv"], c["D"]),
+                     dtype=torch.uint8, device=DEV)
+    o_ws, lse_ws = mk.fwd(q.to(DEV), k.to(DEV), v.to(DEV), causal=c["causal"], scale=c["scale"],
+                          kv_seqlens=sl, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(o_ws.view(torch.int16), o.view(torch.int16)), f"fwd_random_{i}: ws O"
+    assert torch.equal(lse_ws.view(torch.int32), lse.view(torch.int32)), f"fwd_random_{i}: ws LSE"
 
 
 @pytest.mark.parametrize("i", range(N_VARLEN))
