@@ -410,7 +410,7 @@ def main():
     ap.add_argument("--cpu-baseline", choices=("all", "headline", "none"), default="all",
                     help="oracle timing: every workload, the headline sample only, or none")
     ap.add_argument("--page-size", type=int, default=16, help="page size of the paged leg")
-    ap.add_argument("--ws-min-seq", type=int, default=16384,
+    ap.add_argument("--ws-min-seq", type=int, default=8192,
                     help="prefill workloads with at least this many keys run through "
                          "mk_attn_fwd_ws (0: all bf16 ones; a huge value: none)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,

@@ -8,8 +8,8 @@ namespace {
 
 template <int D, bool CAUSAL, bool POS>
 hipError_t go_vt(const FwdArgs& a, unsigned nblocks, hipStream_t st) {
-  hipLaunchKernelGGL((fwd_kernel<D, CAUSAL, false, kFwdQB, POS, false, kFwdWaves, false, true>),
-                     dim3(nblocks), dim3(FwdShape<D, kFwdQB, kFwdWaves>::THREADS), 0, st, a);
+  hipLaunchKernelGGL((fwd_kernel<D, CAUSAL, false, kFwdQB, POS, false, kFwdVtWaves, false, true>),
+                     dim3(nblocks), dim3(FwdShape<D, kFwdQB, kFwdVtWaves>::THREADS), 0, st, a);
   return hipGetLastError();
 }
 

@@ -15,6 +15,9 @@ namespace mk {
 
 constexpr int kFwdQB = 1;     // 32-query blocks per wave in the forward kernel
 constexpr int kFwdWaves = 4;  // waves per forward workgroup (128 query rows)
+// waves per workgroup of the V^T forward (256 query rows sharing each K/V
+// tile, one workgroup per compute unit)
+constexpr int kFwdVtWaves = 8;
 
 // Dense [B, H, S, D] forward: nblocks workgroups of the forward kernel.
 hipError_t launch_fwd(const FwdArgs& a, unsigned nblocks, int D, bool causal, bool out_f32,
@@ -22,7 +25,7 @@ hipError_t launch_fwd(const FwdArgs& a, unsigned nblocks, int D, bool causal, bo
 
 // Dense forward through a V^T copy (bf16 O): the pack kernel writes
 // a.vt (pack_blocks = B * Hkv * vt_tiles workgroups), then the forward
-// reads V from it.
+// (nblocks workgroups of kFwdVtWaves waves) reads V from it.
 hipError_t launch_fwd_vt(const FwdArgs& a, unsigned nblocks, int D, bool causal, bool pos_scale,
                          unsigned pack_blocks, hipStream_t st);
 

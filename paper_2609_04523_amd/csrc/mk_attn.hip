@@ -89,9 +89,14 @@ int fwd_impl(const void* q, const void* k, const void* v, void* o, float* lse, i
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool pos = scale > 0.f;
   if (vt) {
+    // workgroups of kFwdVtWaves waves, one per compute unit
+    const int BM_VT = mk::FwdShape<128, mk::kFwdQB, mk::kFwdVtWaves>::BM;
+    const long long nq_vt = (Sq + BM_VT - 1) / BM_VT;
+    a.n_qtiles = (int)nq_vt;
+    a.xcd_gp = ((B * Hkv) % 8 == 0) ? mk::xcd_group_pairs(Hq / Hkv, (int)nq_vt, 1) : 0;
     const long long pack_blocks = (long long)B * Hkv * a.vt_tiles;
     if (pack_blocks > 0x7fffffffLL) return MK_ERR_SHAPE;
-    const hipError_t e = mk::launch_fwd_vt(a, (unsigned)nblocks, D, causal, pos,
+    const hipError_t e = mk::launch_fwd_vt(a, (unsigned)(nq_vt * B * Hq), D, causal, pos,
                                            (unsigned)pack_blocks, st);
     return e == hipSuccess ? MK_OK : MK_ERR_HIP;
   }

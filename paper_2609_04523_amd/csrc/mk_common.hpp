@@ -291,9 +291,9 @@ __device__ __forceinline__ void xcd_pair_map(int bid, int n_qtiles, int B, int H
 }
 
 // Pairs per group for xcd_pair_map: the q-tiles one XCD holds at once (32
-// compute units, two workgroups each) over the q-tiles of one pair.
-inline int xcd_group_pairs(int G, int n_qtiles) {
-  const int gp = 64 / (G * n_qtiles);
+// compute units, wg_per_cu workgroups each) over the q-tiles of one pair.
+inline int xcd_group_pairs(int G, int n_qtiles, int wg_per_cu = 2) {
+  const int gp = 32 * wg_per_cu / (G * n_qtiles);
   return gp < 1 ? 1 : gp;
 }
 
