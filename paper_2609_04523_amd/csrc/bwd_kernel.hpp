@@ -12,13 +12,14 @@
 // P is recomputed from the forward's LSE, P_ij = exp(scale s_ij - LSE_i),
 // so no attention matrix is stored.
 //
-// Three kernels on one stream:
-//   bwd_delta_kernel  D_i from the forward's O and dO (16 lanes per row);
+// Two kernels on one stream:
 //   bwd_dq_kernel     one workgroup per 128 query rows of one (b, hq),
 //                     shaped like the forward: K and V 64-key tiles stream
 //                     through LDS, each wave keeps its 32 rows' Q and dO in
-//                     registers and accumulates dQ^T = K^T dS^T;
-//   bwd_dkdv_kernel   one workgroup per 128 keys of one (b, kv head): each
+//                     registers and accumulates dQ^T = K^T dS^T; it first
+//                     forms D_i = dO_i . O_i and LSE_i log2 e of its rows
+//                     and writes them to the workspace;
+//   bwd_dkdv_kernel   (after it) one workgroup per 128 keys of one (b, kv head): each
 //                     wave keeps its 32 keys' K and V in registers, the Q,
 //                     dO, LSE and D tiles of every query head of the group
 //                     stream through LDS, and dK^T = Q^T dS, dV^T = dO^T P
@@ -56,41 +57,6 @@ struct BwdArgs {
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-// D_i = dO_i . O_i (16 lanes per row of D bf16 values) and LSE_i log2(e),
-// over sq_pad rows per (b, hq): rows past Sq get D = 0 and +inf.  The dQ
-// and dK/dV kernels read both arrays without row bounds (their 128- and
-// 64-row tiles end at or before sq_pad).
-template <int D>
-__global__ __launch_bounds__(256) void bwd_delta_kernel(BwdArgs a) {
-  constexpr int LPR = 16;
-  constexpr int WORDS = D / LPR / 2;  // 32-bit words (bf16 pairs) per lane
-  const long long rows = (long long)a.B * a.Hq * a.sq_pad;
-  const long long row = (long long)blockIdx.x * (256 / LPR) + threadIdx.x / LPR;
-  const int part = threadIdx.x % LPR;
-  const long long bh = row / a.sq_pad;
-  const int i = (int)(row - bh * a.sq_pad);
-  const bool real = row < rows && i < a.Sq;
-  const long long src = bh * a.Sq + i;  // row of O, dO and LSE
-  float acc = 0.f;
-  if (real) {
-    const uint32_t* o = reinterpret_cast<const uint32_t*>(a.o + src * D) + part * WORDS;
-    const uint32_t* d = reinterpret_cast<const uint32_t*>(a.dout + src * D) + part * WORDS;
-#pragma unroll
-    for (int w = 0; w < WORDS; ++w) {
-      const uint32_t x = o[w], y = d[w];
-      acc = fmaf(bf16_lo(x), bf16_lo(y), acc);
-      acc = fmaf(bf16_hi(x), bf16_hi(y), acc);
-    }
-  }
-#pragma unroll
-  for (int off = LPR / 2; off >= 1; off >>= 1) acc += __shfl_xor(acc, off, 64);
-  if (row < rows && part == 0) {
-    const float lse = real ? a.lse[src] : kNegInf;
-    a.delta[row] = acc;
-    a.lse2[row] = lse == kNegInf ? __builtin_inff() : lse * kLog2e;
-  }
-}
 
 // P of one element: 2^(s c - LSE log2 e), 0 where masked (lse2 = +inf on
 // rows without keys gives 0 by itself).
@@ -155,9 +121,34 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdArgs a) {
     qf[s] = as_bf16x8(u);
     df[s] = as_bf16x8(w);
   }
+  // D_i = dO_i . O_i (this lane's half of the row, then its partner lane's
+  // half) and LSE_i log2 e, kept for this kernel and written to the
+  // workspace for the dK/dV kernel, which runs next; padding rows (past Sq)
+  // and rows without keys get D = 0 and +inf, so that P vanishes there.
   const size_t prow = ((size_t)b * a.Hq + hq) * (size_t)a.sq_pad + qrow;  // qrow < sq_pad
-  const float lse2 = a.lse2[prow];
-  const float dl = a.delta[prow];
+  float dl = 0.f, lse2 = __builtin_inff();
+  {
+    float part = 0.f;
+    if (row_ok) {
+#pragma unroll
+      for (int s = 0; s < KSTEPS; ++s) {
+        const u32x4 ov = *reinterpret_cast<const u32x4*>(a.o + (row0 + qrow) * D + s * 16 + h * 8);
+        const u32x4 dv = as_u32x4(df[s]);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          part = fmaf(bf16_lo(ov[w]), bf16_lo(dv[w]), part);
+          part = fmaf(bf16_hi(ov[w]), bf16_hi(dv[w]), part);
+        }
+      }
+      const float lse = a.lse[row0 + qrow];
+      lse2 = lse == kNegInf ? __builtin_inff() : lse * kLog2e;
+    }
+    dl = part + __shfl_xor(part, 32, 64);
+    if (h == 0) {
+      a.delta[prow] = dl;
+      a.lse2[prow] = lse2;
+    }
+  }
   const int lim = CAUSAL ? min(L - 1, qrow + off) : L - 1;  // last key this row sees
 
   // tile loads, as in the forward kernel

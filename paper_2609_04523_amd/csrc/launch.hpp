@@ -40,10 +40,10 @@ hipError_t launch_fwd_ragged_paged(const FwdArgs& a, unsigned nblocks, int D, bo
 // Decode: the part kernel (contiguous or paged cache) then the merge kernel.
 hipError_t launch_decode(const DecArgs& a, int D, int qblocks, bool paged, hipStream_t st);
 
-// Backward: the row-delta kernel, the dK/dV kernel (skipped when
-// dkdv_blocks is 0), then the dQ kernel.
-hipError_t launch_bwd(const BwdArgs& a, unsigned delta_blocks, unsigned dq_blocks,
-                      unsigned dkdv_blocks, int D, bool causal, hipStream_t st);
+// Backward: the dQ kernel (it also writes the rows' D and LSE log2 e),
+// then the dK/dV kernel (skipped when dkdv_blocks is 0).
+hipError_t launch_bwd(const BwdArgs& a, unsigned dq_blocks, unsigned dkdv_blocks, int D,
+                      bool causal, hipStream_t st);
 
 // MLA decode (q [B, 16, 576], latent cache [B, Smax, 576] in kc, O
 // [B, 16, 512]): the part kernel, then the merge kernel.

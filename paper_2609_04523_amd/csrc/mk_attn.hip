@@ -513,12 +513,9 @@ int mk_attn_bwd(const void* q, const void* k, const void* v, const void* o, cons
   if (kv_seqlens && !aligned(kv_seqlens, 4)) return MK_ERR_ALIGN;
   // workgroups of each launch
   const long long sq_pad = (Sq + 127) / 128 * 128;
-  const long long rows = (long long)B * Hq * sq_pad;
-  const long long delta_blocks = (rows + 15) / 16;
   const long long dq_blocks = (long long)((Sq + 127) / 128) * B * Hq;
   const long long dkdv_blocks = (long long)((Skv + 127) / 128) * B * Hkv;
-  if (delta_blocks > 0x7fffffffLL || dq_blocks > 0x7fffffffLL || dkdv_blocks > 0x7fffffffLL)
-    return MK_ERR_SHAPE;
+  if (dq_blocks > 0x7fffffffLL || dkdv_blocks > 0x7fffffffLL) return MK_ERR_SHAPE;
   const size_t need = mk_attn_bwd_workspace_bytes(B, Hq, Sq);
   if (!workspace || workspace_bytes < need) return MK_ERR_WORKSPACE;
   if (!aligned(workspace, 256)) return MK_ERR_ALIGN;
@@ -548,8 +545,8 @@ int mk_attn_bwd(const void* q, const void* k, const void* v, const void* o, cons
   a.scale = scale;
   a.scale_log2 = scale * mk::kLog2e;
   const hipError_t e =
-      mk::launch_bwd(a, (unsigned)delta_blocks, (unsigned)dq_blocks, (unsigned)dkdv_blocks, D,
-                     causal != 0, static_cast<hipStream_t>(stream));
+      mk::launch_bwd(a, (unsigned)dq_blocks, (unsigned)dkdv_blocks, D, causal != 0,
+                     static_cast<hipStream_t>(stream));
   return e == hipSuccess ? MK_OK : MK_ERR_HIP;
 }
 
