@@ -90,7 +90,10 @@ int mk_attn_fwd_o32(const void *q, const void *k, const void *v, float *o, float
  * 16-byte reads instead of transposing ones.  The copy costs one read and
  * one write of V (4 * B * Hkv * Skv * D bytes of HBM traffic), which pays
  * where each key tile is used by many query tiles (long causal sequences,
- * grouped query heads).
+ * grouped query heads).  The forward itself runs as one workgroup per
+ * compute unit, each taking 256-row query tiles from counters at the end
+ * of the workspace until none are left (the K/V heads' tiles grouped by
+ * XCD, so each XCD's L2 holds the heads it works on).
  *   workspace        device memory of at least
  *                    mk_attn_fwd_workspace_bytes(B, Hkv, Skv, D) bytes,
  *                    16-byte aligned, owned by the caller; overwritten by
@@ -108,8 +111,9 @@ int mk_attn_fwd_ws(const void *q, const void *k, const void *v, void *o, float *
 
 /*
  * Workspace bytes mk_attn_fwd_ws needs: B * Hkv * ceil(Skv / 64) * 64 * D
- * * 2.  Returns 0 for arguments mk_attn_fwd_ws would reject as a shape
- * (B, Hkv, Skv < 1, D not 64 or 128).
+ * * 2 for the V^T tiles, plus 1024 for the work-item counters of its
+ * persistent grid.  Returns 0 for arguments mk_attn_fwd_ws would reject as
+ * a shape (B, Hkv, Skv < 1, D not 64 or 128).
  */
 size_t mk_attn_fwd_workspace_bytes(int B, int Hkv, int Skv, int D);
 

@@ -70,6 +70,12 @@ struct FwdArgs {
   // bf16 (vt_tiles = ceil(Skv / 64))
   const uint16_t* vt;
   int vt_tiles;
+  // PERSIST only: work-item queues.  Queue x (x < n_queues) holds the items
+  // bid = n_queues * i + x, i < per_queue, in fwd_map_block's order; its
+  // counter ctr[32 x] (set to the grid's share per queue before the launch:
+  // workgroup bid takes item bid first) hands out i.
+  int* ctr;
+  int n_queues, per_queue;
 };
 
 // Tokens [start, end) of sequence b from cumulative offsets, clamped into
@@ -133,11 +139,18 @@ __device__ __forceinline__ void fwd_map_block(int bid, const FwdArgs& a, int& qt
 // VT (dense batches only): the V tiles come from the pre-pass's V^T tiles
 // (contiguous 64-key blocks of D * 128 bytes, copied to LDS as they are) and
 // the products read them with ds_read_b128.
+// PERSIST (with VT): a grid of one workgroup per compute unit works through
+// the items of FwdArgs' queues: workgroup bid first takes item bid, then
+// items of its own queue (the K/V heads its XCD holds), then of the others
+// once its own is empty, so XCDs that run ahead take over the rest of the
+// slower ones' work.  The next item's Q and first K tile are loaded while
+// the current one's output goes out, through an LDS area of its own.
 template <int D, bool CAUSAL, bool OUT_F32, int QB, bool POS_SCALE, bool VARLEN, int WAVES,
-          bool PAGED = false, bool VT = false>
+          bool PAGED = false, bool VT = false, bool PERSIST = false>
 __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
   static_assert(VARLEN || !PAGED, "the paged cache is read by the packed forward");
   static_assert(!(VT && VARLEN), "the V^T copy is made for dense batches");
+  static_assert(!PERSIST || (VT && !OUT_F32), "the persistent grid runs the V^T path");
   using S = FwdShape<D, QB, WAVES>;
   constexpr int BN = S::BN;
   constexpr int TILE = BN * D;            // bf16 per tile per tensor
@@ -156,6 +169,10 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
   uint16_t(*const k_lds)[TILE] = kv_lds;
   uint16_t(*const v_lds)[TILE] = kv_lds + 2;
   static_assert(S::WAVES * 32 * QB * D * 2 <= 4 * TILE_BYTES, "output staging fits the tiles");
+  // PERSIST: the output rows' staging area (each wave its own 32 rows), and
+  // the next work item as claimed by thread 0, by item parity
+  __shared__ __attribute__((aligned(16))) uint16_t o_stage[PERSIST ? S::WAVES * 32 * D : 8];
+  __shared__ int next_item[2];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -163,82 +180,101 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
   const int n = lane & 31;  // MFMA column (query) / row (key) within a 32-block
   const int h = lane >> 5;  // MFMA k-group
 
-  int qt, hq, b;
-  fwd_map_block(blockIdx.x, a, qt, hq, b);
   const int G = a.Hq / a.Hkv;
-  const int g = hq / G;
-  // Where the rows of (b, hq) and (b, g) live: query / output row i at
-  // q_base + i * q_stride (elements), key / value row j at byte
-  // j * kv_stride from kg / vg, LSE of row i at lse_base[i].
-  int Sq, L;
+  // The work item: query tile qt of (b, hq), kv head g.  Where its rows
+  // live: query / output row i at q_base + i * q_stride (elements), key /
+  // value row j at byte j * kv_stride from kg / vg, LSE of row i at
+  // lse_base[i].
+  int qt, hq, b, g, Sq, L;
   const uint16_t* q_base;
   size_t o_base, q_stride, kv_stride;
-  float* lse_base = a.lse;
+  float* lse_base;
   const char* kg;
   const char* vg;
-  if constexpr (VARLEN) {
-    int qs, ks = 0;
-    fwd_seq_range(a.cu_q, b, a.total_q, qs, Sq);
-    if constexpr (PAGED)
-      L = clamp_len(a.kv_seqlens[b], a.max_pages * a.page_size);
-    else
-      fwd_seq_range(a.cu_k, b, a.total_k, ks, L);
-    if (qt * S::BM >= Sq) return;  // past this sequence's queries (whole workgroup)
-    o_base = ((size_t)qs * a.Hq + hq) * D;
-    q_stride = (size_t)a.Hq * D;
-    if (lse_base) lse_base += (size_t)hq * a.total_q + qs;
-    if constexpr (PAGED) {
-      // rows of one head inside a page are consecutive; kg / vg point at
-      // head g of page 0 (page p adds p * Hkv * page_size rows)
-      kv_stride = ROW_BYTES;
-      const size_t kv_off = (size_t)g * a.page_size * D;
-      kg = reinterpret_cast<const char*>(a.k + kv_off);
-      vg = reinterpret_cast<const char*>(a.v + kv_off);
+  int off, q0, n_kt, n_full, qw0, n_free, n_live;
+  // Sets the item's geometry; false when the item holds no query rows (a
+  // q-tile past its sequence's queries in a packed batch).
+  auto setup = [&](int bid) -> bool {
+    fwd_map_block(bid, a, qt, hq, b);
+    g = hq / G;
+    lse_base = a.lse;
+    if constexpr (VARLEN) {
+      int qs, ks = 0;
+      fwd_seq_range(a.cu_q, b, a.total_q, qs, Sq);
+      if constexpr (PAGED)
+        L = clamp_len(a.kv_seqlens[b], a.max_pages * a.page_size);
+      else
+        fwd_seq_range(a.cu_k, b, a.total_k, ks, L);
+      if (qt * S::BM >= Sq) return false;  // past this sequence's queries
+      o_base = ((size_t)qs * a.Hq + hq) * D;
+      q_stride = (size_t)a.Hq * D;
+      if (lse_base) lse_base += (size_t)hq * a.total_q + qs;
+      if constexpr (PAGED) {
+        // rows of one head inside a page are consecutive; kg / vg point at
+        // head g of page 0 (page p adds p * Hkv * page_size rows)
+        kv_stride = ROW_BYTES;
+        const size_t kv_off = (size_t)g * a.page_size * D;
+        kg = reinterpret_cast<const char*>(a.k + kv_off);
+        vg = reinterpret_cast<const char*>(a.v + kv_off);
+      } else {
+        kv_stride = (size_t)a.Hkv * ROW_BYTES;
+        const size_t kv_off = ((size_t)ks * a.Hkv + g) * D;
+        kg = reinterpret_cast<const char*>(a.k + kv_off);
+        vg = reinterpret_cast<const char*>(a.v + kv_off);
+      }
     } else {
-      kv_stride = (size_t)a.Hkv * ROW_BYTES;
-      const size_t kv_off = ((size_t)ks * a.Hkv + g) * D;
+      Sq = a.Sq;
+      L = a.kv_seqlens ? clamp_len(a.kv_seqlens[b], a.Skv) : a.Skv;
+      const size_t q_row0 = ((size_t)b * a.Hq + hq) * (size_t)a.Sq;
+      o_base = q_row0 * D;
+      q_stride = D;
+      kv_stride = ROW_BYTES;
+      if (lse_base) lse_base += q_row0;
+      const size_t kv_off = ((size_t)b * a.Hkv + g) * (size_t)a.Skv * D;
       kg = reinterpret_cast<const char*>(a.k + kv_off);
-      vg = reinterpret_cast<const char*>(a.v + kv_off);
+      vg = reinterpret_cast<const char*>(
+          VT ? a.vt + ((size_t)b * a.Hkv + g) * a.vt_tiles * (size_t)TILE : a.v + kv_off);
     }
-  } else {
-    Sq = a.Sq;
-    L = a.kv_seqlens ? clamp_len(a.kv_seqlens[b], a.Skv) : a.Skv;
-    const size_t q_row0 = ((size_t)b * a.Hq + hq) * (size_t)a.Sq;
-    o_base = q_row0 * D;
-    q_stride = D;
-    kv_stride = ROW_BYTES;
-    if (lse_base) lse_base += q_row0;
-    const size_t kv_off = ((size_t)b * a.Hkv + g) * (size_t)a.Skv * D;
-    kg = reinterpret_cast<const char*>(a.k + kv_off);
-    vg = reinterpret_cast<const char*>(
-        VT ? a.vt + ((size_t)b * a.Hkv + g) * a.vt_tiles * (size_t)TILE : a.v + kv_off);
-  }
-  q_base = a.q + o_base;
-  const int off = L - Sq;  // bottom-right causal alignment
-  const int q0 = qt * S::BM;
-  const int q_end = min(q0 + S::BM, Sq);
-  int n_keys = L;
-  if (CAUSAL) n_keys = min(L, q_end + off);
-  if (n_keys < 0) n_keys = 0;
-  const int n_kt = (n_keys + BN - 1) / BN;
-  const int n_full = L / BN;  // tiles that lie wholly inside the sequence
+    q_base = a.q + o_base;
+    off = L - Sq;  // bottom-right causal alignment
+    q0 = qt * S::BM;
+    const int q_end = min(q0 + S::BM, Sq);
+    int n_keys = L;
+    if (CAUSAL) n_keys = min(L, q_end + off);
+    if (n_keys < 0) n_keys = 0;
+    n_kt = (n_keys + BN - 1) / BN;
+    n_full = L / BN;  // tiles that lie wholly inside the sequence
+    qw0 = q0 + wave * 32 * QB;
+    // Tiles [0, n_free) need no mask for any row of this wave; tiles up to
+    // n_live hold at least one admissible key for some row of the wave.
+    const int w_first = qw0;  // first query row of the wave
+    const int w_last = min(qw0 + 32 * QB, Sq) - 1;
+    n_free = (CAUSAL ? min(L, w_first + off + 1) : L) / BN;
+    n_live = qw0 < Sq ? (CAUSAL ? min(L, w_last + off + 1) : L) : 0;
+    n_live = (max(n_live, 0) + BN - 1) / BN;
+    n_free = max(0, min(n_free, n_live));
+    return true;
+  };
+  if (!setup(blockIdx.x)) return;  // (the whole workgroup)
   const float c = a.scale_log2;
 
   // Q^T fragments: lane (column n, k-group h) holds q[row][16 s + 8 h .. +7].
   // Loaded before any K/V traffic so waiting for them waits for nothing else.
-  const int qw0 = q0 + wave * 32 * QB;
   bf16x8 qf[QB][S::KSTEPS];
+  auto load_q = [&]() {
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int row = qw0 + qb * 32 + n;
+    for (int qb = 0; qb < QB; ++qb) {
+      const int row = qw0 + qb * 32 + n;
 #pragma unroll
-    for (int s = 0; s < S::KSTEPS; ++s) {
-      u32x4 u = {0u, 0u, 0u, 0u};
-      if (row < Sq)
-        u = *reinterpret_cast<const u32x4*>(q_base + row * q_stride + s * 16 + h * 8);
-      qf[qb][s] = as_bf16x8(u);
+      for (int s = 0; s < S::KSTEPS; ++s) {
+        u32x4 u = {0u, 0u, 0u, 0u};
+        if (row < Sq)
+          u = *reinterpret_cast<const u32x4*>(q_base + row * q_stride + s * 16 + h * 8);
+        qf[qb][s] = as_bf16x8(u);
+      }
     }
-  }
+  };
+  load_q();
 
   // ---- tile loads: HBM -> LDS, one 1 KB wave-wide load per block ----
   // Block blk = 4 p + wave of a tile holds rows blk*ROWS_PER_KB + l/CHUNKS;
@@ -328,23 +364,18 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
 
   float m_run[QB], l_run[QB];
   f32x16 o_acc[QB][S::DBLK];
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    m_run[qb] = kNegInf;
-    l_run[qb] = 0.f;
-#pragma unroll
-    for (int db = 0; db < S::DBLK; ++db)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o_acc[qb][db][r] = 0.f;
-  }
 
   using B0 = std::integral_constant<int, 0>;
   using B1 = std::integral_constant<int, 1>;
-  if (n_kt > 0)
-    static_for<0, S::BLOCKS_PER_WAVE>([&](auto p_tag) {
-      issue_rows(kg, k_lds_w, 0, B0(), p_tag, std::false_type(),
-                 PAGED ? page_row(block_row(0, decltype(p_tag)::value)) : 0);
-    });
+  // the item's first K tile into K buffer 0
+  auto issue_k0 = [&]() {
+    if (n_kt > 0)
+      static_for<0, S::BLOCKS_PER_WAVE>([&](auto p_tag) {
+        issue_rows(kg, k_lds_w, 0, B0(), p_tag, std::false_type(),
+                   PAGED ? page_row(block_row(0, decltype(p_tag)::value)) : 0);
+      });
+  };
+  issue_k0();
 
   // Lane parts of the LDS read addresses (bytes within a tile).  K row
   // 32 kb + n: the swizzle of n + 32 kb equals that of n.  Transposing V
@@ -375,23 +406,12 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
       }
   }
 
-  // Tiles [0, n_free) need no mask for any row of this wave; tiles up to
-  // n_live hold at least one admissible key for some row of the wave.
-  const int w_first = qw0;                      // first query row of the wave
-  const int w_last = min(qw0 + 32 * QB, Sq) - 1;
-  int n_free = (CAUSAL ? min(L, w_first + off + 1) : L) / BN;
-  int n_live = qw0 < Sq ? (CAUSAL ? min(L, w_last + off + 1) : L) : 0;
-  n_live = (max(n_live, 0) + BN - 1) / BN;
-  n_free = max(0, min(n_free, n_live));
-
   // Scores (fp32) and weights (bf16 P^T fragments) of even and odd tiles.
   // Step t forms the scores of tile t, turns those of tile t - 1 into
   // weights and adds the weights of tile t - 2 times V into O.
   f32x16 s_even[QB][2], s_odd[QB][2];
   u32x4 p_even[QB][4], p_odd[QB][4];  // bf16 bits (carried as integers)
   float m_use[QB];  // exponent offset of the weights being formed
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) m_use[qb] = 0.f;
 
   // Step t (t = 0 .. n_kt + 1) of the pipeline, for one wave:
   //   A  PV (2 <= t <= n_live + 1): O += P(t-2) V(t-2) on the matrix cores,
@@ -791,9 +811,19 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
   // has finished step t - 1, whose buffers the step's loads overwrite.
   using T1 = std::true_type;
   using F0 = std::false_type;
+  // PERSIST: thread 0 claims the next index of its own queue two steps
+  // before an item's last (the atomic's return is waited for with that
+  // step's tile loads) and keeps a mask of the queues it has found empty.
+  const int own_q = PERSIST ? (int)(blockIdx.x % (unsigned)a.n_queues) : 0;
+  int pending = 0;
+  unsigned drained = 0;
   auto run_step = [&](int t, auto par_tag) {
     wait_vmcnt<0>();
     __syncthreads();
+    if constexpr (PERSIST) {
+      if (t == max(n_kt - 1, 0) && tid == 0)
+        pending = ((drained >> own_q) & 1u) ? a.per_queue : atomicAdd(a.ctr + 32 * own_q, 1);
+    }
     const bool qk = t < n_live;
     const bool ex = t >= 1 && t <= n_live;
     const bool pv = t >= 2 && t <= n_live + 1;
@@ -841,42 +871,120 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void fwd_kernel(FwdArgs a) {
       step(t, par_tag, F0(), F0(), F0(), F0(), F0(), F0());
     }
   };
-  if (n_kt > 0) {
-    for (int t = 0; t <= n_kt + 1; t += 2) {
-      run_step(t, B0());
-      if (t + 1 <= n_kt + 1) run_step(t + 1, B1());
-    }
-  }
-
-  // ---- epilogue: O = O_acc / l, LSE = ln 2 * (m + log2 l).  bf16 O is
-  // staged through the (now free) K buffers so that the stores are whole
-  // rows; fp32 O goes out 16 bytes per lane directly. ----
-  if constexpr (!OUT_F32) __syncthreads();
+  for (int par_item = 0;; par_item ^= 1) {
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int qrow = qw0 + qb * 32 + n;
-    const float lsum = sum_xor32(l_run[qb]);
-    const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
-    if constexpr (!OUT_F32) {
-      store_rows_t<D>(o_acc[qb], inv, lds_addr(&k_lds[0][0]) + wave * 32 * ROW_BYTES, n, h,
-                      lane, static_cast<uint16_t*>(a.o) + o_base + (qw0 + qb * 32) * q_stride,
-                      q_stride, Sq - (qw0 + qb * 32));
-    }
-    if (qrow >= Sq) continue;
-    if constexpr (OUT_F32) {
-      const size_t obase = o_base + qrow * q_stride;
+    for (int qb = 0; qb < QB; ++qb) {
+      m_run[qb] = kNegInf;
+      l_run[qb] = 0.f;
+      m_use[qb] = 0.f;
 #pragma unroll
       for (int db = 0; db < S::DBLK; ++db)
 #pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-          const int d = db * 32 + 8 * r4 + 4 * h;
-          const f32x4 w = {o_acc[qb][db][4 * r4 + 0] * inv, o_acc[qb][db][4 * r4 + 1] * inv,
-                           o_acc[qb][db][4 * r4 + 2] * inv, o_acc[qb][db][4 * r4 + 3] * inv};
-          *reinterpret_cast<f32x4*>(static_cast<float*>(a.o) + obase + d) = w;
-        }
+        for (int r = 0; r < 16; ++r) o_acc[qb][db][r] = 0.f;
     }
-    if (h == 0 && lse_base)
-      lse_base[qrow] = lsum > 0.f ? (m_run[qb] + log2f(lsum)) * kLn2 : kNegInf;
+    // (an item without tiles claims here)
+    if constexpr (PERSIST) {
+      if (n_kt == 0 && tid == 0)
+        pending = ((drained >> own_q) & 1u) ? a.per_queue : atomicAdd(a.ctr + 32 * own_q, 1);
+    }
+    if (n_kt > 0) {
+      for (int t = 0; t <= n_kt + 1; t += 2) {
+        run_step(t, B0());
+        if (t + 1 <= n_kt + 1) run_step(t + 1, B1());
+      }
+    }
+
+    // PERSIST: the next item (-1: none left), from the own queue, else from
+    // the others in turn.  Past the barrier every wave is done with the K
+    // buffers, so the next item's first K tile can go into buffer 0 while
+    // this item's output is written.
+    int next = -1;
+    if constexpr (PERSIST) {
+      if (tid == 0) {
+        int nb = -1;
+        if (pending < a.per_queue) {
+          nb = pending * a.n_queues + own_q;
+        } else {
+          drained |= 1u << own_q;
+          for (int k = 1; k < a.n_queues && nb < 0; ++k) {
+            const int x = (own_q + k) % a.n_queues;
+            if ((drained >> x) & 1u) continue;
+            const int i = atomicAdd(a.ctr + 32 * x, 1);
+            if (i < a.per_queue)
+              nb = i * a.n_queues + x;
+            else
+              drained |= 1u << x;
+          }
+        }
+        next_item[par_item] = nb;
+      }
+      __syncthreads();
+      // the same in every lane: saying so keeps the item's geometry in
+      // scalar registers
+      next = __builtin_amdgcn_readfirstlane(next_item[par_item]);
+    }
+    const size_t e_o_base = o_base;  // where the finished item's rows go
+    float* const e_lse = lse_base;
+    const int e_qw0 = qw0, e_Sq = Sq;
+
+    // ---- epilogue: O = O_acc / l, LSE = ln 2 * (m + log2 l).  bf16 O is
+    // staged through LDS (the now free K buffers, or PERSIST's own area) so
+    // that the stores are whole rows; fp32 O goes out 16 bytes per lane
+    // directly.  PERSIST: the next item's loads are issued between the LDS
+    // round trip and the stores (LDS reads issued after LDS-DMA loads would
+    // wait for them). ----
+    if constexpr (!OUT_F32 && !PERSIST) __syncthreads();
+    // the lane's indices formed anew here (an opaque copy of the thread
+    // index), so that the output addresses, which do not change from item
+    // to item, are not computed once and held in registers through the
+    // item's tiles
+    int tid_e = tid;
+    asm volatile("" : "+v"(tid_e));
+    const int lane_e = tid_e & 63, n_e = lane_e & 31, h_e = lane_e >> 5;
+    const uint32_t stage =
+        (PERSIST ? lds_addr(&o_stage[0]) : lds_addr(&k_lds[0][0])) + wave * 32 * ROW_BYTES;
+    float lsum[QB];
+    u32x4 rows[QB][OUT_F32 ? 1 : D / 16];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      lsum[qb] = sum_xor32(l_run[qb]);
+      if constexpr (!OUT_F32)
+        stage_rows_t<D>(o_acc[qb], lsum[qb] > 0.f ? 1.f / lsum[qb] : 0.f, stage, n_e, h_e,
+                        lane_e, rows[qb]);
+    }
+    if constexpr (PERSIST) {
+      if (next >= 0) {
+        setup(next);
+        load_q();
+        issue_k0();
+      }
+    }
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      const int qrow = e_qw0 + qb * 32 + n_e;
+      if constexpr (!OUT_F32) {
+        store_staged_rows<D>(rows[qb], lane_e,
+                             static_cast<uint16_t*>(a.o) + e_o_base + (e_qw0 + qb * 32) * q_stride,
+                             q_stride, e_Sq - (e_qw0 + qb * 32));
+      }
+      if (qrow >= e_Sq) continue;
+      if constexpr (OUT_F32) {
+        const float inv = lsum[qb] > 0.f ? 1.f / lsum[qb] : 0.f;
+        const size_t obase = e_o_base + qrow * q_stride;
+#pragma unroll
+        for (int db = 0; db < S::DBLK; ++db)
+#pragma unroll
+          for (int r4 = 0; r4 < 4; ++r4) {
+            const int d = db * 32 + 8 * r4 + 4 * h_e;
+            const f32x4 w = {o_acc[qb][db][4 * r4 + 0] * inv, o_acc[qb][db][4 * r4 + 1] * inv,
+                             o_acc[qb][db][4 * r4 + 2] * inv, o_acc[qb][db][4 * r4 + 3] * inv};
+            *reinterpret_cast<f32x4*>(static_cast<float*>(a.o) + obase + d) = w;
+          }
+      }
+      if (h_e == 0 && e_lse)
+        e_lse[qrow] = lsum[qb] > 0.f ? (m_run[qb] + log2f(lsum[qb])) * kLn2 : kNegInf;
+    }
+    if (next < 0) break;
   }
 }
 

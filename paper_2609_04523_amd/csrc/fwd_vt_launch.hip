@@ -1,5 +1,5 @@
 // fwd_vt_launch.hip -- the V^T pre-pass and the dense forward's VT
-// instantiations (bf16 O).
+// instantiations (bf16 O, persistent grid).
 #include "launch.hpp"
 #include "vt_pack_kernel.hpp"
 
@@ -8,7 +8,7 @@ namespace {
 
 template <int D, bool CAUSAL, bool POS>
 hipError_t go_vt(const FwdArgs& a, unsigned nblocks, hipStream_t st) {
-  hipLaunchKernelGGL((fwd_kernel<D, CAUSAL, false, kFwdQB, POS, false, kFwdVtWaves, false, true>),
+  hipLaunchKernelGGL((fwd_kernel<D, CAUSAL, false, kFwdQB, POS, false, kFwdVtWaves, false, true, true>),
                      dim3(nblocks), dim3(FwdShape<D, kFwdQB, kFwdVtWaves>::THREADS), 0, st, a);
   return hipGetLastError();
 }
@@ -30,6 +30,9 @@ hipError_t launch_fwd_vt(const FwdArgs& a, unsigned nblocks, int D, bool causal,
   p.Skv = a.Skv;
   p.vt_tiles = a.vt_tiles;
   p.Hkv = a.Hkv;
+  p.ctr = a.ctr;
+  p.ctr_init = (int)(nblocks / (unsigned)a.n_queues);
+  p.n_queues = a.n_queues;
   if (D == 128)
     hipLaunchKernelGGL(vt_pack_kernel<128>, dim3(pack_blocks), dim3(256), 0, st, p);
   else

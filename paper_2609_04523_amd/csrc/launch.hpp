@@ -24,8 +24,10 @@ hipError_t launch_fwd(const FwdArgs& a, unsigned nblocks, int D, bool causal, bo
                       bool pos_scale, hipStream_t st);
 
 // Dense forward through a V^T copy (bf16 O): the pack kernel writes
-// a.vt (pack_blocks = B * Hkv * vt_tiles workgroups), then the forward
-// (nblocks workgroups of kFwdVtWaves waves) reads V from it.
+// a.vt (pack_blocks = B * Hkv * vt_tiles workgroups) and sets a.ctr's
+// a.n_queues counters to nblocks / a.n_queues, then the forward (nblocks
+// persistent workgroups of kFwdVtWaves waves, a multiple of a.n_queues and
+// at most a.n_queues * a.per_queue) reads V from it.
 hipError_t launch_fwd_vt(const FwdArgs& a, unsigned nblocks, int D, bool causal, bool pos_scale,
                          unsigned pack_blocks, hipStream_t st);
 

@@ -7,6 +7,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <mutex>
 
 #include "../../include/mk_attn.h"
@@ -15,7 +16,7 @@
 
 namespace {
 
-constexpr int kVersion = 9;
+constexpr int kVersion = 10;
 constexpr int kComputeUnits = 256;    // MI355X
 constexpr int kLdsPerCu = 160 * 1024; // gfx950
 constexpr int kMaxParts = 1 << 20;    // decode parts per call
@@ -37,10 +38,18 @@ bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// V^T tiles of mk_attn_fwd_ws: ceil(Skv / 64) tiles of 64 * D bf16 per (b, kv head)
+// Workspace of mk_attn_fwd_ws: the V^T tiles, ceil(Skv / 64) tiles of
+// 64 * D bf16 per (b, kv head), then the persistent forward's work-item
+// counters (one per queue, 128 bytes apart).
+constexpr size_t kFwdCtrBytes = 8 * 128;
+
+size_t fwd_vt_tile_bytes(int B, int Hkv, int Skv, int D) {
+  return (size_t)B * Hkv * (size_t)((Skv + 63) / 64) * 64 * D * 2;
+}
+
 size_t fwd_vt_bytes(int B, int Hkv, int Skv, int D) {
   if (B < 1 || Hkv < 1 || Skv < 1 || (D != 64 && D != 128)) return 0;
-  return (size_t)B * Hkv * (size_t)((Skv + 63) / 64) * 64 * D * 2;
+  return fwd_vt_tile_bytes(B, Hkv, Skv, D) + kFwdCtrBytes;
 }
 
 // vt: V^T workspace of mk_attn_fwd_ws (bf16 O), or null for the transposing path
@@ -86,18 +95,29 @@ int fwd_impl(const void* q, const void* k, const void* v, void* o, float* lse, i
   a.tile_in_page = 0;
   a.vt = static_cast<const uint16_t*>(vt);
   a.vt_tiles = (Skv + 63) / 64;
+  a.ctr = nullptr;
+  a.n_queues = 1;
+  a.per_queue = 0;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool pos = scale > 0.f;
   if (vt) {
-    // workgroups of kFwdVtWaves waves, one per compute unit
+    // a persistent grid of kFwdVtWaves-wave workgroups, one per compute
+    // unit, over per-XCD queues of work items (one queue when the K/V
+    // heads do not divide evenly over the XCDs)
     const int BM_VT = mk::FwdShape<128, mk::kFwdQB, mk::kFwdVtWaves>::BM;
     const long long nq_vt = (Sq + BM_VT - 1) / BM_VT;
     a.n_qtiles = (int)nq_vt;
     a.xcd_gp = ((B * Hkv) % 8 == 0) ? mk::xcd_group_pairs(Hq / Hkv, (int)nq_vt, 1) : 0;
+    const long long items = nq_vt * B * Hq;
+    if (items > 0x7fffffffLL) return MK_ERR_SHAPE;
+    a.n_queues = a.xcd_gp > 0 ? 8 : 1;
+    a.per_queue = (int)(items / a.n_queues);
+    const long long per_q_grid = std::min<long long>(a.per_queue, kComputeUnits / a.n_queues);
+    a.ctr = reinterpret_cast<int*>(static_cast<char*>(vt) + fwd_vt_tile_bytes(B, Hkv, Skv, D));
     const long long pack_blocks = (long long)B * Hkv * a.vt_tiles;
     if (pack_blocks > 0x7fffffffLL) return MK_ERR_SHAPE;
-    const hipError_t e = mk::launch_fwd_vt(a, (unsigned)(nq_vt * B * Hq), D, causal, pos,
-                                           (unsigned)pack_blocks, st);
+    const hipError_t e = mk::launch_fwd_vt(a, (unsigned)(per_q_grid * a.n_queues), D, causal,
+                                           pos, (unsigned)pack_blocks, st);
     return e == hipSuccess ? MK_OK : MK_ERR_HIP;
   }
   const hipError_t e = mk::launch_fwd(a, (unsigned)nblocks, D, causal, out_f32, pos, st);
@@ -295,6 +315,9 @@ int mk_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o, flo
   a.tile_in_page = 0;
   a.vt = nullptr;
   a.vt_tiles = 0;
+  a.ctr = nullptr;
+  a.n_queues = 1;
+  a.per_queue = 0;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool pos = scale > 0.f;
   const hipError_t e = mk::launch_fwd_varlen(a, (unsigned)nblocks, D, causal, pos, st);
@@ -362,6 +385,9 @@ int mk_attn_fwd_ragged_paged(const void* q, const void* k_pages, const void* v_p
   a.tile_in_page = page_size % 64 == 0 ? 1 : 0;
   a.vt = nullptr;
   a.vt_tiles = 0;
+  a.ctr = nullptr;
+  a.n_queues = 1;
+  a.per_queue = 0;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool pos = scale > 0.f;
   const hipError_t e = mk::launch_fwd_ragged_paged(a, (unsigned)nblocks, D, causal, pos, st);

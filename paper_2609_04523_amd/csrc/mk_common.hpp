@@ -304,13 +304,14 @@ __device__ __forceinline__ int clamp_len(int len, int hi) {
 // Store x * acc^T as 32 bf16 rows of D values: acc[db][r] of lane
 // (n, h) = l % 32, l / 32 is element (row n, column db*32 + 8 (r/4) + 4 h
 // + r % 4).  The wave writes its rows to LDS at `stage` (32 rows x D bf16,
-// 16-byte chunks XOR-swizzled by row), then stores them 16 bytes per lane,
-// 16 (D = 128) or 8 (D = 64) lanes per row, row i at dst + i * stride
-// (elements); rows >= n_rows are not stored.  x is per lane (its row's).
+// 16-byte chunks XOR-swizzled by row) and reads them back 16 bytes per
+// lane, 16 (D = 128) or 8 (D = 64) lanes per row (stage_rows_t), then
+// stores them, row i at dst + i * stride (elements); rows >= n_rows are not
+// stored (store_staged_rows).  x is per lane (its row's).
 template <int D>
-__device__ __forceinline__ void store_rows_t(const f32x16 (&acc)[D / 32], float x,
+__device__ __forceinline__ void stage_rows_t(const f32x16 (&acc)[D / 32], float x,
                                              uint32_t stage, int n, int h, int lane,
-                                             uint16_t* dst, size_t stride, int n_rows) {
+                                             u32x4 (&rows)[D / 16]) {
   constexpr int CH = D / 8;  // 16-byte chunks per row
   constexpr int ROW_BYTES = D * 2;
   const int swz_w = n & (CH - 1);
@@ -332,9 +333,30 @@ __device__ __forceinline__ void store_rows_t(const f32x16 (&acc)[D / 32], float 
     const int row = i * ROWS_PER_READ + lane / CH;
     const int c = lane % CH;
     const uint32_t ad = stage + row * ROW_BYTES + ((c ^ (row & (CH - 1))) << 4);
-    const u32x4 v = *(const __attribute__((address_space(3))) u32x4*)(uintptr_t)ad;
-    if (row < n_rows) *reinterpret_cast<u32x4*>(dst + (size_t)row * stride + c * 8) = v;
+    rows[i] = *(const __attribute__((address_space(3))) u32x4*)(uintptr_t)ad;
   }
+}
+
+template <int D>
+__device__ __forceinline__ void store_staged_rows(const u32x4 (&rows)[D / 16], int lane,
+                                                  uint16_t* dst, size_t stride, int n_rows) {
+  constexpr int CH = D / 8;
+  constexpr int ROWS_PER_READ = 64 / CH;
+#pragma unroll
+  for (int i = 0; i < 32 / ROWS_PER_READ; ++i) {
+    const int row = i * ROWS_PER_READ + lane / CH;
+    const int c = lane % CH;
+    if (row < n_rows) *reinterpret_cast<u32x4*>(dst + (size_t)row * stride + c * 8) = rows[i];
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void store_rows_t(const f32x16 (&acc)[D / 32], float x,
+                                             uint32_t stage, int n, int h, int lane,
+                                             uint16_t* dst, size_t stride, int n_rows) {
+  u32x4 rows[D / 16];
+  stage_rows_t<D>(acc, x, stage, n, h, lane, rows);
+  store_staged_rows<D>(rows, lane, dst, stride, n_rows);
 }
 
 }  // namespace mk

@@ -30,6 +30,10 @@ struct VtPackArgs {
   uint16_t* vt;            // [B, Hkv, vt_tiles, 4, D, 16]
   const int* kv_seqlens;   // [B] or null (all Skv)
   int Skv, vt_tiles, Hkv;
+  // the forward's work-item counters (FwdArgs::ctr), n_queues of them, each
+  // set to ctr_init here, before the forward runs
+  int* ctr;
+  int ctr_init, n_queues;
 };
 
 // One workgroup per 64-key tile of one (b, kv head), B * Hkv * vt_tiles
@@ -50,6 +54,7 @@ __global__ __launch_bounds__(256) void vt_pack_kernel(VtPackArgs a) {
   const int L = a.kv_seqlens ? clamp_len(a.kv_seqlens[b], a.Skv) : a.Skv;
   const uint16_t* v = a.v + (size_t)bg * a.Skv * D;
   const int tid = threadIdx.x;
+  if (blockIdx.x == 0 && tid < a.n_queues) a.ctr[32 * tid] = a.ctr_init;
 #pragma unroll
   for (int i = tid; i < BN * CH; i += 256) {
     const int r = i / CH, c = i % CH;

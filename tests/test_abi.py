@@ -43,7 +43,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert mk.mk_attn_version() == 9
+    assert mk.mk_attn_version() == 10
     names = ["MK_OK", "MK_ERR_NULL", "MK_ERR_SHAPE", "MK_ERR_UNSUPPORTED", "MK_ERR_ALIGN",
              "MK_ERR_WORKSPACE", "MK_ERR_HIP", "MK_ERR_ARG", "MK_ERR_SCRATCH"]
     for code, name in enumerate(names):
@@ -90,10 +90,11 @@ def fwd_ws_rc(lib, *, q=P, k=P, v=P, o=P, lse=None, B=1, Hq=2, Hkv=1, Sq=8, Skv=
 
 
 def test_fwd_ws_workspace_bytes(lib):
-    # B * Hkv * ceil(Skv / 64) tiles of 64 keys x D bf16
-    assert mk.mk_attn_fwd_workspace_bytes(1, 8, 32768, 128) == 8 * 512 * 64 * 128 * 2
-    assert mk.mk_attn_fwd_workspace_bytes(2, 3, 65, 64) == 2 * 3 * 2 * 64 * 64 * 2
-    assert mk.mk_attn_fwd_workspace_bytes(4, 16, 1, 128) == 4 * 16 * 64 * 128 * 2
+    # B * Hkv * ceil(Skv / 64) tiles of 64 keys x D bf16, then 1 KiB of
+    # work-item counters
+    assert mk.mk_attn_fwd_workspace_bytes(1, 8, 32768, 128) == 8 * 512 * 64 * 128 * 2 + 1024
+    assert mk.mk_attn_fwd_workspace_bytes(2, 3, 65, 64) == 2 * 3 * 2 * 64 * 64 * 2 + 1024
+    assert mk.mk_attn_fwd_workspace_bytes(4, 16, 1, 128) == 4 * 16 * 64 * 128 * 2 + 1024
     for args in ((0, 1, 8, 128), (1, 0, 8, 128), (1, 1, 0, 128), (1, 1, 8, 96), (1, 1, 8, 0)):
         assert mk.mk_attn_fwd_workspace_bytes(*args) == 0
 

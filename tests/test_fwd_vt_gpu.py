@@ -3,7 +3,7 @@
 The workspace path forms the same products in the same order as
 mk_attn_fwd, only its V operand comes from a re-laid-out copy, so its O and
 LSE must equal mk_attn_fwd's bit for bit; mk_attn_fwd itself is held to the
-oracle by test_fwd_gpu.py, and two cases here go to the oracle directly.
+oracle by test_fwd_gpu.py, and three cases here go to the oracle directly.
 The copy's layout is checked against one built on the host from V."""
 import math
 import zlib
@@ -59,6 +59,13 @@ CASES = [
     ("s513_gqa8", 1, 16, 2, 513, 513, 128, True, None, None),
     ("scale_negative", 1, 4, 2, 190, 190, 128, True, None, -0.05),
     ("scale_zero_d64", 1, 2, 1, 150, 150, 64, True, None, 0.0),
+    # the persistent grid's queues: 8 (one per XCD) when B * Hkv is a
+    # multiple of 8, else 1; one item per queue; items without keys; more
+    # items than workgroups (taken from the other queues at the end)
+    ("xcd8_one_item_each", 1, 8, 8, 100, 100, 128, True, None, None),
+    ("xcd8_empty_sequences", 8, 8, 1, 300, 300, 128, True, [300, 0, 17, 256, 0, 1, 299, 64], None),
+    ("xcd8_many_items_d64", 2, 32, 4, 2000, 2000, 64, True, None, None),
+    ("one_queue_many_items", 3, 12, 3, 1100, 1100, 128, True, None, None),
 ]
 
 
@@ -72,7 +79,7 @@ def test_fwd_ws_bitwise_equals_fwd(case):
     assert_bitwise(name, o, lse, o_ref, lse_ref)
 
 
-@pytest.mark.parametrize("name", ["ragged_lens", "s1000_gqa4_d64"])
+@pytest.mark.parametrize("name", ["ragged_lens", "s1000_gqa4_d64", "xcd8_empty_sequences"])
 def test_fwd_ws_oracle_parity(name):
     case = next(c for c in CASES if c[0] == name)
     _, B, Hq, Hkv, Sq, Skv, D, causal, sl, scale = case
@@ -127,8 +134,23 @@ def test_fwd_ws_tile_layout(D, lens):
     q, k, v = workloads.prefill_inputs(B, Hq, Hkv, S, S, D, seed=77 + D)
     ws = ws_for(B, Hkv, S, D)
     both(q, k, v, causal=True, scale=D ** -0.5, kv_seqlens=lens, ws=ws)
-    got = ws.cpu().numpy().view(np.uint16).reshape(B, Hkv, (S + 63) // 64, 4, D, 16)
+    tiles = (S + 63) // 64
+    got = ws.cpu().numpy().view(np.uint16)[:B * Hkv * tiles * 64 * D]
+    got = got.reshape(B, Hkv, tiles, 4, D, 16)
     assert np.array_equal(got, expected_tiles(v, lens))
+
+
+@pytest.mark.parametrize("fill", [0x00, 0xFF, 0x7F])
+def test_fwd_ws_workspace_contents_do_not_matter(fill):
+    # the call sets up its own work-item counters: a workspace holding
+    # anything (here all bytes `fill`) gives the same result
+    B, Hq, Hkv, S, D = 2, 16, 4, 900, 128
+    q, k, v = workloads.prefill_inputs(B, Hq, Hkv, S, S, D, seed=4400 + fill)
+    ws = ws_for(B, Hkv, S, D)
+    ws.fill_(fill)
+    torch.cuda.synchronize()
+    o, lse, o_ref, lse_ref, _ = both(q, k, v, causal=True, scale=D ** -0.5, ws=ws)
+    assert_bitwise(f"fill_{fill}", o, lse, o_ref, lse_ref)
 
 
 def test_fwd_ws_reused_workspace_smaller_second_call():
