@@ -88,9 +88,10 @@ def summarize_trace(path: str, command: str, kernels=None) -> str:
     (the GPU-time share stays relative to all kernels of the run)."""
     import sqlite3
     db = sqlite3.connect(_find_db(path))
+    tags = _dispatch_grids(db)
     try:
-        rows = db.execute("select name, duration, grid_x / max(workgroup_x, 1) from kernels"
-                          ).fetchall()
+        rows = [(n, d, tags.get(i, w)) for i, n, d, w in db.execute(
+            "select dispatch_id, name, duration, grid_x / max(workgroup_x, 1) from kernels")]
     except sqlite3.OperationalError:  # a trace without launch geometry
         rows = [(n, d, 0) for n, d in db.execute("select name, duration from kernels")]
     # launches of one kernel with different grids (one kernel timed on two
@@ -102,7 +103,8 @@ def summarize_trace(path: str, command: str, kernels=None) -> str:
     for name, dur, wgs in rows:
         key = _short(name)
         if len(grids[key]) > 1:
-            key = f"{key} [{wgs} workgroups]"
+            key = (f"{key} [after a V^T copy of {wgs[1:]} tiles]" if isinstance(wgs, str)
+                   else f"{key} [{wgs} workgroups]")
         agg.setdefault(key, []).append(dur / 1e3)  # ns -> us
     total = sum(sum(v) for v in agg.values())
     if kernels:
@@ -119,14 +121,26 @@ def summarize_trace(path: str, command: str, kernels=None) -> str:
 
 def _dispatch_grids(db):
     """dispatch id -> workgroup count, from the trace tables of a run (empty
-    for databases without launch geometry)."""
+    for databases without launch geometry).  The persistent V^T forward
+    launches one workgroup per compute unit whatever the workload, so its
+    dispatches are told apart by the V^T copy made just before them: 'v'
+    and the pack kernel's workgroup count."""
     import sqlite3
     try:
-        rows = db.execute("select dispatch_id, grid_x / max(workgroup_x, 1) from kernels"
-                          ).fetchall()
+        rows = db.execute("select dispatch_id, name, grid_x / max(workgroup_x, 1) from kernels "
+                          "order by dispatch_id").fetchall()
     except sqlite3.OperationalError:
         return {}
-    return {d: int(w) for d, w in rows}
+    out, last_pack = {}, None
+    for d, name, w in rows:
+        short = _short(name)
+        if "vt_pack_kernel" in short:
+            last_pack = int(w)
+        if "fwd_kernel" in short and short.endswith("true, true>") and last_pack is not None:
+            out[d] = f"v{last_pack}"
+        else:
+            out[d] = int(w)
+    return out
 
 
 def _pmc_per_kernel(path: str, counter: str):
@@ -584,7 +598,7 @@ def main():
         # of launches right after warm-up launches of its own
         dec_ms = time_block(stream, decode, 50, args.decode_launches)
         log(f"[bench] decode leg: {dec_ms * 1e3:.1f} us over {args.decode_launches} launches")
-    for leg, cname, warm, n in (("c3", "c3_gqa_s8k_k2", 2, 10), ("c2", "c2_mha_s2k", 20, 100),
+    for leg, cname, warm, n in (("c3", "c3_gqa_s8k_k2", 10, 20), ("c2", "c2_mha_s2k", 20, 100),
                                 ("c1", "c1_mha_s128_d64", 20, 100)):
         if leg not in legs or cname == pcfg.name:
             continue
