@@ -1,12 +1,14 @@
 // fwd_kernel.hpp -- fused attention forward (prefill) for gfx950.
 //
-// One workgroup = 4 waves = BM query rows of one (batch, query head); wave w
-// owns QB blocks of 32 consecutive rows.  The workgroup streams the 64-key
-// K and V tiles of its KV head (hq / (Hq/Hkv)) from HBM straight into LDS
-// (LDS-DMA loads, double-buffered), up to the causal
-// diagonal, and keeps the softmax state and the output accumulator in
-// registers: online softmax, an exact rewrite of softmax(Q K^T * scale) V
-// folded tile by tile.
+// A work item = BM query rows (a q-tile) of one (batch, query head), taken
+// by one workgroup of WAVES waves (4; 8 on the V^T path); wave w owns QB
+// blocks of 32 consecutive rows.  The workgroup streams the 64-key K and V
+// tiles of its KV head (hq / (Hq/Hkv)) from HBM straight into LDS (LDS-DMA
+// loads, double-buffered), up to the causal diagonal, and keeps the softmax
+// state and the output accumulator in registers: online softmax, an exact
+// rewrite of softmax(Q K^T * scale) V folded tile by tile.  A workgroup
+// takes one item (its own index), or with PERSIST works through queues of
+// items.
 //
 // Orientation.  Scores are formed transposed, S^T = K Q^T, with K as the
 // MFMA A operand (rows = keys) and Q^T as the B operand (columns =
