@@ -107,7 +107,9 @@ int fwd_impl(const void* q, const void* k, const void* v, void* o, float* lse, i
     const int BM_VT = mk::FwdShape<128, mk::kFwdQB, mk::kFwdVtWaves>::BM;
     const long long nq_vt = (Sq + BM_VT - 1) / BM_VT;
     a.n_qtiles = (int)nq_vt;
-    a.xcd_gp = ((B * Hkv) % 8 == 0) ? mk::xcd_group_pairs(Hq / Hkv, (int)nq_vt, 1) : 0;
+    // groups of two pairs: an XCD's queue then starts with the longest
+    // q-tiles of both (its workgroups take items longest first)
+    a.xcd_gp = ((B * Hkv) % 8 == 0) ? 2 : 0;
     const long long items = nq_vt * B * Hq;
     if (items > 0x7fffffffLL) return MK_ERR_SHAPE;
     a.n_queues = a.xcd_gp > 0 ? 8 : 1;
