@@ -92,8 +92,12 @@ def summarize_trace(path: str, command: str, kernels=None) -> str:
     try:
         rows = [(n, d, tags.get(i, w)) for i, n, d, w in db.execute(
             "select dispatch_id, name, duration, grid_x / max(workgroup_x, 1) from kernels")]
-    except sqlite3.OperationalError:  # a trace without launch geometry
-        rows = [(n, d, 0) for n, d in db.execute("select name, duration from kernels")]
+    except sqlite3.OperationalError:
+        try:  # a trace without dispatch ids
+            rows = db.execute("select name, duration, grid_x / max(workgroup_x, 1) from kernels"
+                              ).fetchall()
+        except sqlite3.OperationalError:  # a trace without launch geometry
+            rows = [(n, d, 0) for n, d in db.execute("select name, duration from kernels")]
     # launches of one kernel with different grids (one kernel timed on two
     # workloads) get a row per workgroup count
     grids = {}

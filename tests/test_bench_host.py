@@ -106,6 +106,32 @@ def test_summarize_trace_splits_one_kernel_by_grid(tmp_path):
     assert small[2] == "2" and small[3] == "81.00"
 
 
+def test_summarize_trace_tells_persistent_launches_by_their_copy(tmp_path):
+    """The persistent forward launches 256 workgroups on every workload; its
+    launches are told apart by the V^T copy made just before each."""
+    pers = "void mk::fwd_kernel<128, true, false, 1, true, false, 8, false, true, true>(mk::FwdArgs)"
+    pack = "void mk::vt_pack_kernel<128>(mk::VtPackArgs)"
+    d = str(tmp_path / "p")
+    os.makedirs(d)
+    con = sqlite3.connect(os.path.join(d, "x_results.db"))
+    con.execute("create table kernels (dispatch_id integer, name text, duration integer, "
+                "grid_x integer, workgroup_x integer)")
+    con.executemany("insert into kernels values (?, ?, ?, ?, ?)",
+                    [(1, pack, 25_000, 4096 * 256, 256), (2, pers, 7_000_000, 256 * 512, 512),
+                     (3, pack, 15_000, 2048 * 256, 256), (4, pers, 1_000_000, 256 * 512, 512),
+                     (5, pack, 26_000, 4096 * 256, 256), (6, pers, 7_200_000, 256 * 512, 512)])
+    con.commit()
+    con.close()
+    out = bench.summarize_trace(d, "cmd", ["fwd_kernel"])
+    rows = {l.split("`")[1]: [c.strip() for c in l.split("|")]
+            for l in out.splitlines() if l.startswith("| `")}
+    name = "mk::fwd_kernel<128, true, false, 1, true, false, 8, false, true, true>"
+    assert set(rows) == {f"{name} [after a V^T copy of 4096 tiles]",
+                         f"{name} [after a V^T copy of 2048 tiles]"}
+    assert rows[f"{name} [after a V^T copy of 4096 tiles]"][2:4] == ["2", "7100.00"]
+    assert rows[f"{name} [after a V^T copy of 2048 tiles]"][2:4] == ["1", "1000.00"]
+
+
 def test_summarize_pmc_splits_one_kernel_by_grid(tmp_path):
     """'name@N' selects the launches of a kernel with N workgroups, so one
     forward kernel timed on two workloads gets one traffic figure each."""
