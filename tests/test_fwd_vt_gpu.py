@@ -66,6 +66,10 @@ CASES = [
     ("xcd8_empty_sequences", 8, 8, 1, 300, 300, 128, True, [300, 0, 17, 256, 0, 1, 299, 64], None),
     ("xcd8_many_items_d64", 2, 32, 4, 2000, 2000, 64, True, None, None),
     ("one_queue_many_items", 3, 12, 3, 1100, 1100, 128, True, None, None),
+    # long sequences: many items per workgroup, items taken across XCDs,
+    # the other head dim and the non-causal instantiation
+    ("long_d64_s16k", 1, 16, 8, 16384, 16384, 64, True, None, None),
+    ("long_noncausal_s8k", 1, 16, 8, 8192, 8192, 128, False, None, None),
 ]
 
 
